@@ -1,0 +1,48 @@
+/*
+ * metro_ops.h -- single kernels of libmetro.so's forward pass, exported so
+ * that each can be checked on its own against a CPU reference.  The model
+ * entry points in metro.h are what a serving loop calls; these run one step
+ * of it on caller-owned device buffers.
+ *
+ * All pointers are device pointers on the current HIP device; work is
+ * enqueued on `stream` (a hipStream_t, NULL = default stream).  Return value
+ * and metro_last_error() as in metro.h; a launch failure returns METRO_E_HIP.
+ */
+#ifndef METRO_OPS_H
+#define METRO_OPS_H
+
+#include <stdint.h>
+
+#include "metro.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Projection GEMM of the Llama block (QKV, O, gate/up, down, LM head):
+ *   acc[m, n] = sum_k X[m, k] * W[n, k]   (bf16 operands, fp32 accumulation)
+ * X: bf16 [M, ldx] row-major, the first Kp columns used; W: bf16 [N, Kp];
+ * Kp % 128 == 0, N % 32 == 0.  epilogue:
+ *   0  out_f32[m*ldo + n]  = acc[m, n]
+ *   1  out_f32[m*ldo + n] += acc[m, n]                       (residual add)
+ *   2  W rows come in blocks of 32 = 16 gate rows then 16 up rows of the same
+ *      features; out_bf16[m*ldo + j] = bf16(silu(gate_j) * up_j), j < N/2
+ *      (SwiGLU, Shazeer 2020).
+ * Errors: E_INVAL for shapes outside these rules or a NULL operand. */
+metro_status metro_op_gemm(const uint16_t* X, int32_t ldx, const uint16_t* W, int32_t Kp, int32_t M, int32_t N,
+                           int32_t epilogue, float* out_f32, uint16_t* out_bf16, int32_t ldo, void* stream);
+
+/* RMSNorm (Zhang & Sennrich 2019): h[r, :] = bf16(x[r, :] / sqrt(mean(x[r, :]^2)
+ * + eps) * g), x fp32 [rows, d], g bf16 [d], h bf16 [rows, d], d % 4 == 0. */
+metro_status metro_op_rmsnorm(const float* x, const uint16_t* g, float eps, uint16_t* h, int32_t rows, int32_t d,
+                              void* stream);
+
+/* Greedy choice: out[r] = lowest index of the maximum of logits[r, :] (fp32
+ * [rows, vocab], vocab % 4 == 0); NaN values are skipped, -1 if none is left. */
+metro_status metro_op_argmax(const float* logits, int32_t rows, int32_t vocab, int32_t* out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* METRO_OPS_H */

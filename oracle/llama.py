@@ -7,6 +7,7 @@ time, with no batching, blocking or fusion.
 
 from __future__ import annotations
 
+import math
 from dataclasses import dataclass
 
 import numpy as np
@@ -79,8 +80,8 @@ def rope_rotate(u: np.ndarray, positions: np.ndarray, base: float) -> np.ndarray
     i = np.arange(half, dtype=np.float64)
     theta = base ** (-2.0 * i / hd)
     phi = np.asarray(positions, dtype=np.float64)[:, None] * theta[None, :]
-    c = np.cos(phi)[:, None, :]
-    s = np.sin(phi)[:, None, :]
+    c = np.cos(phi)[:, None, :].astype(u.dtype)
+    s = np.sin(phi)[:, None, :].astype(u.dtype)
     a = u[..., :half]
     b = u[..., half:]
     return np.concatenate([a * c - b * s, a * s + b * c], axis=-1)
@@ -107,10 +108,10 @@ def causal_gqa_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray,
     ctx, nkv, _ = k.shape
     group = nq // nkv
     visible = np.arange(ctx)[None, :] <= np.asarray(q_pos)[:, None]
-    out = np.empty((n, nq, hd), dtype=np.float64)
+    out = np.empty((n, nq, hd), dtype=q.dtype)
     for j in range(nq):
         kvh = j // group
-        s = (q[:, j, :] @ k[:, kvh, :].T) / np.sqrt(hd)
+        s = (q[:, j, :] @ k[:, kvh, :].T) / math.sqrt(hd)
         s = np.where(visible, s, -np.inf)
         out[:, j, :] = softmax_rows(s) @ v[:, kvh, :]
     return out
@@ -140,11 +141,15 @@ class ContiguousKV:
 
     def __init__(self, shape: LlamaShape):
         self.shape = shape
-        self.k = [np.zeros((0, shape.n_kv_heads, shape.head_dim)) for _ in range(shape.n_layers)]
-        self.v = [np.zeros((0, shape.n_kv_heads, shape.head_dim)) for _ in range(shape.n_layers)]
+        self.k = [None] * shape.n_layers
+        self.v = [None] * shape.n_layers
         self.length = 0
 
     def write(self, layer: int, positions: np.ndarray, k: np.ndarray, v: np.ndarray) -> None:
+        if self.k[layer] is None:
+            assert positions[0] == 0, "positions must append"
+            self.k[layer], self.v[layer] = k.copy(), v.copy()
+            return
         assert positions[0] == self.k[layer].shape[0], "positions must append"
         self.k[layer] = np.concatenate([self.k[layer], k], axis=0)
         self.v[layer] = np.concatenate([self.v[layer], v], axis=0)
@@ -168,13 +173,17 @@ class PagedKV:
     def __init__(self, shape: LlamaShape, n_pages: int, page: int, free_pages):
         self.shape = shape
         self.page = page
-        self.pool = np.zeros((n_pages, shape.n_layers, 2, page, shape.n_kv_heads, shape.head_dim))
+        self.pool = None  # allocated on first write, in the arithmetic dtype
+        self.n_pages = n_pages
         self.free = list(free_pages)
         self.block_table: list[int] = []
         self.filled = [0] * shape.n_layers
         self.length = 0
 
     def write(self, layer: int, positions: np.ndarray, k: np.ndarray, v: np.ndarray) -> None:
+        if self.pool is None:
+            S = self.shape
+            self.pool = np.zeros((self.n_pages, S.n_layers, 2, self.page, S.n_kv_heads, S.head_dim), dtype=k.dtype)
         for t, p in enumerate(positions):
             b, off = divmod(int(p), self.page)
             while b >= len(self.block_table):
@@ -211,11 +220,17 @@ class OracleModel:
     ``wgate [F, d]``, ``wup [F, d]``, ``wdown [d, F]`` (all ``[out, in]``).
     Arrays of dtype uint16 are read as bfloat16 bit patterns; any other dtype is
     taken as real values (rounded to bf16 when ``quantize``).
+
+    ``dtype`` is the arithmetic: float64 (the oracle) or float32, the same
+    function evaluated the way an fp32-accumulating implementation would; the
+    difference between the two measures how far legitimate fp32 rounding alone
+    moves the result (the noise floor a tolerance must allow for).
     """
 
-    def __init__(self, shape: LlamaShape, weights: dict, quantize: bool = True):
+    def __init__(self, shape: LlamaShape, weights: dict, quantize: bool = True, dtype=np.float64):
         self.shape = shape
         self.quantize = quantize
+        self.dtype = np.dtype(dtype)
 
         def load(a):
             a = np.asarray(a)
@@ -229,8 +244,9 @@ class OracleModel:
         assert len(self.layers) == shape.n_layers
 
     def q(self, x):
-        """The bf16 storage points of the precision contract (identity if not quantize)."""
-        return bf16_round(x) if self.quantize else x
+        """The bf16 storage points of the precision contract (identity if not
+        quantize), returned in the arithmetic dtype."""
+        return (bf16_round(x) if self.quantize else np.asarray(x)).astype(self.dtype, copy=False)
 
     def new_cache(self) -> ContiguousKV:
         return ContiguousKV(self.shape)

@@ -1,0 +1,261 @@
+// Row-wise and elementwise kernels of the forward pass (gfx950, wave64):
+// embedding gather, RMSNorm, RoPE + paged KV write, row gather, greedy argmax,
+// plus weight initialisation and page copy used by the runtime.
+#include "common.h"
+#include "kernels.h"
+
+namespace metro {
+
+// ---------------------------------------------------------------------------
+// Embedding gather: x[t, :] = fp32(E[tok[t], :]).  One block per token.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void embed_kernel(const int32_t* __restrict__ tok,
+                                                    const uint16_t* __restrict__ E, int vocab, int d,
+                                                    float* __restrict__ x) {
+  const int t = blockIdx.x;
+  const int id = tok[t];
+  float* xr = x + static_cast<size_t>(t) * d;
+  if (id < 0 || id >= vocab) {
+    for (int i = threadIdx.x; i < d; i += blockDim.x) xr[i] = __builtin_nanf("");
+    return;
+  }
+  const uint4* er = reinterpret_cast<const uint4*>(E + static_cast<size_t>(id) * d);
+  for (int i = threadIdx.x; i < d / 8; i += blockDim.x) {
+    uint4 w = er[i];
+    float4 a = make_float4(lo_bf16(w.x), hi_bf16(w.x), lo_bf16(w.y), hi_bf16(w.y));
+    float4 b = make_float4(lo_bf16(w.z), hi_bf16(w.z), lo_bf16(w.w), hi_bf16(w.w));
+    reinterpret_cast<float4*>(xr)[2 * i] = a;
+    reinterpret_cast<float4*>(xr)[2 * i + 1] = b;
+  }
+}
+
+hipError_t launch_embed(const int32_t* tok, const uint16_t* embed, int vocab, int d, float* x, int T,
+                        hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  hipLaunchKernelGGL(embed_kernel, dim3(T), dim3(256), 0, s, tok, embed, vocab, d, x);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// RMSNorm: h = bf16(x * rsqrt(mean(x^2) + eps) * g).  One block per row.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ x, int ldx,
+                                                      const uint16_t* __restrict__ g, float eps,
+                                                      uint16_t* __restrict__ h, int ldh, int d) {
+  const int r = blockIdx.x;
+  const float4* xr = reinterpret_cast<const float4*>(x + static_cast<size_t>(r) * ldx);
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d / 4; i += 256) {
+    float4 v = xr[i];
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  ss = wave_sum(ss);
+  __shared__ float red[4];
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float tot = (red[0] + red[1]) + (red[2] + red[3]);
+  const float inv = rsqrtf(tot / static_cast<float>(d) + eps);
+  const uint2* gr = reinterpret_cast<const uint2*>(g);
+  uint2* hr = reinterpret_cast<uint2*>(h + static_cast<size_t>(r) * ldh);
+  for (int i = threadIdx.x; i < d / 4; i += 256) {
+    float4 v = xr[i];
+    uint2 gw = gr[i];
+    uint2 o;
+    o.x = pack_bf16x2(v.x * inv * lo_bf16(gw.x), v.y * inv * hi_bf16(gw.x));
+    o.y = pack_bf16x2(v.z * inv * lo_bf16(gw.y), v.w * inv * hi_bf16(gw.y));
+    hr[i] = o;
+  }
+}
+
+hipError_t launch_rmsnorm(const float* x, int ldx, const uint16_t* g, float eps, uint16_t* h, int ldh, int rows,
+                          int d, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(rmsnorm_kernel, dim3(rows), dim3(256), 0, s, x, ldx, g, eps, h, ldh, d);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// RoPE on q and k (rotate-half pairs (i, i + hd/2)), bf16 rounding, and the
+// write of k and v into their page slot.  One block per token.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void rope_kv_kernel(const float* __restrict__ qkv, int nq, int nkv, int hd,
+                                                      const int32_t* __restrict__ pos,
+                                                      const int32_t* __restrict__ slot,
+                                                      const float2* __restrict__ rope, uint16_t* __restrict__ q,
+                                                      uint16_t* __restrict__ kv) {
+  const int t = blockIdx.x;
+  const int half = hd / 2;
+  const int width = (nq + 2 * nkv) * hd;
+  const float* row = qkv + static_cast<size_t>(t) * width;
+  const float2* cs = rope + static_cast<size_t>(pos[t]) * half;
+  const int sl = slot[t];
+  const int page = sl / kPage, off = sl % kPage;
+  // rotated heads: nq query heads then nkv key heads, hd/2 pairs each
+  const int n_pairs = (nq + nkv) * half;
+  for (int i = threadIdx.x; i < n_pairs; i += blockDim.x) {
+    const int head = i / half, j = i % half;
+    const float a = row[head * hd + j], b = row[head * hd + j + half];
+    const float2 c = cs[j];
+    const float ra = a * c.x - b * c.y;
+    const float rb = a * c.y + b * c.x;
+    if (head < nq) {
+      uint16_t* qr = q + static_cast<size_t>(t) * nq * hd + head * hd;
+      qr[j] = f32_to_bf16(ra);
+      qr[j + half] = f32_to_bf16(rb);
+    } else {
+      uint16_t* kr = kv + kv_offset(page, 0, nkv, head - nq, off, hd, 0);
+      kr[j] = f32_to_bf16(ra);
+      kr[j + half] = f32_to_bf16(rb);
+    }
+  }
+  const float* vr = row + (nq + nkv) * hd;
+  for (int i = threadIdx.x; i < nkv * hd; i += blockDim.x) {
+    const int head = i / hd, dd = i % hd;
+    kv[kv_offset(page, 1, nkv, head, off, hd, dd)] = f32_to_bf16(vr[i]);
+  }
+}
+
+hipError_t launch_rope_kv(const float* qkv, int T, int nq, int nkv, int hd, const int32_t* pos,
+                          const int32_t* slot, const float2* rope, uint16_t* q, uint16_t* kv_layer,
+                          hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  hipLaunchKernelGGL(rope_kv_kernel, dim3(T), dim3(256), 0, s, qkv, nq, nkv, hd, pos, slot, rope, q, kv_layer);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Row gather (the last position of each prefill item).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void gather_rows_kernel(const float* __restrict__ x, int d,
+                                                          const int32_t* __restrict__ rows,
+                                                          float* __restrict__ out) {
+  const float4* src = reinterpret_cast<const float4*>(x + static_cast<size_t>(rows[blockIdx.x]) * d);
+  float4* dst = reinterpret_cast<float4*>(out + static_cast<size_t>(blockIdx.x) * d);
+  for (int i = threadIdx.x; i < d / 4; i += blockDim.x) dst[i] = src[i];
+}
+
+hipError_t launch_gather_rows(const float* x, int d, const int32_t* rows, int n, float* out, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(gather_rows_kernel, dim3(n), dim3(256), 0, s, x, d, rows, out);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Greedy argmax over fp32 logits: lowest index among the maxima, NaN skipped.
+// One block of 1024 threads per row.
+// ---------------------------------------------------------------------------
+struct ArgBest {
+  float v;
+  int i;
+};
+
+__device__ __forceinline__ ArgBest arg_better(ArgBest a, ArgBest b) {
+  if (b.i < 0) return a;
+  if (a.i < 0) return b;
+  if (b.v > a.v || (b.v == a.v && b.i < a.i)) return b;
+  return a;
+}
+
+__global__ __launch_bounds__(1024) void argmax_kernel(const float* __restrict__ logits, int vocab,
+                                                      int32_t* __restrict__ out) {
+  const float4* row = reinterpret_cast<const float4*>(logits + static_cast<size_t>(blockIdx.x) * vocab);
+  ArgBest b{0.f, -1};
+  for (int j = threadIdx.x; j < vocab / 4; j += 1024) {
+    const float4 v = row[j];
+    const float e[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (e[k] == e[k] && (b.i < 0 || e[k] > b.v)) b = ArgBest{e[k], 4 * j + k};
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    ArgBest other{__shfl_xor(b.v, o, kWave), __shfl_xor(b.i, o, kWave)};
+    b = arg_better(b, other);
+  }
+  __shared__ float sv[16];
+  __shared__ int si[16];
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    sv[w] = b.v;
+    si[w] = b.i;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    ArgBest r{sv[0], si[0]};
+    for (int k = 1; k < 16; ++k) r = arg_better(r, ArgBest{sv[k], si[k]});
+    out[blockIdx.x] = r.i;
+  }
+}
+
+hipError_t launch_argmax(const float* logits, int vocab, int rows, int32_t* out, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(argmax_kernel, dim3(rows), dim3(1024), 0, s, logits, vocab, out);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Weight initialisation: SplitMix64 (Steele, Lea & Flood 2014) as a
+// counter-based hash of (key, element index) -> two uniforms -> Box-Muller
+// (one normal per element) -> 0.02 * z -> bf16.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint64_t splitmix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+  return z ^ (z >> 31);
+}
+
+__global__ __launch_bounds__(256) void init_normal_kernel(uint16_t* __restrict__ dst, int64_t ld, int rows,
+                                                          int cols, int row_block, int row_shift, uint64_t key) {
+  const int64_t n = static_cast<int64_t>(rows) * cols;
+  for (int64_t e = blockIdx.x * 256ll + threadIdx.x; e < n; e += static_cast<int64_t>(gridDim.x) * 256) {
+    const int r = static_cast<int>(e / cols), c = static_cast<int>(e % cols);
+    const uint64_t h = splitmix64(key + static_cast<uint64_t>(e + 1) * 0x9e3779b97f4a7c15ull);
+    const float u1 = (static_cast<float>(h >> 40) + 1.0f) * (1.0f / 16777216.0f);  // (0, 1]
+    const float u2 = static_cast<float>((h >> 16) & 0xffffffull) * (1.0f / 16777216.0f);  // [0, 1)
+    const float z = sqrtf(-2.0f * logf(u1)) * cosf(6.283185307179586f * u2);
+    const int64_t pr = static_cast<int64_t>(r / 16) * row_block + row_shift + (r % 16);
+    dst[pr * ld + c] = f32_to_bf16(0.02f * z);
+  }
+}
+
+hipError_t launch_init_normal(uint16_t* dst, int64_t ld, int rows, int cols, int row_block, int row_shift,
+                              uint64_t key, hipStream_t s) {
+  const int64_t n = static_cast<int64_t>(rows) * cols;
+  const int64_t blocks = (n + 255) / 256;
+  const int grid = static_cast<int>(blocks < 65536 ? blocks : 65536);
+  hipLaunchKernelGGL(init_normal_kernel, dim3(grid), dim3(256), 0, s, dst, ld, rows, cols, row_block, row_shift,
+                     key);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void fill_bf16_kernel(uint16_t* __restrict__ dst, int64_t n, uint16_t v) {
+  for (int64_t e = blockIdx.x * 256ll + threadIdx.x; e < n; e += static_cast<int64_t>(gridDim.x) * 256) dst[e] = v;
+}
+
+hipError_t launch_fill_bf16(uint16_t* dst, int64_t n, uint16_t value, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = (n + 255) / 256;
+  hipLaunchKernelGGL(fill_bf16_kernel, dim3(static_cast<int>(blocks < 65536 ? blocks : 65536)), dim3(256), 0, s,
+                     dst, n, value);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Page copy across all layers (partial last page of a forked prefix).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void page_copy_kernel(uint16_t* __restrict__ pool, int64_t layer_stride,
+                                                        int64_t page_elems, int src, int dst) {
+  uint16_t* base = pool + static_cast<size_t>(blockIdx.x) * layer_stride;
+  const uint4* s = reinterpret_cast<const uint4*>(base + static_cast<size_t>(src) * page_elems);
+  uint4* d = reinterpret_cast<uint4*>(base + static_cast<size_t>(dst) * page_elems);
+  for (int64_t i = threadIdx.x; i < page_elems / 8; i += 256) d[i] = s[i];
+}
+
+hipError_t launch_page_copy(uint16_t* pool, int64_t layer_stride, int64_t page_elems, int layers, int src,
+                            int dst, hipStream_t s) {
+  hipLaunchKernelGGL(page_copy_kernel, dim3(layers), dim3(256), 0, s, pool, layer_stride, page_elems, src, dst);
+  return hipGetLastError();
+}
+
+}  // namespace metro

@@ -1,0 +1,86 @@
+// Host-side launchers of the gfx950 kernels used by the runtime.
+// Shapes are checked by the runtime before any launch; the launchers assume
+// them (see each kernel's comment for what it requires).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace metro {
+
+// --- elementwise / row kernels (elementwise.hip) ---------------------------
+
+// x[t, :] = E[tok[t], :] as fp32; a token outside [0, vocab) gives a NaN row.
+hipError_t launch_embed(const int32_t* tok, const uint16_t* embed, int vocab, int d, float* x, int T,
+                        hipStream_t s);
+
+// h[r, :] = bf16(x[r, :] * rsqrt(mean(x[r, :]^2) + eps) * g); d % 4 == 0.
+hipError_t launch_rmsnorm(const float* x, int ldx, const uint16_t* g, float eps, uint16_t* h, int ldh, int rows,
+                          int d, hipStream_t s);
+
+// RoPE (rotate-half) on q and k of qkv [T, (nq+2nkv)*hd] fp32 at positions
+// pos[t]; q -> bf16 [T, nq*hd]; k, v -> bf16 into the KV slot slot[t]
+// (page*16 + offset) of this layer's slab.  rope is [max_pos][hd/2] (cos, sin).
+hipError_t launch_rope_kv(const float* qkv, int T, int nq, int nkv, int hd, const int32_t* pos,
+                          const int32_t* slot, const float2* rope, uint16_t* q, uint16_t* kv_layer,
+                          hipStream_t s);
+
+// out[i, :] = x[rows[i], :]
+hipError_t launch_gather_rows(const float* x, int d, const int32_t* rows, int n, float* out, hipStream_t s);
+
+// out[r] = lowest index of the maximum of logits[r, :]; -1 if the row has no
+// non-NaN value.
+hipError_t launch_argmax(const float* logits, int vocab, int rows, int32_t* out, hipStream_t s);
+
+// Random initialisation of one logical weight tensor [rows, cols] into a
+// packed matrix with row stride ld: logical row r goes to packed row
+// map(r) = (r / 16) * row_block + row_shift + r % 16.  Values are
+// 0.02 * N(0, 1) from a SplitMix64-keyed Box-Muller draw, rounded to bf16.
+hipError_t launch_init_normal(uint16_t* dst, int64_t ld, int rows, int cols, int row_block, int row_shift,
+                              uint64_t key, hipStream_t s);
+hipError_t launch_fill_bf16(uint16_t* dst, int64_t n, uint16_t value, hipStream_t s);
+
+// Copy page src to page dst in every layer (page_elems bf16 per layer).
+hipError_t launch_page_copy(uint16_t* pool, int64_t layer_stride, int64_t page_elems, int layers, int src,
+                            int dst, hipStream_t s);
+
+// --- GEMMs (gemm.hip) -------------------------------------------------------
+
+enum GemmEpilogue {
+  kEpiStoreF32 = 0,  // out_f32[m, n] = acc
+  kEpiAddF32 = 1,    // out_f32[m, n] += acc   (residual stream)
+  kEpiSwiGLU = 2,    // W rows interleaved in blocks of 16 (gate, up):
+                     // out_bf16[m, j] = bf16(silu(gate_j) * up_j), N = 2 * F
+};
+
+// Y = X[M, Kp] (bf16, row stride ldx) x W[N, Kp]^T (bf16, packed row stride
+// Kp, Kp % 128 == 0, N % 16 == 0), fp32 accumulation, then the epilogue.
+// ldo is the row stride of the output in elements.
+hipError_t launch_gemm(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, int epilogue,
+                       float* out_f32, uint16_t* out_bf16, int ldo, hipStream_t s);
+
+// --- attention (attention.hip) ---------------------------------------------
+
+struct AttnArgs {
+  const uint16_t* q;        // [rows_total, nq, hd] bf16 (row = query token)
+  const uint16_t* kv;       // this layer's slab of the KV pool
+  const int32_t* work;      // [n_work][2]: (row, split)
+  const int32_t* row_ctx;   // [rows]: keys visible to the row (0 .. ctx-1)
+  const int32_t* row_qrow;  // [rows]: row of q / out for this row
+  const int32_t* row_bt;    // [rows]: offset of the row's block table in bt
+  const int32_t* row_work;  // [rows]: first work item of the row
+  const int32_t* row_nsplit;// [rows]
+  const int32_t* bt;        // block tables
+  float* part;              // [n_work][nkv][group][hd + 2] fp32 partials
+  uint16_t* out;            // [rows_total, nq*hd] bf16
+  int n_work, rows, nq, nkv, hd, pages_per_split;
+  float scale;              // 1/sqrt(hd)
+};
+
+// Paged GQA attention, one work item = (row, split of pages_per_split pages)
+// x one kv head; rows with one split write out directly, others write
+// partials that launch_attn_combine merges.
+hipError_t launch_attn_paged(const AttnArgs& a, hipStream_t s);
+hipError_t launch_attn_combine(const AttnArgs& a, hipStream_t s);
+
+}  // namespace metro

@@ -1,0 +1,240 @@
+"""ctypes binding of libmetro.so (include/metro.h, include/metro_ops.h).
+
+Argument marshalling only: every step of the forward pass runs in the HIP
+library.  PyTorch serves as the source of device buffers (``tensor.data_ptr()``)
+and of the current HIP stream.  Importing this module raises ImportError when
+the library has not been built -- there is no fallback.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmetro.so")
+if not os.path.exists(_LIB_PATH):
+    raise ImportError(f"{_LIB_PATH} is not built; run `python -m paper_2411_03519_amd.build`")
+lib = ctypes.CDLL(_LIB_PATH)
+
+ABI_VERSION = 1
+
+STATUS = {0: "METRO_OK", -1: "METRO_E_INVAL", -2: "METRO_E_NOMEM", -3: "METRO_E_NOPAGES", -4: "METRO_E_SEQ",
+          -5: "METRO_E_CAPACITY", -6: "METRO_E_HIP"}
+
+WEIGHT_ID = {"embed": 0, "final_norm": 1, "lm_head": 2, "attn_norm": 3, "wq": 4, "wk": 5, "wv": 6, "wo": 7,
+             "ffn_norm": 8, "wgate": 9, "wup": 10, "wdown": 11}
+
+EPI_STORE_F32, EPI_ADD_F32, EPI_SWIGLU = 0, 1, 2
+
+KERNEL_CLASS = {"embed": 0, "rmsnorm": 1, "gemm_qkv": 2, "rope_kv": 3, "attention": 4, "attn_combine": 5,
+                "gemm_o": 6, "gemm_gate_up": 7, "gemm_down": 8, "lm_head": 9, "argmax": 10}
+PHASE = {"any": 0, "prefill": 1, "decode": 2}
+
+
+class Config(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("ffn_dim", ctypes.c_int32),
+                ("vocab", ctypes.c_int32), ("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float),
+                ("page_size", ctypes.c_int32), ("max_batch", ctypes.c_int32), ("max_tokens", ctypes.c_int32),
+                ("max_context", ctypes.c_int32), ("max_seqs", ctypes.c_int32), ("kv_pool_bytes", ctypes.c_int64)]
+
+
+class ModelInfo(ctypes.Structure):
+    _fields_ = [("weight_bytes", ctypes.c_int64), ("scratch_bytes", ctypes.c_int64),
+                ("kv_pool_bytes", ctypes.c_int64), ("kv_bytes_per_token", ctypes.c_int64),
+                ("n_pages", ctypes.c_int32), ("free_pages", ctypes.c_int32), ("open_seqs", ctypes.c_int32),
+                ("device", ctypes.c_int32)]
+
+
+_vp, _i32, _i64, _u64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64
+_SIGS = {
+    "metro_abi_version": (_i32, []),
+    "metro_last_error": (ctypes.c_char_p, []),
+    "metro_status_name": (ctypes.c_char_p, [_i32]),
+    "metro_create_model": (_i32, [ctypes.POINTER(Config), _u64, ctypes.POINTER(_vp)]),
+    "metro_destroy_model": (None, [_vp]),
+    "metro_load_weight": (_i32, [_vp, _i32, _i32, _vp, _i64]),
+    "metro_model_get_info": (_i32, [_vp, ctypes.POINTER(ModelInfo)]),
+    "metro_seq_open": (_i32, [_vp, ctypes.POINTER(_i64)]),
+    "metro_seq_fork": (_i32, [_vp, _i64, _i32, _vp, ctypes.POINTER(_i64)]),
+    "metro_seq_close": (_i32, [_vp, _i64]),
+    "metro_seq_length": (_i32, [_vp, _i64, ctypes.POINTER(_i32)]),
+    "metro_seq_pages": (_i32, [_vp, _i64, _vp, _i32, ctypes.POINTER(_i32)]),
+    "metro_prefill_chunk": (_i32, [_vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "metro_decode_step": (_i32, [_vp, _i32, _vp, _vp, _vp, _vp, _vp]),
+    "metro_profile_start": (_i32, [_vp, _i32, _i32]),
+    "metro_profile_stop": (_i32, [_vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_i64)]),
+    "metro_op_gemm": (_i32, [_vp, _i32, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _i32, _vp]),
+    "metro_op_rmsnorm": (_i32, [_vp, _vp, ctypes.c_float, _vp, _i32, _i32, _vp]),
+    "metro_op_argmax": (_i32, [_vp, _i32, _i32, _vp, _vp]),
+}
+for _name, (_res, _args) in _SIGS.items():
+    _f = getattr(lib, _name)
+    _f.restype = _res
+    _f.argtypes = _args
+
+if lib.metro_abi_version() != ABI_VERSION:
+    raise ImportError(f"libmetro.so ABI {lib.metro_abi_version()} != binding ABI {ABI_VERSION}")
+
+
+class MetroError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+        self.name = STATUS.get(status, str(status))
+
+
+def check(status: int) -> None:
+    if status != 0:
+        raise MetroError(status, lib.metro_last_error().decode())
+
+
+def _ptr(t) -> int | None:
+    """Device address of a torch tensor (None passes NULL)."""
+    if t is None:
+        return None
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError("expected a contiguous device tensor")
+    return t.data_ptr()
+
+
+def _stream(stream) -> int | None:
+    if stream is not None:
+        return stream if isinstance(stream, int) else stream.cuda_stream
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _host_i64(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int64))
+
+
+def _host_i32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+class Model:
+    """One Llama-style model on the current HIP device (see metro_create_model)."""
+
+    def __init__(self, shape: dict, *, max_batch: int, max_tokens: int, max_context: int, max_seqs: int | None = None,
+                 kv_pool_bytes: int = 0, seed: int = 0):
+        self.shape = dict(shape)
+        cfg = Config(n_layers=shape["n_layers"], d_model=shape["d_model"], n_heads=shape["n_heads"],
+                     n_kv_heads=shape["n_kv_heads"], head_dim=shape["head_dim"], ffn_dim=shape["ffn_dim"],
+                     vocab=shape["vocab"], rope_base=shape["rope_base"], rms_eps=shape["rms_eps"], page_size=16,
+                     max_batch=max_batch, max_tokens=max_tokens, max_context=max_context,
+                     max_seqs=max_seqs if max_seqs is not None else max(max_batch, 1),
+                     kv_pool_bytes=kv_pool_bytes)
+        h = _vp()
+        check(lib.metro_create_model(ctypes.byref(cfg), seed, ctypes.byref(h)))
+        self._h = h
+        self.vocab = shape["vocab"]
+
+    # -- lifetime --------------------------------------------------------------
+    def close(self) -> None:
+        if getattr(self, "_h", None) and self._h.value:
+            lib.metro_destroy_model(self._h)
+            self._h = _vp()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    # -- weights -----------------------------------------------------------------
+    def load_weight(self, name: str, layer: int, bits: np.ndarray) -> None:
+        a = np.ascontiguousarray(bits, dtype=np.uint16)
+        check(lib.metro_load_weight(self._h, WEIGHT_ID[name], layer, a.ctypes.data, a.size))
+
+    def load_weights(self, weights: dict) -> None:
+        """Weights as produced by ``synth.llama_weights`` (bf16 bit arrays)."""
+        for name in ("embed", "final_norm", "lm_head"):
+            self.load_weight(name, -1, weights[name])
+        for li, lw in enumerate(weights["layers"]):
+            for name, arr in lw.items():
+                self.load_weight(name, li, arr)
+
+    def info(self) -> ModelInfo:
+        inf = ModelInfo()
+        check(lib.metro_model_get_info(self._h, ctypes.byref(inf)))
+        return inf
+
+    # -- sequences ---------------------------------------------------------------
+    def seq_open(self) -> int:
+        s = _i64()
+        check(lib.metro_seq_open(self._h, ctypes.byref(s)))
+        return s.value
+
+    def seq_fork(self, src: int, n_tokens: int, stream=None) -> int:
+        s = _i64()
+        check(lib.metro_seq_fork(self._h, src, n_tokens, _stream(stream), ctypes.byref(s)))
+        return s.value
+
+    def seq_close(self, seq: int) -> None:
+        check(lib.metro_seq_close(self._h, seq))
+
+    def seq_length(self, seq: int) -> int:
+        n = _i32()
+        check(lib.metro_seq_length(self._h, seq, ctypes.byref(n)))
+        return n.value
+
+    def seq_pages(self, seq: int) -> np.ndarray:
+        n = _i32()
+        check(lib.metro_seq_pages(self._h, seq, None, 0, ctypes.byref(n)))
+        out = np.zeros(n.value, dtype=np.int32)
+        check(lib.metro_seq_pages(self._h, seq, out.ctypes.data, n.value, ctypes.byref(n)))
+        return out
+
+    # -- forward -----------------------------------------------------------------
+    def prefill_chunk(self, seqs, chunks, logits=None, next_tok=None, stream=None) -> None:
+        """Append ``chunks[i]`` (host token ids) to ``seqs[i]``; fills ``logits``
+        (device fp32 [n, vocab]) and ``next_tok`` (device int32 [n]) if given."""
+        s = _host_i64(seqs)
+        lens = [len(c) for c in chunks]
+        cu = _host_i32(np.concatenate([[0], np.cumsum(lens)]))
+        toks = _host_i32(np.concatenate([np.asarray(c) for c in chunks]) if chunks else [])
+        check(lib.metro_prefill_chunk(self._h, len(s), s.ctypes.data, cu.ctypes.data, toks.ctypes.data,
+                                      _ptr(logits), _ptr(next_tok), _stream(stream)))
+
+    def decode_step(self, seqs, tokens_dev, logits=None, next_tok=None, stream=None) -> None:
+        """One token per sequence: ``tokens_dev`` is a device int32 [batch]."""
+        s = _host_i64(seqs)
+        check(lib.metro_decode_step(self._h, len(s), s.ctypes.data, _ptr(tokens_dev), _ptr(logits), _ptr(next_tok),
+                                    _stream(stream)))
+
+
+    # -- launch timing ------------------------------------------------------------
+    def profile_start(self, kernel_class: str, phase: str = "any") -> None:
+        check(lib.metro_profile_start(self._h, KERNEL_CLASS[kernel_class], PHASE[phase]))
+
+    def profile_stop(self):
+        """(total GPU ms between the bracketing events, number of launches)."""
+        ms, n = ctypes.c_double(), _i64()
+        check(lib.metro_profile_stop(self._h, ctypes.byref(ms), ctypes.byref(n)))
+        return ms.value, n.value
+
+
+# -- single-op entry points -------------------------------------------------------
+
+def op_gemm(X, W, M: int, N: int, Kp: int, epilogue: int, out, ldo: int, ldx: int | None = None, stream=None):
+    f32 = out if epilogue != EPI_SWIGLU else None
+    b16 = out if epilogue == EPI_SWIGLU else None
+    check(lib.metro_op_gemm(_ptr(X), ldx if ldx is not None else Kp, _ptr(W), Kp, M, N, epilogue, _ptr(f32),
+                            _ptr(b16), ldo, _stream(stream)))
+
+
+def op_rmsnorm(x, g, eps: float, h, rows: int, d: int, stream=None):
+    check(lib.metro_op_rmsnorm(_ptr(x), _ptr(g), eps, _ptr(h), rows, d, _stream(stream)))
+
+
+def op_argmax(logits, rows: int, vocab: int, out, stream=None):
+    check(lib.metro_op_argmax(_ptr(logits), rows, vocab, _ptr(out), _stream(stream)))

@@ -1,0 +1,126 @@
+"""Single kernels of the HIP path against CPU references (through metro_ops.h).
+
+GEMM: every epilogue, in the skinny (M <= 64) and tiled (M > 64) kernels,
+with ragged M, K padded to 128 and N covering several tiles plus a tail.
+The reference products are exact-value float64 sums of the same bf16
+operands; the GPU accumulates in fp32, so the bound is a few fp32 ulps of
+the row's absolute sum.
+"""
+
+import numpy as np
+import pytest
+
+from oracle import bf16_bits_to_f64, bf16_round, greedy_argmax, rms_norm, swiglu
+from paper_2411_03519_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def metro():
+    if not torch.cuda.is_available():
+        pytest.skip("no HIP device")
+    from paper_2411_03519_amd import metro as m
+    return m
+
+
+def dev_u16(a):
+    return torch.from_numpy(np.ascontiguousarray(a.view(np.int16))).cuda()
+
+
+def rand_bf16(rng, shape, scale=1.0):
+    return synth.f32_to_bf16_bits(rng.standard_normal(shape).astype(np.float32) * np.float32(scale))
+
+
+GEMM_CASES = [(1, 256, 64), (7, 640, 96), (16, 256, 32), (25, 4096, 512), (33, 768, 160), (64, 384, 1376),
+              (65, 256, 160), (200, 1152, 416), (129, 128, 96), (300, 4096, 256)]
+
+
+@pytest.mark.parametrize("M,K,N", GEMM_CASES)
+@pytest.mark.parametrize("epi", [0, 1])
+def test_gemm_f32_epilogues(metro, M, K, N, epi):
+    print(f"gemm M={M} K={K} N={N} epi={epi}", flush=True)
+    rng = np.random.default_rng(M * 7 + K + N + epi)
+    Kp = (K + 127) // 128 * 128
+    X = np.zeros((M, Kp), np.uint16)
+    W = np.zeros((N, Kp), np.uint16)
+    X[:, :K] = rand_bf16(rng, (M, K))
+    W[:, :K] = rand_bf16(rng, (N, K), 0.05)
+    ref = bf16_bits_to_f64(X) @ bf16_bits_to_f64(W).T
+    ldo = N + 4
+    init = rng.standard_normal((M, ldo)).astype(np.float32)
+    out = torch.from_numpy(init.copy()).cuda()
+    metro.op_gemm(dev_u16(X), dev_u16(W), M, N, Kp, epi, out, ldo)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().astype(np.float64)
+    want = ref + (init[:, :N] if epi == 1 else 0.0)
+    bound = 1e-5 * (np.abs(bf16_bits_to_f64(X)) @ np.abs(bf16_bits_to_f64(W)).T) + 1e-6
+    assert np.all(np.abs(got[:, :N] - want) <= bound), np.max(np.abs(got[:, :N] - want) - bound)
+    np.testing.assert_array_equal(got[:, N:], init[:, N:])  # padding columns untouched
+
+
+@pytest.mark.parametrize("M,K,F", [(3, 256, 688), (25, 256, 48), (64, 512, 112), (96, 256, 688), (130, 384, 80)])
+def test_gemm_swiglu_epilogue(metro, M, K, F):
+    print(f"swiglu M={M} K={K} F={F}", flush=True)
+    rng = np.random.default_rng(M + K + F)
+    X = rand_bf16(rng, (M, K))
+    Wg = rand_bf16(rng, (F, K), 0.1)
+    Wu = rand_bf16(rng, (F, K), 0.1)
+    packed = np.zeros((2 * F, K), np.uint16)
+    for b in range(F // 16):
+        packed[32 * b:32 * b + 16] = Wg[16 * b:16 * b + 16]
+        packed[32 * b + 16:32 * b + 32] = Wu[16 * b:16 * b + 16]
+    ldo = (F + 127) // 128 * 128
+    out = torch.zeros((M, ldo), dtype=torch.int16, device="cuda")
+    metro.op_gemm(dev_u16(X), dev_u16(packed), M, 2 * F, K, 2, out, ldo)
+    torch.cuda.synchronize()
+    got = bf16_bits_to_f64(out.cpu().numpy().view(np.uint16))
+    xf, wg, wu = bf16_bits_to_f64(X), bf16_bits_to_f64(Wg), bf16_bits_to_f64(Wu)
+    g, u = xf @ wg.T, xf @ wu.T
+    want = bf16_round(swiglu(g, u))
+    # fp32 accumulation error of g and u (bounded by the sums of |products|),
+    # carried through silu(g)*u, plus one bf16 ulp of the rounding
+    err_g = 1e-5 * (np.abs(xf) @ np.abs(wg).T)
+    err_u = 1e-5 * (np.abs(xf) @ np.abs(wu).T)
+    prop = 1.1 * np.abs(u) * err_g + np.abs(swiglu(g, np.ones_like(g))) * err_u
+    big = np.maximum(np.abs(want), np.abs(got[:, :F]))
+    ulp = np.ldexp(1.0, np.frexp(big)[1] - 8)
+    assert np.all(np.abs(got[:, :F] - want) <= ulp + 2 * prop + 1e-30)
+    assert np.mean(got[:, :F] == want) > 0.98
+    assert not np.any(got[:, F:])
+
+
+def test_rmsnorm(metro):
+    rng = np.random.default_rng(5)
+    rows, d = 37, 4096
+    x = (rng.standard_normal((rows, d)) * 3).astype(np.float32)
+    g = rand_bf16(rng, (d,), 1.0)
+    h = torch.zeros((rows, d), dtype=torch.int16, device="cuda")
+    metro.op_rmsnorm(torch.from_numpy(x).cuda(), dev_u16(g), 1e-5, h, rows, d)
+    torch.cuda.synchronize()
+    got = bf16_bits_to_f64(h.cpu().numpy().view(np.uint16))
+    want = bf16_round(rms_norm(x.astype(np.float64), bf16_bits_to_f64(g), 1e-5))
+    ulp = np.ldexp(1.0, np.frexp(np.abs(want))[1] - 8)
+    assert np.all(np.abs(got - want) <= ulp)
+    assert np.mean(got == want) > 0.99
+
+
+def test_argmax_lowest_index_and_nan(metro):
+    rng = np.random.default_rng(6)
+    V = 128256
+    L = rng.standard_normal((6, V)).astype(np.float32)
+    L[1, [5, 77, 128000]] = 50.0          # tie: lowest index wins
+    L[2, :] = -3.0                        # all equal
+    L[3, 100] = np.nan
+    L[3, 64000] = 40.0
+    L[4, :] = np.nan                      # no value left
+    L[5, V - 1] = 99.0                    # last element
+    out = torch.zeros(6, dtype=torch.int32, device="cuda")
+    metro.op_argmax(torch.from_numpy(L).cuda(), 6, V, out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    want = greedy_argmax(np.where(np.isnan(L), -np.inf, L))
+    want[4] = -1
+    np.testing.assert_array_equal(got, want)

@@ -1,0 +1,287 @@
+"""The HIP path against the oracle, through the C ABI (metro.h).
+
+Tiny Llama-style shape (2 layers, d 256, 4/2 heads of 64, FFN 688, vocab
+4096): agent batches with prompts of 32..128 tokens, batched prefill, chunked
+prefill, greedy decode, prefix forks, page-order and batch-composition
+invariance, and the error conventions.  The 8B-width case runs the real
+Llama-3-8B layer widths at reduced depth.
+"""
+
+import numpy as np
+import pytest
+
+from oracle import LlamaShape, OracleModel
+from paper_2411_03519_amd import synth
+from tests.parity import assert_logits_close, check_tokens, noise_floor
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def metro():
+    if not torch.cuda.is_available():
+        pytest.skip("no HIP device")
+    from paper_2411_03519_amd import metro as m
+    return m
+
+
+def make_model(metro, shape, weights, **kw):
+    args = dict(max_batch=64, max_tokens=1024, max_context=512, kv_pool_bytes=256 << 20)
+    args.update(kw)
+    m = metro.Model(shape, **args)
+    m.load_weights(weights)
+    return m
+
+
+def gpu_teacher_forced(m, prompts, feeds, chunk=None):
+    """Batched (optionally chunked) prefill of all prompts, then decode steps
+    fed with ``feeds[i][k]``.  Returns logits [n, 1+steps, V] and tokens."""
+    n = len(prompts)
+    V = m.vocab
+    seqs = [m.seq_open() for _ in range(n)]
+    rows = [[None] for _ in range(n)]
+    toks = [[None] for _ in range(n)]
+    step = chunk or max(len(p) for p in prompts)
+    off = 0
+    while True:
+        items = [i for i in range(n) if off < len(prompts[i])]
+        if not items:
+            break
+        lg = torch.empty(len(items), V, device="cuda")
+        nt = torch.empty(len(items), dtype=torch.int32, device="cuda")
+        m.prefill_chunk([seqs[i] for i in items], [prompts[i][off:off + step] for i in items], lg, nt)
+        lgh, nth = lg.cpu().numpy(), nt.cpu().numpy()
+        for j, i in enumerate(items):
+            if off + step >= len(prompts[i]):
+                rows[i][0], toks[i][0] = lgh[j], nth[j]
+        off += step
+    n_steps = len(feeds[0])
+    lg = torch.empty(n, V, device="cuda")
+    nt = torch.empty(n, dtype=torch.int32, device="cuda")
+    for k in range(n_steps):
+        feed = torch.tensor([int(feeds[i][k]) for i in range(n)], dtype=torch.int32, device="cuda")
+        m.decode_step(seqs, feed, lg, nt)
+        lgh, nth = lg.cpu().numpy(), nt.cpu().numpy()
+        for i in range(n):
+            rows[i].append(lgh[i])
+            toks[i].append(nth[i])
+    for s in seqs:
+        m.seq_close(s)
+    return np.array([np.stack(r) for r in rows]), np.array([np.array(t) for t in toks])
+
+
+@pytest.fixture(scope="module")
+def tiny_case():
+    prompts, n_new = synth.tiny_agent_batch(0)
+    out = {}
+    for norm in ("ones", "random"):
+        w = synth.llama_weights(synth.TINY, 0, norm=norm)
+        ref = OracleModel(LlamaShape(**synth.TINY), w)
+        gens = [ref.generate(p, n_new) for p in prompts]
+        out[norm] = (w, gens)
+    return prompts, n_new, out
+
+
+@pytest.mark.parametrize("norm", ["ones", "random"])
+def test_tiny_agent_batch_teacher_forced(metro, tiny_case, norm):
+    prompts, n_new, cases = tiny_case
+    w, gens = cases[norm]
+    print(f"tiny teacher-forced norm={norm}", flush=True)
+    with make_model(metro, synth.TINY, w) as m:
+        logits, toks = gpu_teacher_forced(m, prompts, [g[0][:-1] for g in gens])
+    want = np.stack([g[1] for g in gens])
+    assert_logits_close(logits, want, "tiny c0")
+    ties = check_tokens(toks, want, "tiny c0")
+    assert ties <= 2
+
+
+def test_tiny_free_running_greedy_streams(metro, tiny_case):
+    prompts, n_new, cases = tiny_case
+    w, gens = cases["ones"]
+    ref = OracleModel(LlamaShape(**synth.TINY), w)
+    with make_model(metro, synth.TINY, w) as m:
+        seqs = [m.seq_open() for _ in prompts]
+        lg = torch.empty(len(prompts), m.vocab, device="cuda")
+        nt = torch.empty(len(prompts), dtype=torch.int32, device="cuda")
+        m.prefill_chunk(seqs, prompts, lg, nt)
+        streams = [nt.cpu().numpy()]
+        for _ in range(n_new - 1):
+            m.decode_step(seqs, nt.clone(), lg, nt)
+            streams.append(nt.cpu().numpy())
+    streams = np.stack(streams, axis=1)
+    for i, p in enumerate(prompts):
+        want = gens[i][0]
+        if np.array_equal(streams[i], want):
+            continue
+        k = int(np.argmax(streams[i] != want))
+        # the first divergence must be a tie of the oracle at that step
+        assert check_tokens(streams[i][k:k + 1], gens[i][1][k:k + 1]) == 1
+        # and the oracle, fed the GPU's stream, agrees with the rest of it
+        tf = ref.teacher_forced(p, streams[i][:-1])
+        check_tokens(streams[i], tf)
+
+
+@pytest.mark.parametrize("chunk", [16, 23, 64])
+def test_tiny_chunked_prefill(metro, tiny_case, chunk):
+    prompts, n_new, cases = tiny_case
+    w, gens = cases["random"]
+    with make_model(metro, synth.TINY, w) as m:
+        logits, toks = gpu_teacher_forced(m, prompts, [g[0][:3] for g in gens], chunk=chunk)
+    want = np.stack([g[1][:4] for g in gens])
+    assert_logits_close(logits, want, f"chunk {chunk}")
+    check_tokens(toks, want)
+
+
+def test_decode_rows_independent_of_batch_composition(metro):
+    w = synth.llama_weights(synth.TINY, 1)
+    rng = np.random.default_rng(21)
+    prompts = [rng.integers(0, 4096, int(rng.integers(20, 90))) for _ in range(40)]
+    with make_model(metro, synth.TINY, w) as m:
+        seqs = [m.seq_open() for _ in prompts]
+        for g in range(0, 40, 10):
+            m.prefill_chunk(seqs[g:g + 10], prompts[g:g + 10])
+        feed = torch.tensor(rng.integers(0, 4096, 40), dtype=torch.int32, device="cuda")
+        results = []
+        for B in (1, 4, 20, 40):
+            forks = [m.seq_fork(s, m.seq_length(s)) for s in seqs[:B]]
+            lg = torch.empty(B, m.vocab, device="cuda")
+            m.decode_step(forks, feed[:B].contiguous(), lg)
+            results.append(lg[0].cpu().numpy())
+            for f in forks:
+                m.seq_close(f)
+    for r in results[1:]:
+        np.testing.assert_array_equal(r, results[0])
+
+
+def test_page_order_does_not_change_results(metro):
+    w = synth.llama_weights(synth.TINY, 2)
+    rng = np.random.default_rng(22)
+    prompts = [rng.integers(0, 4096, n) for n in (77, 50)]
+    outs = []
+    for scramble in (False, True):
+        with make_model(metro, synth.TINY, w) as m:
+            if scramble:
+                junk = [m.seq_open() for _ in range(12)]
+                m.prefill_chunk(junk, [rng.integers(0, 4096, int(n)) for n in rng.integers(1, 60, 12)])
+                for j in junk[::2]:
+                    m.seq_close(j)
+            seqs = [m.seq_open() for _ in prompts]
+            lg = torch.empty(2, m.vocab, device="cuda")
+            m.prefill_chunk(seqs, prompts, lg)
+            feed = torch.tensor([5, 6], dtype=torch.int32, device="cuda")
+            lg2 = torch.empty(2, m.vocab, device="cuda")
+            m.decode_step(seqs, feed, lg2)
+            outs.append((lg.cpu().numpy(), lg2.cpu().numpy(), [m.seq_pages(s) for s in seqs]))
+    np.testing.assert_array_equal(outs[0][0], outs[1][0])
+    np.testing.assert_array_equal(outs[0][1], outs[1][1])
+    assert any(not np.array_equal(a, b) for a, b in zip(outs[0][2], outs[1][2]))
+
+
+@pytest.mark.parametrize("prefix_len", [48, 37])
+def test_prefix_fork_shares_pages(metro, prefix_len):
+    w = synth.llama_weights(synth.TINY, 3, norm="random")
+    ref = OracleModel(LlamaShape(**synth.TINY), w)
+    rng = np.random.default_rng(23)
+    prefix = rng.integers(0, 4096, prefix_len)
+    suffixes = [rng.integers(0, 4096, n) for n in (20, 33, 9)]
+    with make_model(metro, synth.TINY, w) as m:
+        base = m.seq_open()
+        m.prefill_chunk([base], [prefix])
+        forks = [m.seq_fork(base, prefix_len) for _ in suffixes]
+        shared = prefix_len // 16
+        for f in forks:
+            assert np.array_equal(m.seq_pages(f)[:shared], m.seq_pages(base)[:shared])
+            if prefix_len % 16:
+                assert m.seq_pages(f)[shared] != m.seq_pages(base)[shared]
+        lg = torch.empty(3, m.vocab, device="cuda")
+        m.prefill_chunk(forks, suffixes, lg)
+        got = lg.cpu().numpy()
+        # the same chunks without sharing give bit-identical results
+        plain = [m.seq_open() for _ in suffixes]
+        for p in plain:  # same GEMM shapes as the base prefill
+            m.prefill_chunk([p], [prefix])
+        lg2 = torch.empty(3, m.vocab, device="cuda")
+        m.prefill_chunk(plain, suffixes, lg2)
+        np.testing.assert_array_equal(lg2.cpu().numpy(), got)
+        for f in forks:
+            m.seq_close(f)
+        m.seq_close(base)
+    want = np.stack([ref.prefill(ref.new_cache(), np.concatenate([prefix, s])) for s in suffixes])
+    assert_logits_close(got, want, "fork")
+
+
+def test_error_conventions(metro):
+    w = synth.llama_weights(synth.TINY, 4)
+    page_bytes = 2 * 2 * 64 * 16 * 2 * 2  # K+V, 2 kv heads, 16 slots, hd 64, bf16, 2 layers
+    with make_model(metro, synth.TINY, w, max_batch=4, max_tokens=200, max_context=150,
+                    kv_pool_bytes=10 * page_bytes, max_seqs=6) as m:
+        assert m.info().n_pages == 10
+        a, b = m.seq_open(), m.seq_open()
+        with pytest.raises(metro.MetroError) as e:
+            m.prefill_chunk([a, a], [[1, 2], [3]])
+        assert e.value.name == "METRO_E_INVAL"
+        with pytest.raises(metro.MetroError) as e:
+            m.prefill_chunk([a, 12345], [[1, 2], [3]])
+        assert e.value.name == "METRO_E_SEQ"
+        with pytest.raises(metro.MetroError) as e:
+            m.prefill_chunk([a], [[1] * 201])
+        assert e.value.name == "METRO_E_CAPACITY"
+        with pytest.raises(metro.MetroError) as e:
+            m.prefill_chunk([a], [[1, 4096]])
+        assert e.value.name == "METRO_E_INVAL"
+        m.prefill_chunk([a], [list(range(100))])            # 7 pages
+        free = m.info().free_pages
+        with pytest.raises(metro.MetroError) as e:        # needs 1 + 3 more pages, 3 free
+            m.prefill_chunk([a, b], [list(range(13)), list(range(40))])
+        assert e.value.name == "METRO_E_NOPAGES"
+        assert m.info().free_pages == free and m.seq_length(a) == 100 and m.seq_length(b) == 0
+        m.prefill_chunk([b], [list(range(40))])          # 3 pages: fits exactly
+        assert m.info().free_pages == 0
+        m.seq_close(a)
+        assert m.info().free_pages == 7
+        with pytest.raises(metro.MetroError) as e:
+            m.seq_close(a)
+        assert e.value.name == "METRO_E_SEQ"
+        with pytest.raises(metro.MetroError) as e:
+            m.seq_fork(b, 41)
+        assert e.value.name == "METRO_E_INVAL"
+        c = m.seq_open()
+        m.prefill_chunk([c], [list(range(100))])
+        with pytest.raises(metro.MetroError) as e:        # 151 > max_context
+            m.prefill_chunk([c], [list(range(51))])
+        assert e.value.name == "METRO_E_CAPACITY"
+        # out-of-range decode token: NaN logits and next_tok -1 for that row only
+        lg = torch.empty(2, m.vocab, device="cuda")
+        nt = torch.empty(2, dtype=torch.int32, device="cuda")
+        m.decode_step([b, c], torch.tensor([7, 99999], dtype=torch.int32, device="cuda"), lg, nt)
+        lgh = lg.cpu().numpy()
+        assert np.all(np.isfinite(lgh[0])) and np.all(np.isnan(lgh[1]))
+        assert nt.cpu().numpy()[1] == -1
+
+
+def test_llama3_8b_widths_two_layers(metro):
+    """Llama-3-8B layer widths (d 4096, 32/8 heads of 128, FFN 14336, vocab
+    128256) at depth 2: two agents with 256- and 203-token prompts, prefilled in
+    128-token chunks, then 8 decode steps."""
+    shape = synth.with_layers(synth.LLAMA3_8B, 2)
+    print("8B widths: drawing weights", flush=True)
+    w = synth.llama_weights(shape, 0)
+    rng = np.random.default_rng(24)
+    prompts = [rng.integers(0, shape["vocab"], n) for n in (256, 203)]
+    print("8B widths: oracle (float64)", flush=True)
+    ref = OracleModel(LlamaShape(**shape), w)
+    gens = [ref.generate(p, 9, chunk=128) for p in prompts]
+    del ref
+    print("8B widths: oracle in float32 (noise floor)", flush=True)
+    r32 = OracleModel(LlamaShape(**shape), w, dtype=np.float32)
+    f32 = np.stack([r32.teacher_forced(p, g[0][:-1], chunk=128) for p, g in zip(prompts, gens)])
+    del r32
+    want = np.stack([g[1] for g in gens])
+    bound = noise_floor(want, f32)
+    print("8B widths: gpu", flush=True)
+    with make_model(metro, shape, w, max_batch=4, max_tokens=512, max_context=512, kv_pool_bytes=1 << 30) as m:
+        logits, toks = gpu_teacher_forced(m, prompts, [g[0][:-1] for g in gens], chunk=128)
+    assert_logits_close(logits, want, "8B widths", max_abs_bound=bound)
+    check_tokens(toks, want, "8B widths", tie=bound)

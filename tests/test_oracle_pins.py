@@ -336,3 +336,17 @@ def test_quantized_close_to_unquantized(tiny_model):
     b = exact.forward(exact.new_cache(), prompt)
     rel = np.linalg.norm(a - b) / np.linalg.norm(b)
     assert 0 < rel < 0.05
+
+
+def test_float32_evaluation_stays_within_tolerance_at_tiny_shape(tiny_model):
+    # the same function in float32 arithmetic: the spread legitimate fp32
+    # rounding causes (used as the noise floor of wider shapes)
+    w = synth.llama_weights(synth.TINY, 3, norm="random")
+    m32 = OracleModel(shape_of(synth.TINY), w, dtype=np.float32)
+    prompt = np.random.default_rng(21).integers(0, synth.TINY["vocab"], 60)
+    a = tiny_model.forward(tiny_model.new_cache(), prompt)
+    b = m32.forward(m32.new_cache(), prompt)
+    assert m32.layers[0]["wq"].dtype == np.float32
+    d = np.abs(a.astype(np.float64) - b)
+    assert 0 < d.max() < 2e-2
+    assert np.linalg.norm(a - b) / np.linalg.norm(a) < 1e-2
