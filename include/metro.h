@@ -207,8 +207,7 @@ typedef enum metro_kernel_class {
   METRO_K_RMSNORM = 1,
   METRO_K_GEMM_QKV = 2,
   METRO_K_ROPE_KV = 3,
-  METRO_K_ATTENTION = 4,
-  METRO_K_ATTN_COMBINE = 5,
+  METRO_K_ATTENTION = 4,   /* decode attention includes the merge of context splits */
   METRO_K_GEMM_O = 6,
   METRO_K_GEMM_GATE_UP = 7,
   METRO_K_GEMM_DOWN = 8,

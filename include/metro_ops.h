@@ -28,13 +28,17 @@ extern "C" {
  *   2  W rows come in blocks of 32 = 16 gate rows then 16 up rows of the same
  *      features; out_bf16[m*ldo + j] = bf16(silu(gate_j) * up_j), j < N/2
  *      (SwiGLU, Shazeer 2020).
+ * workspace: NULL, or device fp32 [8][M][N]; when given, a decode-sized GEMM
+ * (M <= 64, epilogue 0 or 1) runs the k-split form the model uses (slices in
+ * the workspace, then summed in slice order into the output).
  * Errors: E_INVAL for shapes outside these rules or a NULL operand. */
 metro_status metro_op_gemm(const uint16_t* X, int32_t ldx, const uint16_t* W, int32_t Kp, int32_t M, int32_t N,
-                           int32_t epilogue, float* out_f32, uint16_t* out_bf16, int32_t ldo, void* stream);
+                           int32_t epilogue, float* out_f32, uint16_t* out_bf16, int32_t ldo, float* workspace,
+                           void* stream);
 
 /* RMSNorm (Zhang & Sennrich 2019): h[r, :] = bf16(x[r, :] / sqrt(mean(x[r, :]^2)
  * + eps) * g), x fp32 [rows, d], g bf16 [d], h bf16 [rows, d], d % 4 == 0. */
-metro_status metro_op_rmsnorm(const float* x, const uint16_t* g, float eps, uint16_t* h, int32_t rows, int32_t d,
+metro_status metro_op_rmsnorm(float* x, const uint16_t* g, float eps, uint16_t* h, int32_t rows, int32_t d,
                               void* stream);
 
 /* Greedy choice: out[r] = lowest index of the maximum of logits[r, :] (fp32

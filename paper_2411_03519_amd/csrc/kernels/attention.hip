@@ -1,19 +1,32 @@
-// Paged grouped-query attention on gfx950 (decode rows, and prefill rows in
-// this first version): one work item = (row, split of the row's pages) for one
-// kv head, computing the G query heads that share that kv head, so each K/V
-// page is read once per group.
+// Paged grouped-query attention on gfx950 with MFMA.
 //
-// Layout.  A page holds 16 positions; per layer and kv head its K tile and V
-// tile are each a contiguous [16][hd] bf16 block.  Lane (tg, dg) of a wave
-// owns dims 8dg .. 8dg+7 of token rows tg, tg+TPL, ...: one 16-byte load per
-// row, and each load instruction of the wave covers TPL whole rows (1 KiB,
-// fully coalesced).
+// KV page layout (per layer, page, kv head): K as [16 keys][hd] and V
+// transposed as [hd][16 keys], both bf16.  With those two layouts every
+// matrix-core operand is a contiguous run of a page:
 //
-// Softmax is the online (streaming) form in fp32 with scores pre-multiplied
-// by log2(e) so exp2 can be used; the four waves of a workgroup take pages
-// round-robin and are merged through LDS; rows whose context spans several
-// splits leave (max, sum, unnormalised output) partials for the combine
-// kernel.  The number of splits depends on the context length only.
+//   scores  S^T[key][q] = sum_d K[key][d] Q[q][d]       v_mfma_f32_16x16x32_bf16
+//           A = K rows (16 keys), B = Q^T (16 query columns)
+//   output  O^T[d][q] += sum_key V^T[d][key] P^T[key][q] v_mfma_f32_16x16x16_bf16
+//           (decode, one page) or 16x16x32 over a page pair (prefill)
+//
+// The MFMA output of S^T leaves lane l with keys 4(l/16)+i of query column
+// l%16, which is exactly the B operand the P.V product needs, so the softmax
+// runs in registers with no lane shuffles except the two cross-row steps of
+// the row maximum.  The query columns are the (token, head) pairs of one GQA
+// group, so a K/V page is read once per group.
+//
+// Precision: scores, the running max/sum and the output accumulators are fp32.
+// P enters the bf16 matrix core as hi = bf16(p) plus lo = bf16(p - hi) (two
+// MFMAs), which keeps p to about 16 significant bits.
+//
+// Decode: one workgroup per (row, kv head); its eight waves take the row's
+// pages round-robin and merge through LDS in wave order, so the result of a
+// row never depends on the rest of the batch and needs no cross-workgroup
+// merge (an agent-scope fence per workgroup is costly on the multi-XCD chip).
+//
+// Prefill (flash attention): one workgroup = (query block, kv head); the K and
+// V pages of the block's visible context go through LDS in pairs (double
+// buffered) and are shared by the four waves; causal masking per element.
 #include "common.h"
 #include "kernels.h"
 
@@ -22,211 +35,363 @@ namespace metro {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegBig = -1.0e30f;
 
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x4 mfma_k32(uint4 a, uint4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x4 mfma_k16(uint2 a, uint2 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, a), __builtin_bit_cast(s16x4, b), c,
+                                                   0, 0, 0);
+}
+
+// p -> (hi, lo) bf16 pairs packed two per word
+__device__ __forceinline__ void split_bf16(float p0, float p1, uint32_t& hi, uint32_t& lo) {
+  const uint16_t h0 = f32_to_bf16(p0), h1 = f32_to_bf16(p1);
+  hi = static_cast<uint32_t>(h0) | (static_cast<uint32_t>(h1) << 16);
+  lo = pack_bf16x2(p0 - bf16_to_f32(h0), p1 - bf16_to_f32(h1));
+}
+
+// ===========================================================================
+// Decode
+// ===========================================================================
+
+// One workgroup of kDecodeWaves waves per (row, kv head); wave w takes pages
+// w, w + kDecodeWaves, ... (several pages in flight in registers) and the
+// waves' (max, sum, output) states are merged through LDS in wave order.
+constexpr int kDecodeWaves = 8;
+
 template <int HD, int G>
-__global__ __launch_bounds__(256) void attn_paged_kernel(AttnArgs a) {
-  constexpr int DL = HD / 8;        // lanes per token row
-  constexpr int TPL = kWave / DL;   // token rows per load instruction
-  constexpr int TPW = kPage / TPL;  // token rows per lane per page
+__global__ __launch_bounds__(kDecodeWaves * 64) void attn_decode_kernel(AttnArgs a) {
+  constexpr int KQ = HD / 32;  // score MFMAs per page
+  constexpr int NT = HD / 16;  // output tiles
+  constexpr int NW = kDecodeWaves;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int dg = lane % DL, tg = lane / DL;
-  const int wi = blockIdx.x / a.nkv, h = blockIdx.x % a.nkv;
-  const int row = a.work[2 * wi], split = a.work[2 * wi + 1];
+  const int col = lane & 15, grp = lane >> 4;
+  const int row = blockIdx.x / a.nkv, h = blockIdx.x % a.nkv;
   const int ctx = a.row_ctx[row];
   const int qrow = a.row_qrow[row];
   const int32_t* bt = a.bt + a.row_bt[row];
   const int n_pages = ceil_div(ctx, kPage);
-  const int p_begin = split * a.pages_per_split;
-  const int p_end = min(n_pages, p_begin + a.pages_per_split);
-
   const float qscale = a.scale * kLog2e;
-  float qv[G][8];
+
+  // Q^T operand: column col = head h*G + col (zero beyond the group);
+  // lane group grp holds dims grp*HD/4 .. +HD/4, MFMA i takes 8 of them.
+  uint4 qf[KQ];
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
-    const uint4 w = *reinterpret_cast<const uint4*>(
-        a.q + (static_cast<size_t>(qrow) * a.nq + h * G + g) * HD + dg * 8);
-    const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+  for (int i = 0; i < KQ; ++i) qf[i] = make_uint4(0, 0, 0, 0);
+  if (col < G) {
+    const uint16_t* qp = a.q + (static_cast<size_t>(qrow) * a.nq + h * G + col) * HD + grp * (HD / 4);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      qv[g][2 * e] = lo_bf16(ww[e]) * qscale;
-      qv[g][2 * e + 1] = hi_bf16(ww[e]) * qscale;
-    }
+    for (int i = 0; i < KQ; ++i) qf[i] = *reinterpret_cast<const uint4*>(qp + 8 * i);
   }
 
-  float m[G], l[G], acc[G][8];
+  f32x4 o[NT];
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
-    m[g] = kNegBig;
-    l[g] = 0.f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[g][e] = 0.f;
-  }
+  for (int t = 0; t < NT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m = kNegBig, l = 0.f;
 
-  for (int p = p_begin + wave; p < p_end; p += 4) {
+  // K operand: key row col, permuted dims; V^T operand: dims 16t + col, keys
+  // 4grp..4grp+3.  The wave's pages are w, w+NW, ...; PD of them are kept in
+  // flight in a register ring, each slot refilled right after use with an
+  // unconditional (clamped) load so every page waits only for itself.
+  constexpr int PD = 3;
+  uint4 kf[PD][KQ];
+  uint2 vf[PD][NT];
+  auto load_page = [&](int sl, int p) {
     const int page = bt[p];
-    const uint16_t* kb = a.kv + kv_offset(page, 0, a.nkv, h, 0, HD, dg * 8);
-    const uint16_t* vb = a.kv + kv_offset(page, 1, a.nkv, h, 0, HD, dg * 8);
-    uint4 kw[TPW], vw[TPW];
+    const uint16_t* kp = a.kv + kv_offset(page, 0, a.nkv, h, 0, HD, 0);
+    const uint16_t* vp = a.kv + kv_offset(page, 1, a.nkv, h, 0, HD, 0);
 #pragma unroll
-    for (int j = 0; j < TPW; ++j) {
-      kw[j] = *reinterpret_cast<const uint4*>(kb + (j * TPL + tg) * HD);
-      vw[j] = *reinterpret_cast<const uint4*>(vb + (j * TPL + tg) * HD);
-    }
-    float s[TPW][G];
+    for (int i = 0; i < KQ; ++i)
+      kf[sl][i] = *reinterpret_cast<const uint4*>(kp + col * HD + grp * (HD / 4) + 8 * i);
 #pragma unroll
-    for (int j = 0; j < TPW; ++j) {
-      const uint32_t kk[4] = {kw[j].x, kw[j].y, kw[j].z, kw[j].w};
+    for (int t = 0; t < NT; ++t) vf[sl][t] = *reinterpret_cast<const uint2*>(vp + (16 * t + col) * kPage + 4 * grp);
+  };
+  const int np = wave < n_pages ? (n_pages - wave + NW - 1) / NW : 0;
+  if (np > 0) {
 #pragma unroll
-      for (int g = 0; g < G; ++g) {
-        float d = 0.f;
+    for (int sl = 0; sl < PD; ++sl) load_page(sl, wave + NW * min(sl, np - 1));
+    for (int base = 0; base < np; base += PD) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          d += qv[g][2 * e] * lo_bf16(kk[e]);
-          d += qv[g][2 * e + 1] * hi_bf16(kk[e]);
+      for (int sl = 0; sl < PD; ++sl) {
+        const int it = base + sl;
+        if (it < np) {
+          const int p = wave + NW * it;
+          f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int i = 0; i < KQ; ++i) s = mfma_k32(kf[sl][i], qf[i], s);
+          float sv[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) sv[r] = (p * kPage + 4 * grp + r < ctx) ? s[r] * qscale : -INFINITY;
+          float mp = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+          mp = fmaxf(mp, __shfl_xor(mp, 16, kWave));
+          mp = fmaxf(mp, __shfl_xor(mp, 32, kWave));
+          const float mn = fmaxf(m, mp);
+          const float corr = exp2f(m - mn);
+          m = mn;
+          float pv[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) pv[r] = exp2f(sv[r] - mn);
+          l = l * corr + ((pv[0] + pv[1]) + (pv[2] + pv[3]));
+          uint2 hi, lo;
+          split_bf16(pv[0], pv[1], hi.x, lo.x);
+          split_bf16(pv[2], pv[3], hi.y, lo.y);
+#pragma unroll
+          for (int t = 0; t < NT; ++t) {
+            o[t] *= corr;
+            o[t] = mfma_k16(vf[sl][t], hi, o[t]);
+            o[t] = mfma_k16(vf[sl][t], lo, o[t]);
+          }
         }
-        s[j][g] = d;
-      }
-    }
-#pragma unroll
-    for (int o = 1; o < DL; o <<= 1)
-#pragma unroll
-      for (int j = 0; j < TPW; ++j)
-#pragma unroll
-        for (int g = 0; g < G; ++g) s[j][g] += __shfl_xor(s[j][g], o, kWave);
-#pragma unroll
-    for (int j = 0; j < TPW; ++j) {
-      const int pos = p * kPage + j * TPL + tg;
-      if (pos >= ctx) {
-#pragma unroll
-        for (int g = 0; g < G; ++g) s[j][g] = -INFINITY;
-      }
-    }
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      float mp = s[0][g];
-#pragma unroll
-      for (int j = 1; j < TPW; ++j) mp = fmaxf(mp, s[j][g]);
-#pragma unroll
-      for (int o = DL; o < kWave; o <<= 1) mp = fmaxf(mp, __shfl_xor(mp, o, kWave));
-      const float mn = fmaxf(m[g], mp);
-      const float corr = exp2f(m[g] - mn);
-      m[g] = mn;
-      l[g] *= corr;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[g][e] *= corr;
-#pragma unroll
-      for (int j = 0; j < TPW; ++j) {
-        const float pj = exp2f(s[j][g] - mn);
-        l[g] += pj;
-        const uint32_t vv[4] = {vw[j].x, vw[j].y, vw[j].z, vw[j].w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc[g][2 * e] += pj * lo_bf16(vv[e]);
-          acc[g][2 * e + 1] += pj * hi_bf16(vv[e]);
-        }
+        load_page(sl, wave + NW * min(it + PD, np - 1));
       }
     }
   }
+  l += __shfl_xor(l, 16, kWave);
+  l += __shfl_xor(l, 32, kWave);
 
-  // sum over the token groups of the wave (all share the wave's running max)
+  // merge the waves in order
+  __shared__ float sm[NW][G], sl[NW][G];
+  __shared__ float so[NW][HD][G];
+  if (col < G) {
 #pragma unroll
-  for (int o = DL; o < kWave; o <<= 1) {
+    for (int t = 0; t < NT; ++t)
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-      l[g] += __shfl_xor(l[g], o, kWave);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[g][e] += __shfl_xor(acc[g][e], o, kWave);
-    }
-  }
-
-  __shared__ float sm[4][G], sl[4][G];
-  __shared__ float sacc[4][G][HD];
-  if (tg == 0) {
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) sacc[wave][g][dg * 8 + e] = acc[g][e];
-      if (dg == 0) {
-        sm[wave][g] = m[g];
-        sl[wave][g] = l[g];
-      }
+      for (int i = 0; i < 4; ++i) so[wave][16 * t + 4 * grp + i][col] = o[t][i];
+    if (grp == 0) {
+      sm[wave][col] = m;
+      sl[wave][col] = l;
     }
   }
   __syncthreads();
-
-  const int nsplit = a.row_nsplit[row];
   for (int idx = threadIdx.x; idx < G * HD; idx += blockDim.x) {
     const int g = idx / HD, d = idx % HD;
     float M = sm[0][g];
 #pragma unroll
-    for (int w = 1; w < 4; ++w) M = fmaxf(M, sm[w][g]);
+    for (int w = 1; w < NW; ++w) M = fmaxf(M, sm[w][g]);
     float L = 0.f, O = 0.f;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
+    for (int w = 0; w < NW; ++w) {
       const float f = exp2f(sm[w][g] - M);
       L += sl[w][g] * f;
-      O += sacc[w][g][d] * f;
+      O += so[w][d][g] * f;
     }
-    if (nsplit == 1) {
-      a.out[(static_cast<size_t>(qrow) * a.nq + h * G + g) * HD + d] = f32_to_bf16(O / L);
-    } else {
-      float* pp = a.part + ((static_cast<size_t>(wi) * a.nkv + h) * G + g) * (HD + 2);
-      pp[d] = O;
-      if (d == 0) {
-        pp[HD] = M;
-        pp[HD + 1] = L;
+    a.out[(static_cast<size_t>(qrow) * a.nq + h * G + g) * HD + d] = f32_to_bf16(O / L);
+  }
+}
+
+// ===========================================================================
+// Prefill (flash attention over pages)
+// ===========================================================================
+
+// Query columns of one 16-wide MFMA tile: 16/G tokens x G heads.
+template <int HD, int G>
+__global__ __launch_bounds__(256) void attn_prefill_kernel(PrefillAttnArgs a) {
+  constexpr int KQ = HD / 32;
+  constexpr int NT = HD / 16;
+  constexpr int NQ = 4;             // query tiles per wave
+  constexpr int TPT = 16 / G;       // tokens per tile
+  constexpr int TPW = NQ * TPT;     // tokens per wave
+  constexpr int TPB = 4 * TPW;      // tokens per workgroup
+  constexpr int PAGE = kPage * HD;  // bf16 elements of one K (or V^T) page
+
+  __shared__ uint16_t ks[2][2][PAGE];  // [buffer][page of the pair]
+  __shared__ uint16_t vs[2][2][PAGE];
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int col = lane & 15, grp = lane >> 4;
+  const int bi = blockIdx.x / a.nkv, h = blockIdx.x % a.nkv;
+  const int item = a.blocks[3 * bi], row0 = a.blocks[3 * bi + 1], nrows = a.blocks[3 * bi + 2];
+  const int32_t* bt = a.bt + a.item_bt[item];
+  const int last_pos = a.pos[row0 + nrows - 1];
+  const int n_pages = last_pos / kPage + 1;
+  const int n_pairs = (n_pages + 1) / 2;
+  const float qscale = a.scale * kLog2e;
+
+  // this lane's query column in each tile
+  int qpos[NQ], qrow[NQ];
+  bool qok[NQ];
+  uint4 qf[NQ][KQ];
+#pragma unroll
+  for (int n = 0; n < NQ; ++n) {
+    const int tok = wave * TPW + n * TPT + col / G;
+    qok[n] = tok < nrows;
+    qrow[n] = row0 + (qok[n] ? tok : 0);
+    qpos[n] = qok[n] ? a.pos[qrow[n]] : -1;
+    const uint16_t* qp = a.q + (static_cast<size_t>(qrow[n]) * a.nq + h * G + col % G) * HD + grp * (HD / 4);
+#pragma unroll
+    for (int i = 0; i < KQ; ++i)
+      qf[n][i] = qok[n] ? *reinterpret_cast<const uint4*>(qp + 8 * i) : make_uint4(0, 0, 0, 0);
+  }
+
+  f32x4 o[NQ][NT];
+  float m[NQ], l[NQ];
+#pragma unroll
+  for (int n = 0; n < NQ; ++n) {
+    m[n] = kNegBig;
+    l[n] = 0.f;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) o[n][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // cooperative staging of one page pair: 2 K pages + 2 V^T pages, 16 B chunks
+  constexpr int CH = PAGE / 8;  // 16-byte chunks per page
+  constexpr int PER = (4 * CH) / 256;
+  uint4 stage[PER];
+  auto fetch = [&](int pair) {
+#pragma unroll
+    for (int r = 0; r < PER; ++r) {
+      const int c = tid + 256 * r;
+      const int which = c / CH, off = c % CH;  // which: 0,1 = K pages, 2,3 = V pages
+      const int pi = 2 * pair + (which & 1);
+      if (pi < n_pages) {
+        const int page = bt[pi];
+        const uint16_t* src = a.kv + kv_offset(page, which >> 1, a.nkv, h, 0, HD, 0);
+        stage[r] = *reinterpret_cast<const uint4*>(src + 8 * off);
+      } else {
+        stage[r] = make_uint4(0, 0, 0, 0);
       }
     }
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int r = 0; r < PER; ++r) {
+      const int c = tid + 256 * r;
+      const int which = c / CH, off = c % CH;
+      uint16_t* dst = (which < 2 ? ks[buf][which] : vs[buf][which - 2]) + 8 * off;
+      *reinterpret_cast<uint4*>(dst) = stage[r];
+    }
+  };
+
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  for (int pair = 0; pair < n_pairs; ++pair) {
+    const int buf = pair & 1;
+    if (pair + 1 < n_pairs) fetch(pair + 1);
+
+    // K operand of both pages (A of S^T): key row col, permuted dims
+    uint4 kf[2][KQ];
+#pragma unroll
+    for (int pg = 0; pg < 2; ++pg)
+#pragma unroll
+      for (int i = 0; i < KQ; ++i)
+        kf[pg][i] = *reinterpret_cast<const uint4*>(&ks[buf][pg][col * HD + grp * (HD / 4) + 8 * i]);
+
+#pragma unroll
+    for (int n = 0; n < NQ; ++n) {
+      float sv[2][4];
+#pragma unroll
+      for (int pg = 0; pg < 2; ++pg) {
+        f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int i = 0; i < KQ; ++i) s = mfma_k32(kf[pg][i], qf[n][i], s);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int kpos = (2 * pair + pg) * kPage + 4 * grp + r;
+          sv[pg][r] = kpos <= qpos[n] ? s[r] * qscale : -INFINITY;
+        }
+      }
+      float mp = fmaxf(fmaxf(fmaxf(sv[0][0], sv[0][1]), fmaxf(sv[0][2], sv[0][3])),
+                       fmaxf(fmaxf(sv[1][0], sv[1][1]), fmaxf(sv[1][2], sv[1][3])));
+      mp = fmaxf(mp, __shfl_xor(mp, 16, kWave));
+      mp = fmaxf(mp, __shfl_xor(mp, 32, kWave));
+      const float mn = fmaxf(m[n], mp);
+      const float corr = exp2f(m[n] - mn);
+      m[n] = mn;
+      float pv[2][4];
+      float ps = 0.f;
+#pragma unroll
+      for (int pg = 0; pg < 2; ++pg)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          pv[pg][r] = exp2f(sv[pg][r] - mn);
+          ps += pv[pg][r];
+        }
+      l[n] = l[n] * corr + ps;
+      // P^T operand over the page pair: k-slot 8grp+j is key 4grp+j of page
+      // j/4; the V^T operand below uses the same order.
+      uint4 hi, lo;
+      split_bf16(pv[0][0], pv[0][1], hi.x, lo.x);
+      split_bf16(pv[0][2], pv[0][3], hi.y, lo.y);
+      split_bf16(pv[1][0], pv[1][1], hi.z, lo.z);
+      split_bf16(pv[1][2], pv[1][3], hi.w, lo.w);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const uint2 va = *reinterpret_cast<const uint2*>(&vs[buf][0][(16 * t + col) * kPage + 4 * grp]);
+        const uint2 vb = *reinterpret_cast<const uint2*>(&vs[buf][1][(16 * t + col) * kPage + 4 * grp]);
+        const uint4 vf = make_uint4(va.x, va.y, vb.x, vb.y);
+        o[n][t] *= corr;
+        o[n][t] = mfma_k32(vf, hi, o[n][t]);
+        o[n][t] = mfma_k32(vf, lo, o[n][t]);
+      }
+    }
+    if (pair + 1 < n_pairs) stash(buf ^ 1);
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int n = 0; n < NQ; ++n) {
+    float L = l[n];
+    L += __shfl_xor(L, 16, kWave);
+    L += __shfl_xor(L, 32, kWave);
+    if (!qok[n]) continue;
+    const float inv = 1.0f / L;
+    uint16_t* op = a.out + (static_cast<size_t>(qrow[n]) * a.nq + h * G + col % G) * HD;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      uint2 w;
+      w.x = pack_bf16x2(o[n][t][0] * inv, o[n][t][1] * inv);
+      w.y = pack_bf16x2(o[n][t][2] * inv, o[n][t][3] * inv);
+      *reinterpret_cast<uint2*>(op + 16 * t + 4 * grp) = w;
+    }
   }
 }
 
-// Merge the split partials of each (row, query head).  One block of hd
-// threads per (row, head); rows with a single split were already written.
-__global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
-  const int row = blockIdx.x / a.nq, j = blockIdx.x % a.nq;
-  const int ns = a.row_nsplit[row];
-  if (ns == 1) return;
-  const int G = a.nq / a.nkv;
-  const int h = j / G, g = j % G;
-  const int hd = a.hd;
-  const int w0 = a.row_work[row];
-  const int d = threadIdx.x;
-  auto part = [&](int s) { return a.part + ((static_cast<size_t>(w0 + s) * a.nkv + h) * G + g) * (hd + 2); };
-  float M = kNegBig;
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, part(s)[hd]);
-  float L = 0.f, O = 0.f;
-  for (int s = 0; s < ns; ++s) {
-    const float* pp = part(s);
-    const float f = exp2f(pp[hd] - M);
-    L += pp[hd + 1] * f;
-    O += pp[d] * f;
-  }
-  a.out[(static_cast<size_t>(a.row_qrow[row]) * a.nq + j) * hd + d] = f32_to_bf16(O / L);
-}
+// ===========================================================================
 
 template <int HD>
-static hipError_t launch_hd(const AttnArgs& a, hipStream_t s) {
-  const dim3 grid(a.n_work * a.nkv);
+static hipError_t launch_decode_hd(const AttnArgs& a, hipStream_t s) {
+  const dim3 grid(a.rows * a.nkv), block(kDecodeWaves * 64);
   switch (a.nq / a.nkv) {
-    case 1: hipLaunchKernelGGL((attn_paged_kernel<HD, 1>), grid, dim3(256), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((attn_paged_kernel<HD, 2>), grid, dim3(256), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((attn_paged_kernel<HD, 4>), grid, dim3(256), 0, s, a); break;
-    case 8: hipLaunchKernelGGL((attn_paged_kernel<HD, 8>), grid, dim3(256), 0, s, a); break;
+    case 1: hipLaunchKernelGGL((attn_decode_kernel<HD, 1>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((attn_decode_kernel<HD, 2>), grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL((attn_decode_kernel<HD, 4>), grid, block, 0, s, a); break;
+    case 8: hipLaunchKernelGGL((attn_decode_kernel<HD, 8>), grid, block, 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_attn_paged(const AttnArgs& a, hipStream_t s) {
-  if (a.n_work <= 0) return hipSuccess;
-  if (a.hd == 128) return launch_hd<128>(a, s);
-  if (a.hd == 64) return launch_hd<64>(a, s);
+hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s) {
+  if (a.rows <= 0) return hipSuccess;
+  if (a.hd == 128) return launch_decode_hd<128>(a, s);
+  if (a.hd == 64) return launch_decode_hd<64>(a, s);
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_attn_combine(const AttnArgs& a, hipStream_t s) {
-  if (a.rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(attn_combine_kernel, dim3(a.rows * a.nq), dim3(a.hd), 0, s, a);
+template <int HD>
+static hipError_t launch_prefill_hd(const PrefillAttnArgs& a, hipStream_t s) {
+  const dim3 grid(a.n_blocks * a.nkv);
+  switch (a.nq / a.nkv) {
+    case 1: hipLaunchKernelGGL((attn_prefill_kernel<HD, 1>), grid, dim3(256), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((attn_prefill_kernel<HD, 2>), grid, dim3(256), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((attn_prefill_kernel<HD, 4>), grid, dim3(256), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((attn_prefill_kernel<HD, 8>), grid, dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
+
+hipError_t launch_attn_prefill(const PrefillAttnArgs& a, hipStream_t s) {
+  if (a.n_blocks <= 0) return hipSuccess;
+  if (a.hd == 128) return launch_prefill_hd<128>(a, s);
+  if (a.hd == 64) return launch_prefill_hd<64>(a, s);
+  return hipErrorInvalidValue;
+}
+
+int prefill_tokens_per_block(int group) { return 256 / group; }
 
 }  // namespace metro

@@ -39,25 +39,49 @@ hipError_t launch_embed(const int32_t* tok, const uint16_t* embed, int vocab, in
 // ---------------------------------------------------------------------------
 // RMSNorm: h = bf16(x * rsqrt(mean(x^2) + eps) * g).  One block per row.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ x, int ldx,
-                                                      const uint16_t* __restrict__ g, float eps,
-                                                      uint16_t* __restrict__ h, int ldh, int d) {
+template <int NTH>
+__global__ __launch_bounds__(NTH) void rmsnorm_kernel(float* __restrict__ x, int ldx, const uint16_t* __restrict__ g,
+                                                      float eps, uint16_t* __restrict__ h, int ldh, int d,
+                                                      const float* __restrict__ parts, int n_parts, int rows) {
   const int r = blockIdx.x;
-  const float4* xr = reinterpret_cast<const float4*>(x + static_cast<size_t>(r) * ldx);
+  float4* xr = reinterpret_cast<float4*>(x + static_cast<size_t>(r) * ldx);
+  if (n_parts > 0) {
+    const size_t stride = static_cast<size_t>(rows) * d / 4;
+    const float4* pr = reinterpret_cast<const float4*>(parts + static_cast<size_t>(r) * d);
+    for (int i = threadIdx.x; i < d / 4; i += NTH) {
+      float4 s = pr[i];
+      for (int k = 1; k < n_parts; ++k) {
+        const float4 v = pr[k * stride + i];
+        s.x += v.x;
+        s.y += v.y;
+        s.z += v.z;
+        s.w += v.w;
+      }
+      float4 v = xr[i];
+      v.x += s.x;
+      v.y += s.y;
+      v.z += s.z;
+      v.w += s.w;
+      xr[i] = v;
+    }
+  }
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d / 4; i += 256) {
+  for (int i = threadIdx.x; i < d / 4; i += NTH) {
     float4 v = xr[i];
     ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
   ss = wave_sum(ss);
-  __shared__ float red[4];
+  constexpr int NWV = NTH / 64;
+  __shared__ float red[NWV];
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
   __syncthreads();
-  const float tot = (red[0] + red[1]) + (red[2] + red[3]);
+  float tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < NWV; ++w) tot += red[w];
   const float inv = rsqrtf(tot / static_cast<float>(d) + eps);
   const uint2* gr = reinterpret_cast<const uint2*>(g);
   uint2* hr = reinterpret_cast<uint2*>(h + static_cast<size_t>(r) * ldh);
-  for (int i = threadIdx.x; i < d / 4; i += 256) {
+  for (int i = threadIdx.x; i < d / 4; i += NTH) {
     float4 v = xr[i];
     uint2 gw = gr[i];
     uint2 o;
@@ -67,59 +91,68 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
   }
 }
 
-hipError_t launch_rmsnorm(const float* x, int ldx, const uint16_t* g, float eps, uint16_t* h, int ldh, int rows,
-                          int d, hipStream_t s) {
+hipError_t launch_rmsnorm(float* x, int ldx, const uint16_t* g, float eps, uint16_t* h, int ldh, int rows, int d,
+                          const float* parts, int n_parts, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(rmsnorm_kernel, dim3(rows), dim3(256), 0, s, x, ldx, g, eps, h, ldh, d);
+  // one float4 per thread where the row allows
+  if (d >= 4096)
+    hipLaunchKernelGGL(rmsnorm_kernel<1024>, dim3(rows), dim3(1024), 0, s, x, ldx, g, eps, h, ldh, d, parts, n_parts,
+                       rows);
+  else
+    hipLaunchKernelGGL(rmsnorm_kernel<256>, dim3(rows), dim3(256), 0, s, x, ldx, g, eps, h, ldh, d, parts, n_parts,
+                       rows);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
 // RoPE on q and k (rotate-half pairs (i, i + hd/2)), bf16 rounding, and the
-// write of k and v into their page slot.  One block per token.
+// write of k and v into their page slot (K row-major, V transposed).  One
+// wave per (token, head) of the nq + 2 nkv heads; lane j < hd/2 takes the pair
+// (j, j + hd/2).  The qkv value is the sum of the GEMM's k slices in slice
+// order when the GEMM was split.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void rope_kv_kernel(const float* __restrict__ qkv, int nq, int nkv, int hd,
-                                                      const int32_t* __restrict__ pos,
-                                                      const int32_t* __restrict__ slot,
-                                                      const float2* __restrict__ rope, uint16_t* __restrict__ q,
-                                                      uint16_t* __restrict__ kv) {
-  const int t = blockIdx.x;
+__global__ __launch_bounds__(64) void rope_kv_kernel(const float* __restrict__ qkv, int n_parts, int T, int nq,
+                                                     int nkv, int hd, const int32_t* __restrict__ pos,
+                                                     const int32_t* __restrict__ slot,
+                                                     const float2* __restrict__ rope, uint16_t* __restrict__ q,
+                                                     uint16_t* __restrict__ kv) {
+  const int nh = nq + 2 * nkv;
+  const int t = blockIdx.x / nh, head = blockIdx.x % nh;
   const int half = hd / 2;
-  const int width = (nq + 2 * nkv) * hd;
-  const float* row = qkv + static_cast<size_t>(t) * width;
-  const float2* cs = rope + static_cast<size_t>(pos[t]) * half;
+  const int width = nh * hd;
+  const float* row = qkv + static_cast<size_t>(t) * width + head * hd;
+  const size_t pstride = static_cast<size_t>(T) * width;
+  auto val = [&](int i) {
+    float v = row[i];
+    for (int k = 1; k < n_parts; ++k) v += row[k * pstride + i];
+    return v;
+  };
+  const int j = threadIdx.x;
+  if (j >= half) return;
   const int sl = slot[t];
   const int page = sl / kPage, off = sl % kPage;
-  // rotated heads: nq query heads then nkv key heads, hd/2 pairs each
-  const int n_pairs = (nq + nkv) * half;
-  for (int i = threadIdx.x; i < n_pairs; i += blockDim.x) {
-    const int head = i / half, j = i % half;
-    const float a = row[head * hd + j], b = row[head * hd + j + half];
-    const float2 c = cs[j];
+  const float a = val(j), b = val(j + half);
+  if (head < nq + nkv) {
+    const float2 c = rope[static_cast<size_t>(pos[t]) * half + j];
     const float ra = a * c.x - b * c.y;
     const float rb = a * c.y + b * c.x;
-    if (head < nq) {
-      uint16_t* qr = q + static_cast<size_t>(t) * nq * hd + head * hd;
-      qr[j] = f32_to_bf16(ra);
-      qr[j + half] = f32_to_bf16(rb);
-    } else {
-      uint16_t* kr = kv + kv_offset(page, 0, nkv, head - nq, off, hd, 0);
-      kr[j] = f32_to_bf16(ra);
-      kr[j + half] = f32_to_bf16(rb);
-    }
-  }
-  const float* vr = row + (nq + nkv) * hd;
-  for (int i = threadIdx.x; i < nkv * hd; i += blockDim.x) {
-    const int head = i / hd, dd = i % hd;
-    kv[kv_offset(page, 1, nkv, head, off, hd, dd)] = f32_to_bf16(vr[i]);
+    uint16_t* dst = head < nq ? q + static_cast<size_t>(t) * nq * hd + head * hd
+                              : kv + kv_offset(page, 0, nkv, head - nq, off, hd, 0);
+    dst[j] = f32_to_bf16(ra);
+    dst[j + half] = f32_to_bf16(rb);
+  } else {
+    uint16_t* vt = kv + kv_offset(page, 1, nkv, head - nq - nkv, 0, hd, 0);
+    vt[j * kPage + off] = f32_to_bf16(a);
+    vt[(j + half) * kPage + off] = f32_to_bf16(b);
   }
 }
 
-hipError_t launch_rope_kv(const float* qkv, int T, int nq, int nkv, int hd, const int32_t* pos,
+hipError_t launch_rope_kv(const float* qkv, int n_parts, int T, int nq, int nkv, int hd, const int32_t* pos,
                           const int32_t* slot, const float2* rope, uint16_t* q, uint16_t* kv_layer,
                           hipStream_t s) {
   if (T <= 0) return hipSuccess;
-  hipLaunchKernelGGL(rope_kv_kernel, dim3(T), dim3(256), 0, s, qkv, nq, nkv, hd, pos, slot, rope, q, kv_layer);
+  hipLaunchKernelGGL(rope_kv_kernel, dim3(T * (nq + 2 * nkv)), dim3(64), 0, s, qkv, n_parts, T, nq, nkv, hd, pos,
+                     slot, rope, q, kv_layer);
   return hipGetLastError();
 }
 

@@ -11,6 +11,8 @@
 // Any fixed permutation of the reduction index is allowed as long as A and B
 // use the same one; the skinny kernel uses this to let each lane read 64
 // contiguous bytes of a W row per 128-wide k block.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -48,22 +50,28 @@ __device__ __forceinline__ void store_swiglu(f32x4 gt, f32x4 up, int m, int j, u
 }
 
 // ---------------------------------------------------------------------------
-// Skinny GEMM (M <= 16*MT, decode batches).  Weight streaming is the cost, so
-// one workgroup of 8 waves owns 16*NT rows of W and the whole K: wave w takes
-// the 128-wide k blocks w, w+8, ... (so the 8 waves read adjacent 256-byte
-// runs of each row), partial tiles are summed through LDS in a fixed order.
-// Lane (r = l%16, g = l/16) reads W[n0 + r][kb*128 + 32g .. +31] and the same
-// 32 k of its activation row; MFMA i of the block consumes elements 8i .. 8i+7.
+// Skinny GEMM (M <= 16*MT, decode batches).  Streaming W from HBM is the cost,
+// and every W row tile needs the activation rows of its k range, so each wave
+// owns NT = 4 row tiles (64 rows of W) to keep those activation reads at half
+// the W bytes.  A workgroup of 8 waves owns the 16*NT rows and a k slice
+// (grid.y = KS slices); wave w takes the 128-wide k blocks w, w+8, ... of the
+// slice.  Lane (r = l%16, g = l/16) reads W[n0 + r][k + 32i + 8g .. +7] for
+// MFMA i, so every load instruction covers 64 contiguous bytes of 16 rows.
+// Partial tiles of the 8 waves are summed through LDS in wave order; with
+// KS > 1 the slice sums go to part[slice][m][n] and the consumer kernel adds
+// the slices (in slice order) where it reads the result.
 // ---------------------------------------------------------------------------
-template <int MT, int NT, int EPI>
+template <int MT, int NT, int EPI, int PF>
 __global__ __launch_bounds__(512) void gemm_skinny_kernel(const uint16_t* __restrict__ X, int ldx,
-                                                          const uint16_t* __restrict__ W, int Kp, int M,
+                                                          const uint16_t* __restrict__ W, int Kp, int M, int N,
                                                           float* __restrict__ outf, uint16_t* __restrict__ outb,
-                                                          int ldo) {
+                                                          int ldo, float* __restrict__ part) {
   constexpr int NW = 8;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r = lane & 15, g = lane >> 4;
   const int n0 = blockIdx.x * 16 * NT;
+  const int KS = gridDim.y, slice = blockIdx.y;
+  const int kslice = Kp / KS, k0 = slice * kslice;
 
   f32x4 acc[NT][MT];
 #pragma unroll
@@ -73,35 +81,53 @@ __global__ __launch_bounds__(512) void gemm_skinny_kernel(const uint16_t* __rest
 
   const uint16_t* wrow[NT];
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) wrow[nt] = W + static_cast<size_t>(n0 + nt * 16 + r) * Kp + g * 32;
+  for (int nt = 0; nt < NT; ++nt) wrow[nt] = W + static_cast<size_t>(n0 + nt * 16 + r) * Kp + k0 + 8 * g;
   const uint16_t* xrow[MT];
   bool xok[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
     const int m = mt * 16 + r;
     xok[mt] = m < M;
-    xrow[mt] = X + static_cast<size_t>(xok[mt] ? m : 0) * ldx + g * 32;
+    xrow[mt] = X + static_cast<size_t>(xok[mt] ? m : 0) * ldx + k0 + 8 * g;
   }
 
-  const int nkb = Kp / 128;
-  for (int kb = wave; kb < nkb; kb += NW) {
-    const int k = kb * 128;
-    uint4 wv[NT][4], xv[MT][4];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) wv[nt][i] = *reinterpret_cast<const uint4*>(wrow[nt] + k + 8 * i);
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        xv[mt][i] = xok[mt] ? *reinterpret_cast<const uint4*>(xrow[mt] + k + 8 * i) : make_uint4(0, 0, 0, 0);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
+  // the wave's k blocks are wave, wave + NW, ...; PF of them are in flight in a
+  // register ring whose slots are refilled right after use (clamped, so every
+  // load is unconditional and each block waits only for its own loads)
+  const int nkb = kslice / 128;
+  const int nb = wave < nkb ? (nkb - wave + NW - 1) / NW : 0;
+  if (nb > 0) {
+    uint4 wv[PF][NT][4], xv[PF][MT][4];
+    auto load = [&](int sl, int j) {
+      const int k = (wave + NW * j) * 128;
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) acc[nt][mt] = mfma16(wv[nt][i], xv[mt][i], acc[nt][mt]);
+        for (int i = 0; i < 4; ++i) wv[sl][nt][i] = *reinterpret_cast<const uint4*>(wrow[nt] + k + 32 * i);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          xv[sl][mt][i] = xok[mt] ? *reinterpret_cast<const uint4*>(xrow[mt] + k + 32 * i) : make_uint4(0, 0, 0, 0);
+    };
+#pragma unroll
+    for (int sl = 0; sl < PF; ++sl) load(sl, min(sl, nb - 1));
+    for (int base = 0; base < nb; base += PF) {
+#pragma unroll
+      for (int sl = 0; sl < PF; ++sl) {
+        const int it = base + sl;
+        if (it < nb) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+              for (int mt = 0; mt < MT; ++mt) acc[nt][mt] = mfma16(wv[sl][nt][i], xv[sl][mt][i], acc[nt][mt]);
+        }
+        if (PF > 1) load(sl, min(it + PF, nb - 1));
+        else if (it + 1 < nb) load(sl, it + 1);
+      }
+    }
   }
 
   __shared__ f32x4 red[NW][NT * MT][kWave];
@@ -114,26 +140,58 @@ __global__ __launch_bounds__(512) void gemm_skinny_kernel(const uint16_t* __rest
   const int m_lane = r;  // activation row within a 16-row tile
   const int n_lane = 4 * g;
   if (EPI == kEpiSwiGLU) {
-    // NT == 2: tile 0 holds gate features, tile 1 up features of block n0/32
-    for (int mt = wave; mt < MT; mt += NW) {
-      f32x4 gs = red[0][mt][lane], us = red[0][MT + mt][lane];
+    // tiles (2p, 2p+1) hold the gate and up features of (gate, up) block n0/32 + p
+    for (int u = wave; u < (NT / 2) * MT; u += NW) {
+      const int pr = u / MT, mt = u % MT;
+      f32x4 gs = red[0][2 * pr * MT + mt][lane], us = red[0][(2 * pr + 1) * MT + mt][lane];
 #pragma unroll
       for (int w = 1; w < NW; ++w) {
-        gs += red[w][mt][lane];
-        us += red[w][MT + mt][lane];
+        gs += red[w][2 * pr * MT + mt][lane];
+        us += red[w][(2 * pr + 1) * MT + mt][lane];
       }
       const int m = mt * 16 + m_lane;
-      if (m < M) store_swiglu(gs, us, m, (n0 / 32) * 16 + n_lane, outb, ldo);
+      if (m < M) store_swiglu(gs, us, m, (n0 / 32 + pr) * 16 + n_lane, outb, ldo);
     }
   } else {
     for (int t = wave; t < NT * MT; t += NW) {
-      f32x4 s = red[0][t][lane];
+      f32x4 sum = red[0][t][lane];
 #pragma unroll
-      for (int w = 1; w < NW; ++w) s += red[w][t][lane];
+      for (int w = 1; w < NW; ++w) sum += red[w][t][lane];
       const int nt = t / MT, mt = t % MT;
       const int m = mt * 16 + m_lane;
-      if (m < M) store_tile<EPI>(s, m, n0 + nt * 16 + n_lane, outf, ldo);
+      if (m >= M) continue;
+      if (KS > 1)
+        store_tile<kEpiStoreF32>(sum, m, n0 + nt * 16 + n_lane, part + static_cast<size_t>(slice) * M * N, N);
+      else
+        store_tile<EPI>(sum, m, n0 + nt * 16 + n_lane, outf, ldo);
     }
+  }
+}
+
+// out[m, n] (=|+=) sum over slices of part[s][m][n], in slice order
+template <int EPI>
+__global__ __launch_bounds__(256) void reduce_parts_kernel(const float* __restrict__ part, int KS, int M, int N,
+                                                           float* __restrict__ out, int ldo) {
+  const int64_t n4 = static_cast<int64_t>(M) * N / 4;
+  for (int64_t e = blockIdx.x * 256ll + threadIdx.x; e < n4; e += static_cast<int64_t>(gridDim.x) * 256) {
+    const int m = static_cast<int>((4 * e) / N), n = static_cast<int>((4 * e) % N);
+    float4 s = reinterpret_cast<const float4*>(part)[e];
+    for (int k = 1; k < KS; ++k) {
+      const float4 v = reinterpret_cast<const float4*>(part + static_cast<size_t>(k) * M * N)[e];
+      s.x += v.x;
+      s.y += v.y;
+      s.z += v.z;
+      s.w += v.w;
+    }
+    float4* o = reinterpret_cast<float4*>(out + static_cast<size_t>(m) * ldo + n);
+    if (EPI == kEpiAddF32) {
+      const float4 x = *o;
+      s.x += x.x;
+      s.y += x.y;
+      s.z += x.z;
+      s.w += x.w;
+    }
+    *o = s;
   }
 }
 
@@ -233,19 +291,47 @@ __global__ __launch_bounds__(256) void gemm_tiled_kernel(const uint16_t* __restr
 
 // ---------------------------------------------------------------------------
 
+#ifndef METRO_SKINNY_PF
+#define METRO_SKINNY_PF 1
+#endif
+constexpr int kSkinnyPF = METRO_SKINNY_PF;  // k blocks in flight per wave
+
+int gemm_splits(int M, int N, int Kp, int epilogue) {
+  if (M > 64 || epilogue == kEpiSwiGLU) return 1;
+  const int nt = N % 64 == 0 ? 4 : 2;
+  const int wgs = N / (16 * nt);
+  int ks = 1;
+  // enough workgroups to cover the 256 CUs; each slice a multiple of 128
+  while (wgs * ks < 256 && ks < 8 && (Kp / (2 * ks)) % 128 == 0) ks *= 2;
+  return ks;
+}
+
+template <int MT, int NT, int EPI>
+static void launch_skinny(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, float* outf,
+                          uint16_t* outb, int ldo, float* part, int ks, hipStream_t s) {
+  hipLaunchKernelGGL((gemm_skinny_kernel<MT, NT, EPI, kSkinnyPF>), dim3(N / (16 * NT), ks), dim3(512), 0, s, X, ldx,
+                     W, Kp, M, N, outf, outb, ldo, part);
+}
+
+template <int NT, int EPI>
+static void launch_skinny_m(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, float* outf,
+                            uint16_t* outb, int ldo, float* part, int ks, hipStream_t s) {
+  if (M <= 16)
+    launch_skinny<1, NT, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, ks, s);
+  else if (M <= 32)
+    launch_skinny<2, NT, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, ks, s);
+  else
+    launch_skinny<4, NT, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, ks, s);
+}
+
 template <int EPI>
 static hipError_t launch_epi(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, float* outf,
-                             uint16_t* outb, int ldo, hipStream_t s) {
+                             uint16_t* outb, int ldo, float* part, int ks, hipStream_t s) {
   if (M <= 64) {
-    // SwiGLU needs a (gate, up) pair per workgroup
-    constexpr int NT = 2;
-    const dim3 grid(N / (16 * NT));
-    if (M <= 16)
-      hipLaunchKernelGGL((gemm_skinny_kernel<1, NT, EPI>), grid, dim3(512), 0, s, X, ldx, W, Kp, M, outf, outb, ldo);
-    else if (M <= 32)
-      hipLaunchKernelGGL((gemm_skinny_kernel<2, NT, EPI>), grid, dim3(512), 0, s, X, ldx, W, Kp, M, outf, outb, ldo);
+    if (N % 64 == 0)
+      launch_skinny_m<4, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, ks, s);
     else
-      hipLaunchKernelGGL((gemm_skinny_kernel<4, NT, EPI>), grid, dim3(512), 0, s, X, ldx, W, Kp, M, outf, outb, ldo);
+      launch_skinny_m<2, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, ks, s);
   } else {
     const dim3 grid((N + TBN - 1) / TBN, (M + TBM - 1) / TBM);
     hipLaunchKernelGGL((gemm_tiled_kernel<EPI>), grid, dim3(256), 0, s, X, ldx, W, Kp, M, N, outf, outb, ldo);
@@ -254,18 +340,32 @@ static hipError_t launch_epi(const uint16_t* X, int ldx, const uint16_t* W, int 
 }
 
 hipError_t launch_gemm(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, int epilogue,
-                       float* out_f32, uint16_t* out_bf16, int ldo, hipStream_t s) {
+                       float* out_f32, uint16_t* out_bf16, int ldo, float* part, int* n_parts, hipStream_t s) {
+  *n_parts = 0;
   if (M <= 0) return hipSuccess;
+  const int ks = part ? gemm_splits(M, N, Kp, epilogue) : 1;
+  if (ks > 1) *n_parts = ks;
   switch (epilogue) {
     case kEpiStoreF32:
-      return launch_epi<kEpiStoreF32>(X, ldx, W, Kp, M, N, out_f32, out_bf16, ldo, s);
+      return launch_epi<kEpiStoreF32>(X, ldx, W, Kp, M, N, out_f32, out_bf16, ldo, part, ks, s);
     case kEpiAddF32:
-      return launch_epi<kEpiAddF32>(X, ldx, W, Kp, M, N, out_f32, out_bf16, ldo, s);
+      return launch_epi<kEpiAddF32>(X, ldx, W, Kp, M, N, out_f32, out_bf16, ldo, part, ks, s);
     case kEpiSwiGLU:
-      return launch_epi<kEpiSwiGLU>(X, ldx, W, Kp, M, N, out_f32, out_bf16, ldo, s);
+      return launch_epi<kEpiSwiGLU>(X, ldx, W, Kp, M, N, out_f32, out_bf16, ldo, part, ks, s);
     default:
       return hipErrorInvalidValue;
   }
+}
+
+hipError_t launch_reduce_parts(const float* part, int KS, int M, int N, int epilogue, float* out, int ldo,
+                               hipStream_t s) {
+  const int64_t n4 = static_cast<int64_t>(M) * N / 4;
+  const int grid = static_cast<int>(std::min<int64_t>((n4 + 255) / 256, 4096));
+  if (epilogue == kEpiAddF32)
+    hipLaunchKernelGGL((reduce_parts_kernel<kEpiAddF32>), dim3(grid), dim3(256), 0, s, part, KS, M, N, out, ldo);
+  else
+    hipLaunchKernelGGL((reduce_parts_kernel<kEpiStoreF32>), dim3(grid), dim3(256), 0, s, part, KS, M, N, out, ldo);
+  return hipGetLastError();
 }
 
 }  // namespace metro

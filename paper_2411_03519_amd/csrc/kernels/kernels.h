@@ -15,13 +15,17 @@ hipError_t launch_embed(const int32_t* tok, const uint16_t* embed, int vocab, in
                         hipStream_t s);
 
 // h[r, :] = bf16(x[r, :] * rsqrt(mean(x[r, :]^2) + eps) * g); d % 4 == 0.
-hipError_t launch_rmsnorm(const float* x, int ldx, const uint16_t* g, float eps, uint16_t* h, int ldh, int rows,
-                          int d, hipStream_t s);
+// With n_parts > 0 the row first takes the pending GEMM slices:
+// x[r, :] += sum_s parts[s][r][:] (slice stride rows*d), written back to x.
+hipError_t launch_rmsnorm(float* x, int ldx, const uint16_t* g, float eps, uint16_t* h, int ldh, int rows, int d,
+                          const float* parts, int n_parts, hipStream_t s);
 
 // RoPE (rotate-half) on q and k of qkv [T, (nq+2nkv)*hd] fp32 at positions
 // pos[t]; q -> bf16 [T, nq*hd]; k, v -> bf16 into the KV slot slot[t]
-// (page*16 + offset) of this layer's slab.  rope is [max_pos][hd/2] (cos, sin).
-hipError_t launch_rope_kv(const float* qkv, int T, int nq, int nkv, int hd, const int32_t* pos,
+// (page*16 + offset) of this layer's slab (K row-major, V transposed).
+// rope is [max_pos][hd/2] (cos, sin).
+// With n_parts > 0, qkv is the first of n_parts slices [T][(nq+2nkv)hd] to sum.
+hipError_t launch_rope_kv(const float* qkv, int n_parts, int T, int nq, int nkv, int hd, const int32_t* pos,
                           const int32_t* slot, const float2* rope, uint16_t* q, uint16_t* kv_layer,
                           hipStream_t s);
 
@@ -54,33 +58,52 @@ enum GemmEpilogue {
 };
 
 // Y = X[M, Kp] (bf16, row stride ldx) x W[N, Kp]^T (bf16, packed row stride
-// Kp, Kp % 128 == 0, N % 16 == 0), fp32 accumulation, then the epilogue.
-// ldo is the row stride of the output in elements.
+// Kp, Kp % 128 == 0, N % 32 == 0), fp32 accumulation, then the epilogue.
+// ldo is the row stride of the output in elements.  With a workspace `part`
+// ([8][M][N] fp32) a decode-sized GEMM (M <= 64, fp32 epilogue) may split K
+// over workgroups: it then writes *n_parts > 0 slices part[s][m][n] instead of
+// applying the epilogue, and the consumer sums them in slice order.
 hipError_t launch_gemm(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, int epilogue,
-                       float* out_f32, uint16_t* out_bf16, int ldo, hipStream_t s);
+                       float* out_f32, uint16_t* out_bf16, int ldo, float* part, int* n_parts, hipStream_t s);
+int gemm_splits(int M, int N, int Kp, int epilogue);
+// Apply the fp32 epilogue to KS slices: out (=|+=) sum_s part[s].
+hipError_t launch_reduce_parts(const float* part, int KS, int M, int N, int epilogue, float* out, int ldo,
+                               hipStream_t s);
 
 // --- attention (attention.hip) ---------------------------------------------
 
+// KV page layout per (layer, page, kv head): K [16][hd] then V^T [hd][16].
 struct AttnArgs {
   const uint16_t* q;        // [rows_total, nq, hd] bf16 (row = query token)
   const uint16_t* kv;       // this layer's slab of the KV pool
-  const int32_t* work;      // [n_work][2]: (row, split)
   const int32_t* row_ctx;   // [rows]: keys visible to the row (0 .. ctx-1)
   const int32_t* row_qrow;  // [rows]: row of q / out for this row
   const int32_t* row_bt;    // [rows]: offset of the row's block table in bt
-  const int32_t* row_work;  // [rows]: first work item of the row
-  const int32_t* row_nsplit;// [rows]
   const int32_t* bt;        // block tables
-  float* part;              // [n_work][nkv][group][hd + 2] fp32 partials
   uint16_t* out;            // [rows_total, nq*hd] bf16
-  int n_work, rows, nq, nkv, hd, pages_per_split;
+  int rows, nq, nkv, hd;
   float scale;              // 1/sqrt(hd)
 };
 
-// Paged GQA attention, one work item = (row, split of pages_per_split pages)
-// x one kv head; rows with one split write out directly, others write
-// partials that launch_attn_combine merges.
-hipError_t launch_attn_paged(const AttnArgs& a, hipStream_t s);
-hipError_t launch_attn_combine(const AttnArgs& a, hipStream_t s);
+// Decode attention: one workgroup per (row, kv head).
+hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s);
+
+struct PrefillAttnArgs {
+  const uint16_t* q;        // [T, nq, hd] bf16
+  const uint16_t* kv;       // this layer's slab of the KV pool
+  uint16_t* out;            // [T, nq*hd] bf16
+  const int32_t* blocks;    // [n_blocks][3]: (item, first row, rows) of a query block
+  const int32_t* item_bt;   // [items]: offset of the item's block table in bt
+  const int32_t* pos;       // [T]: absolute position of each row
+  const int32_t* bt;        // block tables
+  int n_blocks, nq, nkv, hd;
+  float scale;
+};
+
+// Causal flash attention of prefill rows over their sequence's pages (which
+// already hold this call's keys).  Query blocks hold prefill_tokens_per_block
+// consecutive rows of one item.
+hipError_t launch_attn_prefill(const PrefillAttnArgs& a, hipStream_t s);
+int prefill_tokens_per_block(int group);
 
 }  // namespace metro

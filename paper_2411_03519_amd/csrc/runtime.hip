@@ -40,8 +40,6 @@ uint64_t splitmix64_host(uint64_t z) {
 }
 
 constexpr int kRing = 4;              // pinned descriptor buffers in flight
-constexpr int kDecodePagesPerSplit = 16;
-constexpr int kPrefillPagesPerSplit = 256;
 
 int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
 
@@ -84,7 +82,7 @@ struct metro_model {
   float* xr = nullptr;
   float* logits_ws = nullptr;
   int32_t* next_ws = nullptr;
-  float* part = nullptr;
+  float* parts = nullptr;    // k-slice sums of decode GEMMs, [8][64][max(qkv_n, d)]
   int32_t* desc_dev = nullptr;
   int64_t desc_cap = 0;  // int32 elements
   // host
@@ -193,17 +191,12 @@ struct Carve {
 int64_t desc_capacity(const metro_config& c) {
   const int64_t T = c.max_tokens, B = c.max_batch;
   const int64_t P = (c.max_context + 15) / 16;
-  const int64_t prefill = 8 * T + 2 * T * ((P + kPrefillPagesPerSplit - 1) / kPrefillPagesPerSplit) + B * P + 4 * B;
-  const int64_t decode = 7 * B + 2 * B * ((P + kDecodePagesPerSplit - 1) / kDecodePagesPerSplit) + B * P + 4 * B;
+  // tokens, positions, slots, last rows, item block tables, query blocks, block tables
+  const int64_t prefill = 3 * T + 2 * B + 3 * (T + B) + B * P;
+  // positions, slots, 3 per-row arrays, block tables
+  const int64_t decode = 5 * B + B * P;
   // + per-array rounding to 16 elements (at most 16 arrays per call)
   return std::max(prefill, decode) + 16 * 16 + 64;
-}
-
-int64_t work_capacity(const metro_config& c) {
-  const int64_t P = (c.max_context + 15) / 16;
-  return std::max<int64_t>(
-      int64_t(c.max_tokens) * ((P + kPrefillPagesPerSplit - 1) / kPrefillPagesPerSplit),
-      int64_t(c.max_batch) * ((P + kDecodePagesPerSplit - 1) / kDecodePagesPerSplit));
 }
 
 void free_model(metro_model* m) {
@@ -237,52 +230,69 @@ struct Desc {
   }
 };
 
-// Build per-row attention descriptors.  Row r attends to row_ctx[r] keys of
-// the block table at row_bt[r]; its work items are (r, 0 .. nsplit-1).
-struct RowPlan {
-  int32_t *ctx, *qrow, *bt, *work_off, *nsplit, *work;
-  int32_t n_work;
-};
-
-metro_status launch_layers(metro_model* m, int T, int rows, const int32_t* tok_dev, const int32_t* pos,
-                           const int32_t* slot, const metro::AttnArgs& attn_proto, hipStream_t s) {
+// The launch sequence of the decoder blocks over T rows; attention is the
+// decode kernel (dec) or the prefill kernel (pre).  Decode-sized GEMMs may
+// leave k-slice sums in m->parts; the kernel that next reads their result
+// (RMSNorm for the residual stream, RoPE for q/k/v) adds them.  On return
+// *x_parts says how many slices the residual stream still has to take.
+metro_status launch_layers(metro_model* m, int T, const int32_t* tok_dev, const int32_t* pos, const int32_t* slot,
+                           const metro::AttnArgs* dec, const metro::PrefillAttnArgs* pre, int* x_parts,
+                           hipStream_t s) {
   const metro_config& c = m->cfg;
   const int d = c.d_model;
+  int xp = 0, qp = 0;
   LAUNCH(m, METRO_K_EMBED, s, metro::launch_embed(tok_dev, m->embed, c.vocab, d, m->x, T, s));
   for (int l = 0; l < c.n_layers; ++l) {
     const Layer& L = m->layers[l];
     uint16_t* kv_l = m->kv + static_cast<size_t>(l) * m->layer_stride;
-    LAUNCH(m, METRO_K_RMSNORM, s, metro::launch_rmsnorm(m->x, d, L.attn_norm, c.rms_eps, m->h, d, T, d, s));
+    LAUNCH(m, METRO_K_RMSNORM, s,
+           metro::launch_rmsnorm(m->x, d, L.attn_norm, c.rms_eps, m->h, d, T, d, m->parts, xp, s));
     LAUNCH(m, METRO_K_GEMM_QKV, s,
-           metro::launch_gemm(m->h, d, L.wqkv, d, T, m->qkv_n, metro::kEpiStoreF32, m->qkv, nullptr, m->qkv_n, s));
+           metro::launch_gemm(m->h, d, L.wqkv, d, T, m->qkv_n, metro::kEpiStoreF32, m->qkv, nullptr, m->qkv_n,
+                              m->parts, &qp, s));
     LAUNCH(m, METRO_K_ROPE_KV, s,
-           metro::launch_rope_kv(m->qkv, T, c.n_heads, c.n_kv_heads, c.head_dim, pos, slot, m->rope, m->q, kv_l, s));
-    metro::AttnArgs a = attn_proto;
-    a.kv = kv_l;
-    LAUNCH(m, METRO_K_ATTENTION, s, metro::launch_attn_paged(a, s));
-    LAUNCH(m, METRO_K_ATTN_COMBINE, s, metro::launch_attn_combine(a, s));
+           metro::launch_rope_kv(qp ? m->parts : m->qkv, qp, T, c.n_heads, c.n_kv_heads, c.head_dim, pos, slot,
+                                 m->rope, m->q, kv_l, s));
+    if (dec) {
+      metro::AttnArgs a = *dec;
+      a.kv = kv_l;
+      LAUNCH(m, METRO_K_ATTENTION, s, metro::launch_attn_decode(a, s));
+    } else {
+      metro::PrefillAttnArgs a = *pre;
+      a.kv = kv_l;
+      LAUNCH(m, METRO_K_ATTENTION, s, metro::launch_attn_prefill(a, s));
+    }
     LAUNCH(m, METRO_K_GEMM_O, s,
-           metro::launch_gemm(m->o, m->q_dim, L.wo, m->q_dim, T, d, metro::kEpiAddF32, m->x, nullptr, d, s));
-    LAUNCH(m, METRO_K_RMSNORM, s, metro::launch_rmsnorm(m->x, d, L.ffn_norm, c.rms_eps, m->h, d, T, d, s));
+           metro::launch_gemm(m->o, m->q_dim, L.wo, m->q_dim, T, d, metro::kEpiAddF32, m->x, nullptr, d, m->parts,
+                              &xp, s));
+    LAUNCH(m, METRO_K_RMSNORM, s,
+           metro::launch_rmsnorm(m->x, d, L.ffn_norm, c.rms_eps, m->h, d, T, d, m->parts, xp, s));
+    int gp = 0;
     LAUNCH(m, METRO_K_GEMM_GATE_UP, s,
-           metro::launch_gemm(m->h, d, L.wgu, d, T, 2 * c.ffn_dim, metro::kEpiSwiGLU, nullptr, m->a, m->Fp, s));
+           metro::launch_gemm(m->h, d, L.wgu, d, T, 2 * c.ffn_dim, metro::kEpiSwiGLU, nullptr, m->a, m->Fp, nullptr,
+                              &gp, s));
     LAUNCH(m, METRO_K_GEMM_DOWN, s,
-           metro::launch_gemm(m->a, m->Fp, L.wdown, m->Fp, T, d, metro::kEpiAddF32, m->x, nullptr, d, s));
+           metro::launch_gemm(m->a, m->Fp, L.wdown, m->Fp, T, d, metro::kEpiAddF32, m->x, nullptr, d, m->parts, &xp,
+                              s));
   }
-  (void)rows;
+  *x_parts = xp;
   return METRO_OK;
 }
 
-metro_status launch_head(metro_model* m, const float* xrows, int R, float* logits, int32_t* next_tok,
+// Final RMSNorm (adding x_parts pending slices of the residual), LM head,
+// greedy argmax over R rows.
+metro_status launch_head(metro_model* m, float* xrows, int R, int x_parts, float* logits, int32_t* next_tok,
                          hipStream_t s) {
   const metro_config& c = m->cfg;
   float* lg = logits ? logits : m->logits_ws;
   int32_t* nt = next_tok ? next_tok : m->next_ws;
+  int lp = 0;
   LAUNCH(m, METRO_K_RMSNORM, s,
-         metro::launch_rmsnorm(xrows, c.d_model, m->final_norm, c.rms_eps, m->h, c.d_model, R, c.d_model, s));
+         metro::launch_rmsnorm(xrows, c.d_model, m->final_norm, c.rms_eps, m->h, c.d_model, R, c.d_model, m->parts,
+                               x_parts, s));
   LAUNCH(m, METRO_K_LM_HEAD, s,
          metro::launch_gemm(m->h, c.d_model, m->lm_head, c.d_model, R, c.vocab, metro::kEpiStoreF32, lg, nullptr,
-                            c.vocab, s));
+                            c.vocab, nullptr, &lp, s));
   if (next_tok || !logits) LAUNCH(m, METRO_K_ARGMAX, s, metro::launch_argmax(lg, c.vocab, R, nt, s));
   return METRO_OK;
 }
@@ -309,61 +319,6 @@ metro_status check_live(const metro_model* m) {
   if (!m) return fail(METRO_E_INVAL, "model is NULL");
   if (m->poisoned) return fail(METRO_E_HIP, "model is poisoned by an earlier HIP error");
   return METRO_OK;
-}
-
-// Fill the attention plan of `rows` rows; row r uses the block table at
-// bt_off[r] (into the bt array already in the descriptor) with ctx[r] keys.
-void plan_rows(Desc& d, int rows, const std::vector<int32_t>& ctx, const std::vector<int32_t>& qrow,
-               const std::vector<int32_t>& bt_off, int pages_per_split, RowPlan* rp) {
-  rp->ctx = d.put(rows);
-  rp->qrow = d.put(rows);
-  rp->bt = d.put(rows);
-  rp->work_off = d.put(rows);
-  rp->nsplit = d.put(rows);
-  int32_t nw = 0;
-  for (int r = 0; r < rows; ++r) {
-    const int pages = (ctx[r] + 15) / 16;
-    const int ns = (pages + pages_per_split - 1) / pages_per_split;
-    rp->ctx[r] = ctx[r];
-    rp->qrow[r] = qrow[r];
-    rp->bt[r] = bt_off[r];
-    rp->work_off[r] = nw;
-    rp->nsplit[r] = ns;
-    nw += ns;
-  }
-  rp->work = d.put(2 * static_cast<int64_t>(nw));
-  int32_t k = 0;
-  for (int r = 0; r < rows; ++r)
-    for (int sp = 0; sp < rp->nsplit[r]; ++sp) {
-      rp->work[2 * k] = r;
-      rp->work[2 * k + 1] = sp;
-      ++k;
-    }
-  rp->n_work = nw;
-}
-
-metro::AttnArgs attn_args(metro_model* m, const Desc& d, const RowPlan& rp, int32_t* bt_dev_ptr, int rows,
-                          int pages_per_split) {
-  auto dev = [&](const int32_t* hp) { return m->desc_dev + (hp - d.host); };
-  metro::AttnArgs a{};
-  a.q = m->q;
-  a.work = dev(rp.work);
-  a.row_ctx = dev(rp.ctx);
-  a.row_qrow = dev(rp.qrow);
-  a.row_bt = dev(rp.bt);
-  a.row_work = dev(rp.work_off);
-  a.row_nsplit = dev(rp.nsplit);
-  a.bt = bt_dev_ptr;
-  a.part = m->part;
-  a.out = m->o;
-  a.n_work = rp.n_work;
-  a.rows = rows;
-  a.nq = m->cfg.n_heads;
-  a.nkv = m->cfg.n_kv_heads;
-  a.hd = m->cfg.head_dim;
-  a.pages_per_split = pages_per_split;
-  a.scale = 1.0f / std::sqrt(static_cast<float>(m->cfg.head_dim));
-  return a;
 }
 
 }  // namespace
@@ -442,12 +397,11 @@ metro_status metro_create_model(const metro_config* cfg, uint64_t init_seed, met
 
   // ---- scratch
   const int64_t Tm = std::max(c.max_tokens, c.max_batch);
-  const int64_t work_cap = work_capacity(c);
   m->desc_cap = desc_capacity(c);
   {
     const size_t bytes = Tm * d * 4 + Tm * d * 2 + Tm * m->qkv_n * 4 + 2 * Tm * m->q_dim * 2 + Tm * m->Fp * 2 +
                          int64_t(c.max_batch) * d * 4 + int64_t(c.max_batch) * V * 4 + int64_t(c.max_batch) * 4 +
-                         work_cap * nkv * m->group * (hd + 2) * 4 + m->desc_cap * 4 + 256 * 16;
+                         8LL * 64 * std::max(m->qkv_n, d) * 4 + m->desc_cap * 4 + 256 * 16;
     m->scratch_bytes = bytes;
     e = hipMalloc(&m->sbase, bytes);
     if (e != hipSuccess) return bail(fail(METRO_E_NOMEM, "hipMalloc of %zu scratch bytes failed", bytes));
@@ -461,7 +415,7 @@ metro_status metro_create_model(const metro_config* cfg, uint64_t init_seed, met
     m->xr = cv.take<float>(int64_t(c.max_batch) * d);
     m->logits_ws = cv.take<float>(int64_t(c.max_batch) * V);
     m->next_ws = cv.take<int32_t>(c.max_batch);
-    m->part = cv.take<float>(work_cap * nkv * m->group * (hd + 2));
+    m->parts = cv.take<float>(8LL * 64 * std::max(m->qkv_n, d));
     m->desc_dev = cv.take<int32_t>(m->desc_cap);
     // the SwiGLU output's padding columns must read as zero
     e = hipMemset(m->a, 0, Tm * m->Fp * 2);
@@ -705,34 +659,55 @@ metro_status metro_prefill_chunk(metro_model* m, int32_t n_items, const int64_t*
   int64_t bt_total = 0;
   for (int i = 0; i < n_items; ++i) bt_total += m->seqs->find(seqs[i])->pages.size();
   int32_t* bt = d.put(bt_total);
-  std::vector<int32_t> row_ctx(T), row_q(T), row_bt(T);
-  int64_t bo = 0;
+  int32_t* item_bt = d.put(n_items);
+  const int tpb = metro::prefill_tokens_per_block(m->group);
+  int64_t n_blocks = 0;
+  for (int i = 0; i < n_items; ++i) n_blocks += (add[i] + tpb - 1) / tpb;
+  int32_t* blocks = d.put(3 * n_blocks);
+  int64_t bo = 0, nb = 0;
   for (int i = 0; i < n_items; ++i) {
     const metro::Sequence* s = m->seqs->find(seqs[i]);
     std::copy(s->pages.begin(), s->pages.end(), bt + bo);
+    item_bt[i] = static_cast<int32_t>(bo);
     for (int t = cu[i]; t < cu[i + 1]; ++t) {
       const int p = s->length + (t - cu[i]);
       pos[t] = p;
       slot[t] = s->pages[p / 16] * 16 + p % 16;
-      row_ctx[t] = p + 1;
-      row_q[t] = t;
-      row_bt[t] = static_cast<int32_t>(bo);
+    }
+    for (int r0 = cu[i]; r0 < cu[i + 1]; r0 += tpb) {
+      blocks[3 * nb] = i;
+      blocks[3 * nb + 1] = r0;
+      blocks[3 * nb + 2] = std::min(tpb, cu[i + 1] - r0);
+      ++nb;
     }
     last[i] = cu[i + 1] - 1;
     bo += s->pages.size();
   }
-  RowPlan rp{};
-  plan_rows(d, T, row_ctx, row_q, row_bt, kPrefillPagesPerSplit, &rp);
   m->cur_phase = 1;
   hipStream_t s = static_cast<hipStream_t>(stream);
   st = upload_ring(m, d, s);
   if (st != METRO_OK) return st;
   auto dev = [&](const int32_t* hp) { return m->desc_dev + (hp - d.host); };
-  metro::AttnArgs a = attn_args(m, d, rp, dev(bt), T, kPrefillPagesPerSplit);
-  st = launch_layers(m, T, T, dev(tok), dev(pos), dev(slot), a, s);
+  metro::PrefillAttnArgs pa{};
+  pa.q = m->q;
+  pa.out = m->o;
+  pa.blocks = dev(blocks);
+  pa.item_bt = dev(item_bt);
+  pa.pos = dev(pos);
+  pa.bt = dev(bt);
+  pa.n_blocks = static_cast<int>(n_blocks);
+  pa.nq = c.n_heads;
+  pa.nkv = c.n_kv_heads;
+  pa.hd = c.head_dim;
+  pa.scale = 1.0f / std::sqrt(static_cast<float>(c.head_dim));
+  int xp = 0;
+  st = launch_layers(m, T, dev(tok), dev(pos), dev(slot), nullptr, &pa, &xp, s);
   if (st != METRO_OK) return st;
+  if (xp > 0)
+    LAUNCH(m, METRO_K_GEMM_DOWN, s,
+           metro::launch_reduce_parts(m->parts, xp, T, c.d_model, metro::kEpiAddF32, m->x, c.d_model, s));
   LAUNCH(m, METRO_K_EMBED, s, metro::launch_gather_rows(m->x, c.d_model, dev(last), n_items, m->xr, s));
-  st = launch_head(m, m->xr, n_items, logits, next_tok, s);
+  st = launch_head(m, m->xr, n_items, 0, logits, next_tok, s);
   if (st != METRO_OK) return st;
   m->seqs->commit(seqs, add.data(), n_items);
   return METRO_OK;
@@ -760,7 +735,9 @@ metro_status metro_decode_step(metro_model* m, int32_t B, const int64_t* seqs, c
   int64_t bt_total = 0;
   for (int i = 0; i < B; ++i) bt_total += m->seqs->find(seqs[i])->pages.size();
   int32_t* bt = d.put(bt_total);
-  std::vector<int32_t> row_ctx(B), row_q(B), row_bt(B);
+  int32_t* row_ctx = d.put(B);
+  int32_t* row_q = d.put(B);
+  int32_t* row_bt = d.put(B);
   int64_t bo = 0;
   for (int i = 0; i < B; ++i) {
     const metro::Sequence* s = m->seqs->find(seqs[i]);
@@ -773,17 +750,27 @@ metro_status metro_decode_step(metro_model* m, int32_t B, const int64_t* seqs, c
     row_bt[i] = static_cast<int32_t>(bo);
     bo += s->pages.size();
   }
-  RowPlan rp{};
-  plan_rows(d, B, row_ctx, row_q, row_bt, kDecodePagesPerSplit, &rp);
   m->cur_phase = 2;
   hipStream_t s = static_cast<hipStream_t>(stream);
   st = upload_ring(m, d, s);
   if (st != METRO_OK) return st;
   auto dev = [&](const int32_t* hp) { return m->desc_dev + (hp - d.host); };
-  metro::AttnArgs a = attn_args(m, d, rp, dev(bt), B, kDecodePagesPerSplit);
-  st = launch_layers(m, B, B, tokens_dev, dev(pos), dev(slot), a, s);
+  metro::AttnArgs a{};
+  a.q = m->q;
+  a.row_ctx = dev(row_ctx);
+  a.row_qrow = dev(row_q);
+  a.row_bt = dev(row_bt);
+  a.bt = dev(bt);
+  a.out = m->o;
+  a.rows = B;
+  a.nq = c.n_heads;
+  a.nkv = c.n_kv_heads;
+  a.hd = c.head_dim;
+  a.scale = 1.0f / std::sqrt(static_cast<float>(c.head_dim));
+  int xp = 0;
+  st = launch_layers(m, B, tokens_dev, dev(pos), dev(slot), &a, nullptr, &xp, s);
   if (st != METRO_OK) return st;
-  st = launch_head(m, m->x, B, logits, next_tok, s);
+  st = launch_head(m, m->x, B, xp, logits, next_tok, s);
   if (st != METRO_OK) return st;
   m->seqs->commit(seqs, add.data(), B);
   return METRO_OK;
@@ -793,7 +780,7 @@ metro_status metro_profile_start(metro_model* m, int32_t cls, int32_t phase) {
   g_err.clear();
   metro_status st = check_live(m);
   if (st != METRO_OK) return st;
-  if (cls < METRO_K_EMBED || cls > METRO_K_ARGMAX || phase < 0 || phase > 2)
+  if (cls < METRO_K_EMBED || cls > METRO_K_ARGMAX || cls == 5 || phase < 0 || phase > 2)
     return fail(METRO_E_INVAL, "profile: bad kernel class %d or phase %d", cls, phase);
   HIP_TRY(m, hipSetDevice(m->device));
   if (m->prof_ev.empty()) {
@@ -832,24 +819,28 @@ metro_status metro_profile_stop(metro_model* m, double* total_ms, int64_t* launc
 // ---------------------------------------------------------------------------
 
 metro_status metro_op_gemm(const uint16_t* X, int32_t ldx, const uint16_t* W, int32_t Kp, int32_t M, int32_t N,
-                           int32_t epilogue, float* out_f32, uint16_t* out_bf16, int32_t ldo, void* stream) {
+                           int32_t epilogue, float* out_f32, uint16_t* out_bf16, int32_t ldo, float* workspace,
+                           void* stream) {
   g_err.clear();
   if (!X || !W || M < 0 || N <= 0 || Kp <= 0 || Kp % 128 || N % 32 || ldx < Kp)
     return fail(METRO_E_INVAL, "gemm: bad shape (Kp %% 128, N %% 32, ldx >= Kp required)");
   if (epilogue == metro::kEpiSwiGLU ? !out_bf16 : !out_f32) return fail(METRO_E_INVAL, "gemm: output is NULL");
   if ((epilogue == metro::kEpiSwiGLU ? ldo < N / 2 : ldo < N) || ldo % 4)
     return fail(METRO_E_INVAL, "gemm: bad ldo");
-  hipError_t e = metro::launch_gemm(X, ldx, W, Kp, M, N, epilogue, out_f32, out_bf16, ldo,
+  int parts = 0;
+  hipError_t e = metro::launch_gemm(X, ldx, W, Kp, M, N, epilogue, out_f32, out_bf16, ldo, workspace, &parts,
                                     static_cast<hipStream_t>(stream));
+  if (e == hipSuccess && parts > 0)
+    e = metro::launch_reduce_parts(workspace, parts, M, N, epilogue, out_f32, ldo, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(nullptr, e, "launch_gemm");
   return METRO_OK;
 }
 
-metro_status metro_op_rmsnorm(const float* x, const uint16_t* g, float eps, uint16_t* h, int32_t rows, int32_t d,
+metro_status metro_op_rmsnorm(float* x, const uint16_t* g, float eps, uint16_t* h, int32_t rows, int32_t d,
                               void* stream) {
   g_err.clear();
   if (!x || !g || !h || rows < 0 || d <= 0 || d % 4) return fail(METRO_E_INVAL, "rmsnorm: bad arguments");
-  hipError_t e = metro::launch_rmsnorm(x, d, g, eps, h, d, rows, d, static_cast<hipStream_t>(stream));
+  hipError_t e = metro::launch_rmsnorm(x, d, g, eps, h, d, rows, d, nullptr, 0, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(nullptr, e, "launch_rmsnorm");
   return METRO_OK;
 }

@@ -28,7 +28,7 @@ WEIGHT_ID = {"embed": 0, "final_norm": 1, "lm_head": 2, "attn_norm": 3, "wq": 4,
 
 EPI_STORE_F32, EPI_ADD_F32, EPI_SWIGLU = 0, 1, 2
 
-KERNEL_CLASS = {"embed": 0, "rmsnorm": 1, "gemm_qkv": 2, "rope_kv": 3, "attention": 4, "attn_combine": 5,
+KERNEL_CLASS = {"embed": 0, "rmsnorm": 1, "gemm_qkv": 2, "rope_kv": 3, "attention": 4,
                 "gemm_o": 6, "gemm_gate_up": 7, "gemm_down": 8, "lm_head": 9, "argmax": 10}
 PHASE = {"any": 0, "prefill": 1, "decode": 2}
 
@@ -66,7 +66,7 @@ _SIGS = {
     "metro_decode_step": (_i32, [_vp, _i32, _vp, _vp, _vp, _vp, _vp]),
     "metro_profile_start": (_i32, [_vp, _i32, _i32]),
     "metro_profile_stop": (_i32, [_vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_i64)]),
-    "metro_op_gemm": (_i32, [_vp, _i32, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _i32, _vp]),
+    "metro_op_gemm": (_i32, [_vp, _i32, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp]),
     "metro_op_rmsnorm": (_i32, [_vp, _vp, ctypes.c_float, _vp, _i32, _i32, _vp]),
     "metro_op_argmax": (_i32, [_vp, _i32, _i32, _vp, _vp]),
 }
@@ -225,11 +225,12 @@ class Model:
 
 # -- single-op entry points -------------------------------------------------------
 
-def op_gemm(X, W, M: int, N: int, Kp: int, epilogue: int, out, ldo: int, ldx: int | None = None, stream=None):
+def op_gemm(X, W, M: int, N: int, Kp: int, epilogue: int, out, ldo: int, ldx: int | None = None, workspace=None,
+            stream=None):
     f32 = out if epilogue != EPI_SWIGLU else None
     b16 = out if epilogue == EPI_SWIGLU else None
     check(lib.metro_op_gemm(_ptr(X), ldx if ldx is not None else Kp, _ptr(W), Kp, M, N, epilogue, _ptr(f32),
-                            _ptr(b16), ldo, _stream(stream)))
+                            _ptr(b16), ldo, _ptr(workspace), _stream(stream)))
 
 
 def op_rmsnorm(x, g, eps: float, h, rows: int, d: int, stream=None):

@@ -38,10 +38,11 @@ GEMM_CASES = [(1, 256, 64), (7, 640, 96), (16, 256, 32), (25, 4096, 512), (33, 7
               (65, 256, 160), (200, 1152, 416), (129, 128, 96), (300, 4096, 256)]
 
 
-@pytest.mark.parametrize("M,K,N", GEMM_CASES)
+@pytest.mark.parametrize("M,K,N", GEMM_CASES + [(25, 14336, 512), (3, 1024, 4096)])
 @pytest.mark.parametrize("epi", [0, 1])
-def test_gemm_f32_epilogues(metro, M, K, N, epi):
-    print(f"gemm M={M} K={K} N={N} epi={epi}", flush=True)
+@pytest.mark.parametrize("split", [False, True])
+def test_gemm_f32_epilogues(metro, M, K, N, epi, split):
+    print(f"gemm M={M} K={K} N={N} epi={epi} split={split}", flush=True)
     rng = np.random.default_rng(M * 7 + K + N + epi)
     Kp = (K + 127) // 128 * 128
     X = np.zeros((M, Kp), np.uint16)
@@ -52,7 +53,8 @@ def test_gemm_f32_epilogues(metro, M, K, N, epi):
     ldo = N + 4
     init = rng.standard_normal((M, ldo)).astype(np.float32)
     out = torch.from_numpy(init.copy()).cuda()
-    metro.op_gemm(dev_u16(X), dev_u16(W), M, N, Kp, epi, out, ldo)
+    ws = torch.full((8, M, N), float("nan"), device="cuda") if split else None
+    metro.op_gemm(dev_u16(X), dev_u16(W), M, N, Kp, epi, out, ldo, workspace=ws)
     torch.cuda.synchronize()
     got = out.cpu().numpy().astype(np.float64)
     want = ref + (init[:, :N] if epi == 1 else 0.0)

@@ -138,7 +138,7 @@ def test_decode_rows_independent_of_batch_composition(metro):
     w = synth.llama_weights(synth.TINY, 1)
     rng = np.random.default_rng(21)
     prompts = [rng.integers(0, 4096, int(rng.integers(20, 90))) for _ in range(40)]
-    with make_model(metro, synth.TINY, w) as m:
+    with make_model(metro, synth.TINY, w, max_seqs=128) as m:
         seqs = [m.seq_open() for _ in prompts]
         for g in range(0, 40, 10):
             m.prefill_chunk(seqs[g:g + 10], prompts[g:g + 10])
