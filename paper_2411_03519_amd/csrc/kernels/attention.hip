@@ -1,8 +1,9 @@
 // Paged grouped-query attention on gfx950 with MFMA.
 //
-// KV page layout (per layer, page, kv head): K as [16 keys][hd] and V
-// transposed as [hd][16 keys], both bf16.  With those two layouts every
-// matrix-core operand is a contiguous run of a page:
+// KV page layout (per layer, page, kv head): K and V^T tiles of 16 keys x hd
+// in the layouts of common.h (k_tile_offset, vt_tile_offset), bf16: every
+// matrix-core operand is one 16-byte load per lane and every load instruction
+// reads 1 KiB of a tile contiguously.
 //
 //   scores  S^T[key][q] = sum_d K[key][d] Q[q][d]       v_mfma_f32_16x16x32_bf16
 //           A = K rows (16 keys), B = Q^T (16 query columns)
@@ -19,10 +20,13 @@
 // P enters the bf16 matrix core as hi = bf16(p) plus lo = bf16(p - hi) (two
 // MFMAs), which keeps p to about 16 significant bits.
 //
-// Decode: one workgroup per (row, kv head); its eight waves take the row's
-// pages round-robin and merge through LDS in wave order, so the result of a
-// row never depends on the rest of the batch and needs no cross-workgroup
-// merge (an agent-scope fence per workgroup is costly on the multi-XCD chip).
+// Decode: one workgroup per (work item, kv head), a work item being up to 32
+// pages of one row, so that long rows spread over several CUs; its waves take
+// the pages round-robin and merge through LDS in wave order.  Rows of several
+// work items leave their states in a workspace and a small kernel merges them
+// in split order (an agent-scope fence in every workgroup, which an in-kernel
+// merge would need, costs L2 write-backs on the multi-XCD chip).  The split
+// count depends on the row's own context length only, never on the batch.
 //
 // Prefill (flash attention): one workgroup = (query block, kv head); the K and
 // V pages of the block's visible context go through LDS in pairs (double
@@ -58,33 +62,38 @@ __device__ __forceinline__ void split_bf16(float p0, float p1, uint32_t& hi, uin
 // ===========================================================================
 
 // One workgroup of kDecodeWaves waves per (row, kv head); wave w takes pages
-// w, w + kDecodeWaves, ... (several pages in flight in registers) and the
-// waves' (max, sum, output) states are merged through LDS in wave order.
-constexpr int kDecodeWaves = 8;
+// w, w + kDecodeWaves, ...  The wave's page ids are read once into one VGPR
+// (lane j holds the id of the wave's j-th page, 64 pages per pass) so the page
+// loop never waits on a memory lookup; kDecodeRing pages of K/V are kept in
+// flight in a register ring.  The waves' (max, sum, output) states are merged
+// through LDS in wave order.
+constexpr int kDecodeWaves = 4;
+constexpr int kDecodeRing = 2;
 
-template <int HD, int G>
-__global__ __launch_bounds__(kDecodeWaves * 64) void attn_decode_kernel(AttnArgs a) {
+template <int HD, int G, int NW, int PD>
+__global__ __launch_bounds__(NW * 64) void attn_decode_kernel(AttnArgs a) {
   constexpr int KQ = HD / 32;  // score MFMAs per page
-  constexpr int NT = HD / 16;  // output tiles
-  constexpr int NW = kDecodeWaves;
+  constexpr int NT = HD / 16;  // output tiles (pairs share one 16-byte V load)
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
-  const int row = blockIdx.x / a.nkv, h = blockIdx.x % a.nkv;
+  const int wi = blockIdx.x / a.nkv, h = blockIdx.x % a.nkv;
+  const int row = a.work[2 * wi], split = a.work[2 * wi + 1];
   const int ctx = a.row_ctx[row];
   const int qrow = a.row_qrow[row];
-  const int32_t* bt = a.bt + a.row_bt[row];
-  const int n_pages = ceil_div(ctx, kPage);
+  const int p0 = split * kDecodePagesPerSplit;
+  const int32_t* bt = a.bt + a.row_bt[row] + p0;
+  const int n_pages = min(ceil_div(ctx, kPage) - p0, kDecodePagesPerSplit);  // pages of this split
   const float qscale = a.scale * kLog2e;
 
-  // Q^T operand: column col = head h*G + col (zero beyond the group);
-  // lane group grp holds dims grp*HD/4 .. +HD/4, MFMA i takes 8 of them.
+  // Q^T operand: column col = head h*G + col (zero beyond the group); MFMA i
+  // takes dims 32i + 8grp .. +7, matching the K tile layout.
   uint4 qf[KQ];
 #pragma unroll
   for (int i = 0; i < KQ; ++i) qf[i] = make_uint4(0, 0, 0, 0);
   if (col < G) {
-    const uint16_t* qp = a.q + (static_cast<size_t>(qrow) * a.nq + h * G + col) * HD + grp * (HD / 4);
+    const uint16_t* qp = a.q + (static_cast<size_t>(qrow) * a.nq + h * G + col) * HD;
 #pragma unroll
-    for (int i = 0; i < KQ; ++i) qf[i] = *reinterpret_cast<const uint4*>(qp + 8 * i);
+    for (int i = 0; i < KQ; ++i) qf[i] = *reinterpret_cast<const uint4*>(qp + 32 * i + 8 * grp);
   }
 
   f32x4 o[NT];
@@ -92,33 +101,32 @@ __global__ __launch_bounds__(kDecodeWaves * 64) void attn_decode_kernel(AttnArgs
   for (int t = 0; t < NT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m = kNegBig, l = 0.f;
 
-  // K operand: key row col, permuted dims; V^T operand: dims 16t + col, keys
-  // 4grp..4grp+3.  The wave's pages are w, w+NW, ...; PD of them are kept in
-  // flight in a register ring, each slot refilled right after use with an
-  // unconditional (clamped) load so every page waits only for itself.
-  constexpr int PD = 3;
   uint4 kf[PD][KQ];
-  uint2 vf[PD][NT];
-  auto load_page = [&](int sl, int p) {
-    const int page = bt[p];
-    const uint16_t* kp = a.kv + kv_offset(page, 0, a.nkv, h, 0, HD, 0);
-    const uint16_t* vp = a.kv + kv_offset(page, 1, a.nkv, h, 0, HD, 0);
+  uint4 vf[PD][NT / 2];
+  const size_t koff = kv_offset(0, 0, a.nkv, h, 0, HD, 0), voff = kv_offset(0, 1, a.nkv, h, 0, HD, 0);
+  const size_t pstride = static_cast<size_t>(2) * a.nkv * kPage * HD;
+  auto load_page = [&](int sl, int page) {
+    const uint16_t* kp = a.kv + static_cast<size_t>(page) * pstride + koff;
+    const uint16_t* vp = a.kv + static_cast<size_t>(page) * pstride + voff;
 #pragma unroll
-    for (int i = 0; i < KQ; ++i)
-      kf[sl][i] = *reinterpret_cast<const uint4*>(kp + col * HD + grp * (HD / 4) + 8 * i);
+    for (int i = 0; i < KQ; ++i) kf[sl][i] = *reinterpret_cast<const uint4*>(kp + 512 * i + 8 * lane);
 #pragma unroll
-    for (int t = 0; t < NT; ++t) vf[sl][t] = *reinterpret_cast<const uint2*>(vp + (16 * t + col) * kPage + 4 * grp);
+    for (int c = 0; c < NT / 2; ++c) vf[sl][c] = *reinterpret_cast<const uint4*>(vp + 512 * c + 8 * lane);
   };
+
   const int np = wave < n_pages ? (n_pages - wave + NW - 1) / NW : 0;
-  if (np > 0) {
+  for (int j0 = 0; j0 < np; j0 += 64) {
+    const int nj = min(64, np - j0);
+    // lane j: id of the wave's page j0 + j
+    const int pid = lane < nj ? bt[wave + NW * (j0 + lane)] : 0;
 #pragma unroll
-    for (int sl = 0; sl < PD; ++sl) load_page(sl, wave + NW * min(sl, np - 1));
-    for (int base = 0; base < np; base += PD) {
+    for (int sl = 0; sl < PD; ++sl) load_page(sl, __builtin_amdgcn_readlane(pid, min(sl, nj - 1)));
+    for (int base = 0; base < nj; base += PD) {
 #pragma unroll
       for (int sl = 0; sl < PD; ++sl) {
         const int it = base + sl;
-        if (it < np) {
-          const int p = wave + NW * it;
+        if (it < nj) {
+          const int p = p0 + wave + NW * (j0 + it);
           f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int i = 0; i < KQ; ++i) s = mfma_k32(kf[sl][i], qf[i], s);
@@ -139,13 +147,17 @@ __global__ __launch_bounds__(kDecodeWaves * 64) void attn_decode_kernel(AttnArgs
           split_bf16(pv[0], pv[1], hi.x, lo.x);
           split_bf16(pv[2], pv[3], hi.y, lo.y);
 #pragma unroll
-          for (int t = 0; t < NT; ++t) {
-            o[t] *= corr;
-            o[t] = mfma_k16(vf[sl][t], hi, o[t]);
-            o[t] = mfma_k16(vf[sl][t], lo, o[t]);
+          for (int c = 0; c < NT / 2; ++c) {
+            const uint2 v0 = make_uint2(vf[sl][c].x, vf[sl][c].y), v1 = make_uint2(vf[sl][c].z, vf[sl][c].w);
+            o[2 * c] *= corr;
+            o[2 * c] = mfma_k16(v0, hi, o[2 * c]);
+            o[2 * c] = mfma_k16(v0, lo, o[2 * c]);
+            o[2 * c + 1] *= corr;
+            o[2 * c + 1] = mfma_k16(v1, hi, o[2 * c + 1]);
+            o[2 * c + 1] = mfma_k16(v1, lo, o[2 * c + 1]);
           }
         }
-        load_page(sl, wave + NW * min(it + PD, np - 1));
+        load_page(sl, __builtin_amdgcn_readlane(pid, min(it + PD, nj - 1)));
       }
     }
   }
@@ -153,7 +165,7 @@ __global__ __launch_bounds__(kDecodeWaves * 64) void attn_decode_kernel(AttnArgs
   l += __shfl_xor(l, 32, kWave);
 
   // merge the waves in order
-  __shared__ float sm[NW][G], sl[NW][G];
+  __shared__ float sm[NW][G], sl_[NW][G];
   __shared__ float so[NW][HD][G];
   if (col < G) {
 #pragma unroll
@@ -162,10 +174,11 @@ __global__ __launch_bounds__(kDecodeWaves * 64) void attn_decode_kernel(AttnArgs
       for (int i = 0; i < 4; ++i) so[wave][16 * t + 4 * grp + i][col] = o[t][i];
     if (grp == 0) {
       sm[wave][col] = m;
-      sl[wave][col] = l;
+      sl_[wave][col] = l;
     }
   }
   __syncthreads();
+  const bool whole = a.row_nsplit[row] == 1;
   for (int idx = threadIdx.x; idx < G * HD; idx += blockDim.x) {
     const int g = idx / HD, d = idx % HD;
     float M = sm[0][g];
@@ -175,11 +188,43 @@ __global__ __launch_bounds__(kDecodeWaves * 64) void attn_decode_kernel(AttnArgs
 #pragma unroll
     for (int w = 0; w < NW; ++w) {
       const float f = exp2f(sm[w][g] - M);
-      L += sl[w][g] * f;
+      L += sl_[w][g] * f;
       O += so[w][d][g] * f;
     }
-    a.out[(static_cast<size_t>(qrow) * a.nq + h * G + g) * HD + d] = f32_to_bf16(O / L);
+    if (whole) {
+      a.out[(static_cast<size_t>(qrow) * a.nq + h * G + g) * HD + d] = f32_to_bf16(O / L);
+    } else {
+      float* pp = a.part + ((static_cast<size_t>(wi) * a.nkv + h) * G + g) * (HD + 2);
+      pp[d] = O;
+      if (d == 0) {
+        pp[HD] = M;
+        pp[HD + 1] = L;
+      }
+    }
   }
+}
+
+// Merge the split states of each (row, query head) in split order.  One block
+// of hd threads per (row, head); rows with a single split are already final.
+__global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
+  const int row = blockIdx.x / a.nq, j = blockIdx.x % a.nq;
+  const int ns = a.row_nsplit[row];
+  if (ns == 1) return;
+  const int G = a.nq / a.nkv, hd = a.hd;
+  const int h = j / G, g = j % G;
+  const int w0 = a.row_work[row];
+  const int d = threadIdx.x;
+  auto state = [&](int s2) { return a.part + ((static_cast<size_t>(w0 + s2) * a.nkv + h) * G + g) * (hd + 2); };
+  float M = kNegBig;
+  for (int s2 = 0; s2 < ns; ++s2) M = fmaxf(M, state(s2)[hd]);
+  float L = 0.f, O = 0.f;
+  for (int s2 = 0; s2 < ns; ++s2) {
+    const float* pp = state(s2);
+    const float f = exp2f(pp[hd] - M);
+    L += pp[hd + 1] * f;
+    O += pp[d] * f;
+  }
+  a.out[(static_cast<size_t>(a.row_qrow[row]) * a.nq + j) * hd + d] = f32_to_bf16(O / L);
 }
 
 // ===========================================================================
@@ -220,10 +265,10 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(PrefillAttnArgs a) {
     qok[n] = tok < nrows;
     qrow[n] = row0 + (qok[n] ? tok : 0);
     qpos[n] = qok[n] ? a.pos[qrow[n]] : -1;
-    const uint16_t* qp = a.q + (static_cast<size_t>(qrow[n]) * a.nq + h * G + col % G) * HD + grp * (HD / 4);
+    const uint16_t* qp = a.q + (static_cast<size_t>(qrow[n]) * a.nq + h * G + col % G) * HD + 8 * grp;
 #pragma unroll
     for (int i = 0; i < KQ; ++i)
-      qf[n][i] = qok[n] ? *reinterpret_cast<const uint4*>(qp + 8 * i) : make_uint4(0, 0, 0, 0);
+      qf[n][i] = qok[n] ? *reinterpret_cast<const uint4*>(qp + 32 * i) : make_uint4(0, 0, 0, 0);
   }
 
   f32x4 o[NQ][NT];
@@ -272,13 +317,13 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(PrefillAttnArgs a) {
     const int buf = pair & 1;
     if (pair + 1 < n_pairs) fetch(pair + 1);
 
-    // K operand of both pages (A of S^T): key row col, permuted dims
+    // K operand of both pages (A of S^T): key row col, dims 32i + 8grp .. +7
     uint4 kf[2][KQ];
 #pragma unroll
     for (int pg = 0; pg < 2; ++pg)
 #pragma unroll
       for (int i = 0; i < KQ; ++i)
-        kf[pg][i] = *reinterpret_cast<const uint4*>(&ks[buf][pg][col * HD + grp * (HD / 4) + 8 * i]);
+        kf[pg][i] = *reinterpret_cast<const uint4*>(&ks[buf][pg][512 * i + 8 * lane]);
 
 #pragma unroll
     for (int n = 0; n < NQ; ++n) {
@@ -320,8 +365,9 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(PrefillAttnArgs a) {
       split_bf16(pv[1][2], pv[1][3], hi.w, lo.w);
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        const uint2 va = *reinterpret_cast<const uint2*>(&vs[buf][0][(16 * t + col) * kPage + 4 * grp]);
-        const uint2 vb = *reinterpret_cast<const uint2*>(&vs[buf][1][(16 * t + col) * kPage + 4 * grp]);
+        const int vo = 512 * (t >> 1) + 8 * lane + (t & 1) * 4;
+        const uint2 va = *reinterpret_cast<const uint2*>(&vs[buf][0][vo]);
+        const uint2 vb = *reinterpret_cast<const uint2*>(&vs[buf][1][vo]);
         const uint4 vf = make_uint4(va.x, va.y, vb.x, vb.y);
         o[n][t] *= corr;
         o[n][t] = mfma_k32(vf, hi, o[n][t]);
@@ -354,19 +400,26 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(PrefillAttnArgs a) {
 
 template <int HD>
 static hipError_t launch_decode_hd(const AttnArgs& a, hipStream_t s) {
-  const dim3 grid(a.rows * a.nkv), block(kDecodeWaves * 64);
+  constexpr int NW = kDecodeWaves, PD = kDecodeRing;
+  const dim3 grid(a.n_work * a.nkv), block(NW * 64);
   switch (a.nq / a.nkv) {
-    case 1: hipLaunchKernelGGL((attn_decode_kernel<HD, 1>), grid, block, 0, s, a); break;
-    case 2: hipLaunchKernelGGL((attn_decode_kernel<HD, 2>), grid, block, 0, s, a); break;
-    case 4: hipLaunchKernelGGL((attn_decode_kernel<HD, 4>), grid, block, 0, s, a); break;
-    case 8: hipLaunchKernelGGL((attn_decode_kernel<HD, 8>), grid, block, 0, s, a); break;
+    case 1: hipLaunchKernelGGL((attn_decode_kernel<HD, 1, NW, PD>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((attn_decode_kernel<HD, 2, NW, PD>), grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL((attn_decode_kernel<HD, 4, NW, PD>), grid, block, 0, s, a); break;
+    case 8: hipLaunchKernelGGL((attn_decode_kernel<HD, 8, NW, PD>), grid, block, 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s) {
+hipError_t launch_attn_combine(const AttnArgs& a, hipStream_t s) {
   if (a.rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(attn_combine_kernel, dim3(a.rows * a.nq), dim3(a.hd), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s) {
+  if (a.n_work <= 0) return hipSuccess;
   if (a.hd == 128) return launch_decode_hd<128>(a, s);
   if (a.hd == 64) return launch_decode_hd<64>(a, s);
   return hipErrorInvalidValue;

@@ -55,4 +55,20 @@ __device__ __forceinline__ size_t kv_offset(int page, int kv, int n_kv_heads, in
          static_cast<size_t>((kv * n_kv_heads + head) * kPage + slot) * head_dim + dim;
 }
 
+// Element offsets inside one (page, kv head) tile of 16 keys x hd dims, laid
+// out so that every matrix-core operand of the attention kernels is one
+// 16-byte load per lane, lane l = 16g + r reading bytes 16l .. 16l+15 of a
+// 1 KiB block (g = l/16, r = l%16):
+//   K:   block i = dims 32i .. 32i+31, element (key r, dim 32i + 8g + e) at
+//        ((i*4 + g)*16 + r)*8 + e
+//   V^T: block c = dims 32c .. 32c+31, element (dim 32c + 16u + r, key 4g + j)
+//        at ((c*4 + g)*16 + r)*8 + 4u + j: one load gives lane (r, g) the 4
+//        keys of dims 32c + r and 32c + 16 + r.
+__device__ __forceinline__ int k_tile_offset(int key, int d) {
+  return (((d >> 5) * 4 + ((d >> 3) & 3)) * 16 + key) * 8 + (d & 7);
+}
+__device__ __forceinline__ int vt_tile_offset(int d, int key) {
+  return (((d >> 5) * 4 + (key >> 2)) * 16 + (d & 15)) * 8 + ((d >> 4) & 1) * 4 + (key & 3);
+}
+
 }  // namespace metro

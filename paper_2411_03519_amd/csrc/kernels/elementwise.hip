@@ -106,7 +106,7 @@ hipError_t launch_rmsnorm(float* x, int ldx, const uint16_t* g, float eps, uint1
 
 // ---------------------------------------------------------------------------
 // RoPE on q and k (rotate-half pairs (i, i + hd/2)), bf16 rounding, and the
-// write of k and v into their page slot (K row-major, V transposed).  One
+// write of k and v into their page slot (tile layouts in common.h).  One
 // wave per (token, head) of the nq + 2 nkv heads; lane j < hd/2 takes the pair
 // (j, j + hd/2).  The qkv value is the sum of the GEMM's k slices in slice
 // order when the GEMM was split.
@@ -134,16 +134,21 @@ __global__ __launch_bounds__(64) void rope_kv_kernel(const float* __restrict__ q
   const float a = val(j), b = val(j + half);
   if (head < nq + nkv) {
     const float2 c = rope[static_cast<size_t>(pos[t]) * half + j];
-    const float ra = a * c.x - b * c.y;
-    const float rb = a * c.y + b * c.x;
-    uint16_t* dst = head < nq ? q + static_cast<size_t>(t) * nq * hd + head * hd
-                              : kv + kv_offset(page, 0, nkv, head - nq, off, hd, 0);
-    dst[j] = f32_to_bf16(ra);
-    dst[j + half] = f32_to_bf16(rb);
+    const uint16_t ra = f32_to_bf16(a * c.x - b * c.y);
+    const uint16_t rb = f32_to_bf16(a * c.y + b * c.x);
+    if (head < nq) {
+      uint16_t* dst = q + static_cast<size_t>(t) * nq * hd + head * hd;
+      dst[j] = ra;
+      dst[j + half] = rb;
+    } else {
+      uint16_t* kt = kv + kv_offset(page, 0, nkv, head - nq, 0, hd, 0);
+      kt[k_tile_offset(off, j)] = ra;
+      kt[k_tile_offset(off, j + half)] = rb;
+    }
   } else {
     uint16_t* vt = kv + kv_offset(page, 1, nkv, head - nq - nkv, 0, hd, 0);
-    vt[j * kPage + off] = f32_to_bf16(a);
-    vt[(j + half) * kPage + off] = f32_to_bf16(b);
+    vt[vt_tile_offset(j, off)] = f32_to_bf16(a);
+    vt[vt_tile_offset(j + half, off)] = f32_to_bf16(b);
   }
 }
 

@@ -61,12 +61,11 @@ __device__ __forceinline__ void store_swiglu(f32x4 gt, f32x4 up, int m, int j, u
 // KS > 1 the slice sums go to part[slice][m][n] and the consumer kernel adds
 // the slices (in slice order) where it reads the result.
 // ---------------------------------------------------------------------------
-template <int MT, int NT, int EPI, int PF>
-__global__ __launch_bounds__(512) void gemm_skinny_kernel(const uint16_t* __restrict__ X, int ldx,
-                                                          const uint16_t* __restrict__ W, int Kp, int M, int N,
-                                                          float* __restrict__ outf, uint16_t* __restrict__ outb,
-                                                          int ldo, float* __restrict__ part) {
-  constexpr int NW = 8;
+template <int MT, int NT, int EPI, int PF, int NW>
+__global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const uint16_t* __restrict__ X, int ldx,
+                                                              const uint16_t* __restrict__ W, int Kp, int M, int N,
+                                                              float* __restrict__ outf, uint16_t* __restrict__ outb,
+                                                              int ldo, float* __restrict__ part) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r = lane & 15, g = lane >> 4;
   const int n0 = blockIdx.x * 16 * NT;
@@ -295,6 +294,7 @@ __global__ __launch_bounds__(256) void gemm_tiled_kernel(const uint16_t* __restr
 #define METRO_SKINNY_PF 1
 #endif
 constexpr int kSkinnyPF = METRO_SKINNY_PF;  // k blocks in flight per wave
+constexpr int kSkinnyWaves = 8;             // waves per workgroup (k split inside it)
 
 int gemm_splits(int M, int N, int Kp, int epilogue) {
   if (M > 64 || epilogue == kEpiSwiGLU) return 1;
@@ -309,8 +309,8 @@ int gemm_splits(int M, int N, int Kp, int epilogue) {
 template <int MT, int NT, int EPI>
 static void launch_skinny(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, float* outf,
                           uint16_t* outb, int ldo, float* part, int ks, hipStream_t s) {
-  hipLaunchKernelGGL((gemm_skinny_kernel<MT, NT, EPI, kSkinnyPF>), dim3(N / (16 * NT), ks), dim3(512), 0, s, X, ldx,
-                     W, Kp, M, N, outf, outb, ldo, part);
+  hipLaunchKernelGGL((gemm_skinny_kernel<MT, NT, EPI, kSkinnyPF, kSkinnyWaves>), dim3(N / (16 * NT), ks),
+                     dim3(kSkinnyWaves * 64), 0, s, X, ldx, W, Kp, M, N, outf, outb, ldo, part);
 }
 
 template <int NT, int EPI>

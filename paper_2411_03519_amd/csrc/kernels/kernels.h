@@ -72,21 +72,30 @@ hipError_t launch_reduce_parts(const float* part, int KS, int M, int N, int epil
 
 // --- attention (attention.hip) ---------------------------------------------
 
-// KV page layout per (layer, page, kv head): K [16][hd] then V^T [hd][16].
+// KV page layout per (layer, page, kv head): a K tile then a V^T tile of 16
+// keys x hd (layouts in common.h).
 struct AttnArgs {
   const uint16_t* q;        // [rows_total, nq, hd] bf16 (row = query token)
   const uint16_t* kv;       // this layer's slab of the KV pool
+  const int32_t* work;      // [n_work][2]: (row, split)
   const int32_t* row_ctx;   // [rows]: keys visible to the row (0 .. ctx-1)
   const int32_t* row_qrow;  // [rows]: row of q / out for this row
   const int32_t* row_bt;    // [rows]: offset of the row's block table in bt
+  const int32_t* row_work;  // [rows]: first work item of the row
+  const int32_t* row_nsplit;// [rows]: work items of the row
   const int32_t* bt;        // block tables
+  float* part;              // [n_work][nkv][group][hd + 2] fp32 split states
   uint16_t* out;            // [rows_total, nq*hd] bf16
-  int rows, nq, nkv, hd;
+  int n_work, rows, nq, nkv, hd;
   float scale;              // 1/sqrt(hd)
 };
 
-// Decode attention: one workgroup per (row, kv head).
+// Decode attention: one workgroup per (work item, kv head), a work item being
+// up to kDecodePagesPerSplit pages of one row.  Rows of one split are final;
+// the others leave (max, sum, output) states for launch_attn_combine.
+constexpr int kDecodePagesPerSplit = 32;
 hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s);
+hipError_t launch_attn_combine(const AttnArgs& a, hipStream_t s);
 
 struct PrefillAttnArgs {
   const uint16_t* q;        // [T, nq, hd] bf16

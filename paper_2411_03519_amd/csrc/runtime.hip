@@ -83,6 +83,7 @@ struct metro_model {
   float* logits_ws = nullptr;
   int32_t* next_ws = nullptr;
   float* parts = nullptr;    // k-slice sums of decode GEMMs, [8][64][max(qkv_n, d)]
+  float* attn_part = nullptr;  // decode attention split states
   int32_t* desc_dev = nullptr;
   int64_t desc_cap = 0;  // int32 elements
   // host
@@ -188,13 +189,18 @@ struct Carve {
   }
 };
 
+int64_t decode_work_capacity(const metro_config& c) {
+  const int64_t P = (c.max_context + 15) / 16;
+  return int64_t(c.max_batch) * ((P + metro::kDecodePagesPerSplit - 1) / metro::kDecodePagesPerSplit);
+}
+
 int64_t desc_capacity(const metro_config& c) {
   const int64_t T = c.max_tokens, B = c.max_batch;
   const int64_t P = (c.max_context + 15) / 16;
   // tokens, positions, slots, last rows, item block tables, query blocks, block tables
   const int64_t prefill = 3 * T + 2 * B + 3 * (T + B) + B * P;
-  // positions, slots, 3 per-row arrays, block tables
-  const int64_t decode = 5 * B + B * P;
+  // positions, slots, 5 per-row arrays, work items, block tables
+  const int64_t decode = 7 * B + 2 * decode_work_capacity(c) + B * P;
   // + per-array rounding to 16 elements (at most 16 arrays per call)
   return std::max(prefill, decode) + 16 * 16 + 64;
 }
@@ -257,6 +263,7 @@ metro_status launch_layers(metro_model* m, int T, const int32_t* tok_dev, const 
       metro::AttnArgs a = *dec;
       a.kv = kv_l;
       LAUNCH(m, METRO_K_ATTENTION, s, metro::launch_attn_decode(a, s));
+      if (a.n_work > a.rows) LAUNCH(m, METRO_K_ATTENTION, s, metro::launch_attn_combine(a, s));
     } else {
       metro::PrefillAttnArgs a = *pre;
       a.kv = kv_l;
@@ -401,7 +408,8 @@ metro_status metro_create_model(const metro_config* cfg, uint64_t init_seed, met
   {
     const size_t bytes = Tm * d * 4 + Tm * d * 2 + Tm * m->qkv_n * 4 + 2 * Tm * m->q_dim * 2 + Tm * m->Fp * 2 +
                          int64_t(c.max_batch) * d * 4 + int64_t(c.max_batch) * V * 4 + int64_t(c.max_batch) * 4 +
-                         8LL * 64 * std::max(m->qkv_n, d) * 4 + m->desc_cap * 4 + 256 * 16;
+                         8LL * 64 * std::max(m->qkv_n, d) * 4 +
+                         decode_work_capacity(c) * nkv * m->group * (hd + 2) * 4 + m->desc_cap * 4 + 256 * 16;
     m->scratch_bytes = bytes;
     e = hipMalloc(&m->sbase, bytes);
     if (e != hipSuccess) return bail(fail(METRO_E_NOMEM, "hipMalloc of %zu scratch bytes failed", bytes));
@@ -416,6 +424,7 @@ metro_status metro_create_model(const metro_config* cfg, uint64_t init_seed, met
     m->logits_ws = cv.take<float>(int64_t(c.max_batch) * V);
     m->next_ws = cv.take<int32_t>(c.max_batch);
     m->parts = cv.take<float>(8LL * 64 * std::max(m->qkv_n, d));
+    m->attn_part = cv.take<float>(decode_work_capacity(c) * nkv * m->group * (hd + 2));
     m->desc_dev = cv.take<int32_t>(m->desc_cap);
     // the SwiGLU output's padding columns must read as zero
     e = hipMemset(m->a, 0, Tm * m->Fp * 2);
@@ -738,7 +747,10 @@ metro_status metro_decode_step(metro_model* m, int32_t B, const int64_t* seqs, c
   int32_t* row_ctx = d.put(B);
   int32_t* row_q = d.put(B);
   int32_t* row_bt = d.put(B);
+  int32_t* row_work = d.put(B);
+  int32_t* row_nsplit = d.put(B);
   int64_t bo = 0;
+  int32_t n_work = 0;
   for (int i = 0; i < B; ++i) {
     const metro::Sequence* s = m->seqs->find(seqs[i]);
     const int p = s->length;
@@ -748,8 +760,17 @@ metro_status metro_decode_step(metro_model* m, int32_t B, const int64_t* seqs, c
     row_ctx[i] = p + 1;
     row_q[i] = i;
     row_bt[i] = static_cast<int32_t>(bo);
+    row_work[i] = n_work;
+    row_nsplit[i] = ((p + 1 + 15) / 16 + metro::kDecodePagesPerSplit - 1) / metro::kDecodePagesPerSplit;
+    n_work += row_nsplit[i];
     bo += s->pages.size();
   }
+  int32_t* work = d.put(2 * static_cast<int64_t>(n_work));
+  for (int i = 0, w = 0; i < B; ++i)
+    for (int sp = 0; sp < row_nsplit[i]; ++sp, ++w) {
+      work[2 * w] = i;
+      work[2 * w + 1] = sp;
+    }
   m->cur_phase = 2;
   hipStream_t s = static_cast<hipStream_t>(stream);
   st = upload_ring(m, d, s);
@@ -757,11 +778,16 @@ metro_status metro_decode_step(metro_model* m, int32_t B, const int64_t* seqs, c
   auto dev = [&](const int32_t* hp) { return m->desc_dev + (hp - d.host); };
   metro::AttnArgs a{};
   a.q = m->q;
+  a.work = dev(work);
   a.row_ctx = dev(row_ctx);
   a.row_qrow = dev(row_q);
   a.row_bt = dev(row_bt);
+  a.row_work = dev(row_work);
+  a.row_nsplit = dev(row_nsplit);
   a.bt = dev(bt);
+  a.part = m->attn_part;
   a.out = m->o;
+  a.n_work = n_work;
   a.rows = B;
   a.nq = c.n_heads;
   a.nkv = c.n_kv_heads;
