@@ -195,53 +195,82 @@ __global__ __launch_bounds__(256) void reduce_parts_kernel(const float* __restri
 }
 
 // ---------------------------------------------------------------------------
-// Tiled GEMM (M > 64: prefill chunks, large decode batches).  Block tile
-// 128 (m) x 128 (n) x 64 (k), 4 waves in 2x2, each wave 64x64 = 4x4 MFMA
-// tiles.  Tiles are staged through LDS (double buffered, rows padded by 16 B);
-// the next k tile is fetched into registers while the current one is used.
+// Tiled GEMM (M > 64: prefill chunks, large decode batches), bound by the
+// matrix cores.  Block tile 256 (n, rows of W) x 256 (m, activation rows) x 64
+// (k); 4 waves in 2x2, each 128x128 = 4x4 tiles of v_mfma_f32_32x32x16_bf16
+// (A = W rows, B = activation rows).  Lane l supplies A[l%32][8(l/32) .. +7]
+// and B[8(l/32) .. +7][l%32] and receives D rows 8q + 4(l/32) + i (q = 0..3,
+// i = 0..3) of column l%32: four consecutive output features of one
+// activation row per q.  Operand tiles are staged through LDS, double
+// buffered, with the 16-byte chunk index of each 128-byte row XOR-ed with the
+// row (mod 8) so the 32 rows one MFMA operand read touches fall in distinct
+// banks; the next k tile is fetched into registers while the current one is
+// consumed.
 // ---------------------------------------------------------------------------
-constexpr int TBM = 128, TBN = 128, TBK = 64, TPAD = 8;
+constexpr int TBM = 256, TBN = 256, TBK = 64;
 
-template <int EPI>
-__global__ __launch_bounds__(256) void gemm_tiled_kernel(const uint16_t* __restrict__ X, int ldx,
-                                                         const uint16_t* __restrict__ W, int Kp, int M, int N,
-                                                         float* __restrict__ outf, uint16_t* __restrict__ outb,
-                                                         int ldo) {
-  __shared__ uint16_t xs[2][TBM][TBK + TPAD];
-  __shared__ uint16_t ws[2][TBN][TBK + TPAD];
+__device__ __forceinline__ f32x16 mfma32(uint4 a, uint4 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
+}
+
+template <int EPI, int WN, int WM>
+__global__ __launch_bounds__(WN * WM * 64) void gemm_tiled_kernel(const uint16_t* __restrict__ X, int ldx,
+                                                                  const uint16_t* __restrict__ W, int Kp, int M, int N,
+                                                                  float* __restrict__ outf,
+                                                                  uint16_t* __restrict__ outb, int ldo) {
+  constexpr int NTH = WN * WM * 64;
+  constexpr int TN = TBN / WN / 32, TM = TBM / WM / 32;  // 32x32 tiles per wave
+  constexpr int CPT = TBN * 8 / NTH;                     // 16-byte chunks per thread per operand
+  __shared__ uint4 ws[2][TBN * 8];  // [row][8 chunks of 16 B], chunk swizzled
+  __shared__ uint4 xs[2][TBM * 8];
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
-  const int r = lane & 15, g = lane >> 4;
-  const int wm = wave >> 1, wn = wave & 1;  // wave's 64x64 quadrant
-  const int m0 = blockIdx.y * TBM, n0 = blockIdx.x * TBN;
+  const int wn = wave / WM, wm = wave % WM;  // the wave's (TN*32) x (TM*32) tile
+  const int lr = lane & 31, lh = lane >> 5;
 
-  // global -> register staging: 1024 16-byte chunks per operand tile, 4 per thread
-  const int lrow = tid >> 3, lcol = (tid & 7) * 8;
-  uint4 xr[4], wr[4];
+  // Grouped tile order: blocks in launch order sweep groups of kGroupM m-tiles,
+  // m fastest within a group, so the ~256 blocks in flight cover a compact
+  // 16 x 16 patch of tiles and share their W and X tiles through the caches.
+  constexpr int kGroupM = 16;
+  const int mt = (M + TBM - 1) / TBM, nt = (N + TBN - 1) / TBN;
+  const int b = blockIdx.x;
+  const int group = b / (kGroupM * nt);
+  const int first_m = group * kGroupM;
+  const int gm = min(mt - first_m, kGroupM);
+  const int in = b % (kGroupM * nt);
+  const int n0 = (in / gm) * TBN, m0 = (first_m + in % gm) * TBM;
+
+  // global -> registers -> LDS
+  uint4 wr[CPT], xr[CPT];
   auto fetch = [&](int k) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int m = m0 + lrow + 32 * i;
-      xr[i] = m < M ? *reinterpret_cast<const uint4*>(X + static_cast<size_t>(m) * ldx + k + lcol)
+    for (int j = 0; j < CPT; ++j) {
+      const int c = tid + NTH * j;
+      const int row = c >> 3, ch = c & 7;
+      const int n = n0 + row, m = m0 + row;
+      wr[j] = n < N ? *reinterpret_cast<const uint4*>(W + static_cast<size_t>(n) * Kp + k + 8 * ch)
                     : make_uint4(0, 0, 0, 0);
-      const int n = n0 + lrow + 32 * i;
-      wr[i] = n < N ? *reinterpret_cast<const uint4*>(W + static_cast<size_t>(n) * Kp + k + lcol)
+      xr[j] = m < M ? *reinterpret_cast<const uint4*>(X + static_cast<size_t>(m) * ldx + k + 8 * ch)
                     : make_uint4(0, 0, 0, 0);
     }
   };
   auto stash = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      *reinterpret_cast<uint4*>(&xs[buf][lrow + 32 * i][lcol]) = xr[i];
-      *reinterpret_cast<uint4*>(&ws[buf][lrow + 32 * i][lcol]) = wr[i];
+    for (int j = 0; j < CPT; ++j) {
+      const int c = tid + NTH * j;
+      const int row = c >> 3, ch = c & 7;
+      ws[buf][row * 8 + (ch ^ (row & 7))] = wr[j];
+      xs[buf][row * 8 + (ch ^ (row & 7))] = xr[j];
     }
   };
 
-  f32x4 acc[4][4];
+  f32x16 acc[TN][TM];
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int i = 0; i < TN; ++i)
 #pragma unroll
-    for (int b = 0; b < 4; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < TM; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int nk = Kp / TBK;
   fetch(0);
@@ -251,38 +280,54 @@ __global__ __launch_bounds__(256) void gemm_tiled_kernel(const uint16_t* __restr
     const int buf = kt & 1;
     if (kt + 1 < nk) fetch((kt + 1) * TBK);
 #pragma unroll
-    for (int kc = 0; kc < TBK / 32; ++kc) {
-      uint4 af[4], bf[4];
+    for (int ks = 0; ks < TBK / 16; ++ks) {
+      const int ch = 2 * ks + lh;
+      uint4 af[TN], bf[TM];
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt)
-        af[nt] = *reinterpret_cast<const uint4*>(&ws[buf][wn * 64 + nt * 16 + r][kc * 32 + g * 8]);
+      for (int i = 0; i < TN; ++i) {
+        const int row = wn * TN * 32 + i * 32 + lr;
+        af[i] = ws[buf][row * 8 + (ch ^ (row & 7))];
+      }
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
-        bf[mt] = *reinterpret_cast<const uint4*>(&xs[buf][wm * 64 + mt * 16 + r][kc * 32 + g * 8]);
+      for (int j = 0; j < TM; ++j) {
+        const int row = wm * TM * 32 + j * 32 + lr;
+        bf[j] = xs[buf][row * 8 + (ch ^ (row & 7))];
+      }
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt)
+      for (int i = 0; i < TN; ++i)
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt) acc[nt][mt] = mfma16(af[nt], bf[mt], acc[nt][mt]);
+        for (int j = 0; j < TM; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
     }
     if (kt + 1 < nk) stash(buf ^ 1);
     __syncthreads();
   }
 
+  // fully unrolled (acc must stay in registers); the scheduling barriers keep
+  // the read-modify-write epilogue from hoisting all of its loads at once
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt) {
-    const int m = m0 + wm * 64 + mt * 16 + r;
+  for (int j = 0; j < TM; ++j) {
+    const int m = m0 + wm * TM * 32 + j * 32 + lr;
     if (m >= M) continue;
-    if (EPI == kEpiSwiGLU) {
 #pragma unroll
-      for (int p = 0; p < 2; ++p) {
-        const int nb = n0 + wn * 64 + p * 32;  // 32-row (gate, up) block
-        if (nb < N) store_swiglu(acc[2 * p][mt], acc[2 * p + 1][mt], m, (nb / 32) * 16 + 4 * g, outb, ldo);
-      }
-    } else {
+    for (int i = 0; i < TN; ++i) {
+      const int nb = n0 + wn * TN * 32 + i * 32;  // 32-row tile of W
+      if (nb >= N) continue;
+      if (EPI == kEpiSwiGLU) {
+        // rows 0..15 of the tile are gate features, rows 16..31 the matching up features
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        const int n = n0 + wn * 64 + nt * 16;
-        if (n < N) store_tile<EPI>(acc[nt][mt], m, n + 4 * g, outf, ldo);
+        for (int q = 0; q < 2; ++q) {
+          const f32x4 gt{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+          const f32x4 up{acc[i][j][4 * q + 8], acc[i][j][4 * q + 9], acc[i][j][4 * q + 10], acc[i][j][4 * q + 11]};
+          store_swiglu(gt, up, m, (nb / 32) * 16 + 8 * q + 4 * lh, outb, ldo);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const f32x4 v{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+          store_tile<EPI>(v, m, nb + 8 * q + 4 * lh, outf, ldo);
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
     }
   }
@@ -295,6 +340,7 @@ __global__ __launch_bounds__(256) void gemm_tiled_kernel(const uint16_t* __restr
 #endif
 constexpr int kSkinnyPF = METRO_SKINNY_PF;  // k blocks in flight per wave
 constexpr int kSkinnyWaves = 8;             // waves per workgroup (k split inside it)
+constexpr int kTiledWN = 4, kTiledWM = 2;   // wave grid of the tiled GEMM (8 waves, 2 per SIMD)
 
 int gemm_splits(int M, int N, int Kp, int epilogue) {
   if (M > 64 || epilogue == kEpiSwiGLU) return 1;
@@ -333,8 +379,9 @@ static hipError_t launch_epi(const uint16_t* X, int ldx, const uint16_t* W, int 
     else
       launch_skinny_m<2, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, ks, s);
   } else {
-    const dim3 grid((N + TBN - 1) / TBN, (M + TBM - 1) / TBM);
-    hipLaunchKernelGGL((gemm_tiled_kernel<EPI>), grid, dim3(256), 0, s, X, ldx, W, Kp, M, N, outf, outb, ldo);
+    const int tiles = ((N + TBN - 1) / TBN) * ((M + TBM - 1) / TBM);
+    hipLaunchKernelGGL((gemm_tiled_kernel<EPI, kTiledWN, kTiledWM>), dim3(tiles), dim3(kTiledWN * kTiledWM * 64), 0, s,
+                       X, ldx, W, Kp, M, N, outf, outb, ldo);
   }
   return hipGetLastError();
 }
