@@ -19,14 +19,29 @@
 extern "C" {
 #endif
 
+/* Weight layout of the projection GEMMs.  W_packed receives the bf16 matrix
+ * W [N, Kp] (W[n, k] = W_rowmajor[n * ld + k] for k < K, 0 for K <= k < Kp) in
+ * matrix-core operand order: 16 x 32 tiles (16 rows, 32 columns), tiles
+ * row-major over (n / 16, k / 32), tile (tn, tk) stored as 64 chunks of 8
+ * elements in the order c = r + 16 g, chunk c = W[16 tn + r][32 tk + 8 g ..
+ * 8 g + 7]; i.e. W[n, k] sits at element
+ *   ((n/16 * Kp/32 + k/32) * 64 + n%16 + 16 * ((k/8)%4)) * 8 + k%8.
+ * W_rowmajor: device bf16 [N, ld], ld >= K; W_packed: device bf16, N * Kp
+ * elements, not overlapping W_rowmajor.  N % 16 == 0, Kp % 128 == 0,
+ * 0 < K <= Kp.  Errors: E_INVAL for shapes outside these rules or NULL. */
+metro_status metro_op_pack_weight(const uint16_t* W_rowmajor, int32_t ld, int32_t N, int32_t K, int32_t Kp,
+                                  uint16_t* W_packed, void* stream);
+
 /* Projection GEMM of the Llama block (QKV, O, gate/up, down, LM head):
  *   acc[m, n] = sum_k X[m, k] * W[n, k]   (bf16 operands, fp32 accumulation)
- * X: bf16 [M, ldx] row-major, the first Kp columns used; W: bf16 [N, Kp];
- * Kp % 128 == 0, N % 32 == 0.  epilogue:
+ * X: bf16 [M, ldx] row-major, the first Kp columns used; W: bf16 [N, Kp] in
+ * the layout metro_op_pack_weight writes; Kp % 128 == 0, N % 32 == 0.
+ * epilogue:
  *   0  out_f32[m*ldo + n]  = acc[m, n]
  *   1  out_f32[m*ldo + n] += acc[m, n]                       (residual add)
  *   2  W rows come in blocks of 32 = 16 gate rows then 16 up rows of the same
- *      features; out_bf16[m*ldo + j] = bf16(silu(gate_j) * up_j), j < N/2
+ *      features (16-row tiles alternate gate, up); out_bf16[m*ldo + j] =
+ *      bf16(silu(gate_j) * up_j), j < N/2
  *      (SwiGLU, Shazeer 2020).
  * workspace: NULL, or device fp32 [8][M][N]; when given, a decode-sized GEMM
  * (M <= 64, epilogue 0 or 1) runs the k-split form the model uses (slices in

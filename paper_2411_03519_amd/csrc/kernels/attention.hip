@@ -403,10 +403,10 @@ static hipError_t launch_decode_hd(const AttnArgs& a, hipStream_t s) {
   constexpr int NW = kDecodeWaves, PD = kDecodeRing;
   const dim3 grid(a.n_work * a.nkv), block(NW * 64);
   switch (a.nq / a.nkv) {
-    case 1: hipLaunchKernelGGL((attn_decode_kernel<HD, 1, NW, PD>), grid, block, 0, s, a); break;
-    case 2: hipLaunchKernelGGL((attn_decode_kernel<HD, 2, NW, PD>), grid, block, 0, s, a); break;
-    case 4: hipLaunchKernelGGL((attn_decode_kernel<HD, 4, NW, PD>), grid, block, 0, s, a); break;
-    case 8: hipLaunchKernelGGL((attn_decode_kernel<HD, 8, NW, PD>), grid, block, 0, s, a); break;
+    case 1: launch_kernel((attn_decode_kernel<HD, 1, NW, PD>), grid, block, 0, s, a); break;
+    case 2: launch_kernel((attn_decode_kernel<HD, 2, NW, PD>), grid, block, 0, s, a); break;
+    case 4: launch_kernel((attn_decode_kernel<HD, 4, NW, PD>), grid, block, 0, s, a); break;
+    case 8: launch_kernel((attn_decode_kernel<HD, 8, NW, PD>), grid, block, 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -414,7 +414,7 @@ static hipError_t launch_decode_hd(const AttnArgs& a, hipStream_t s) {
 
 hipError_t launch_attn_combine(const AttnArgs& a, hipStream_t s) {
   if (a.rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(attn_combine_kernel, dim3(a.rows * a.nq), dim3(a.hd), 0, s, a);
+  launch_kernel(attn_combine_kernel, dim3(a.rows * a.nq), dim3(a.hd), 0, s, a);
   return hipGetLastError();
 }
 
@@ -429,10 +429,10 @@ template <int HD>
 static hipError_t launch_prefill_hd(const PrefillAttnArgs& a, hipStream_t s) {
   const dim3 grid(a.n_blocks * a.nkv);
   switch (a.nq / a.nkv) {
-    case 1: hipLaunchKernelGGL((attn_prefill_kernel<HD, 1>), grid, dim3(256), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((attn_prefill_kernel<HD, 2>), grid, dim3(256), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((attn_prefill_kernel<HD, 4>), grid, dim3(256), 0, s, a); break;
-    case 8: hipLaunchKernelGGL((attn_prefill_kernel<HD, 8>), grid, dim3(256), 0, s, a); break;
+    case 1: launch_kernel((attn_prefill_kernel<HD, 1>), grid, dim3(256), 0, s, a); break;
+    case 2: launch_kernel((attn_prefill_kernel<HD, 2>), grid, dim3(256), 0, s, a); break;
+    case 4: launch_kernel((attn_prefill_kernel<HD, 4>), grid, dim3(256), 0, s, a); break;
+    case 8: launch_kernel((attn_prefill_kernel<HD, 8>), grid, dim3(256), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

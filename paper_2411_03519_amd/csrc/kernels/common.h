@@ -71,4 +71,15 @@ __device__ __forceinline__ int vt_tile_offset(int d, int key) {
   return (((d >> 5) * 4 + (key >> 2)) * 16 + (d & 15)) * 8 + ((d >> 4) & 1) * 4 + (key & 3);
 }
 
+// Projection weights W [N][Kp] (bf16, Kp % 128 == 0, N % 16 == 0) are stored in
+// the operand order of v_mfma_f32_16x16x32_bf16: W is cut into 16 x 32 tiles
+// (16 rows n, 32 reduction indices k), tiles row-major over (n/16, k/32), and
+// tile (tn, tk) is 64 chunks of 16 bytes in lane order, the chunk of lane
+// l = 16g + r holding W[16tn + r][32tk + 8g .. 8g + 7].  One wave reading one
+// tile (lane l the bytes 16l .. 16l+15) is a single contiguous 1 KiB request,
+// and a row tile's successive k tiles are contiguous.
+__host__ __device__ __forceinline__ int64_t packed_offset(int64_t n, int64_t k, int64_t Kp) {
+  return ((((n >> 4) * (Kp >> 5) + (k >> 5)) * 64 + (n & 15) + 16 * ((k >> 3) & 3)) << 3) + (k & 7);
+}
+
 }  // namespace metro

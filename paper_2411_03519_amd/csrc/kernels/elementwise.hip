@@ -6,6 +6,8 @@
 
 namespace metro {
 
+thread_local LaunchEvents launch_events;
+
 // ---------------------------------------------------------------------------
 // Embedding gather: x[t, :] = fp32(E[tok[t], :]).  One block per token.
 // ---------------------------------------------------------------------------
@@ -32,7 +34,7 @@ __global__ __launch_bounds__(256) void embed_kernel(const int32_t* __restrict__ 
 hipError_t launch_embed(const int32_t* tok, const uint16_t* embed, int vocab, int d, float* x, int T,
                         hipStream_t s) {
   if (T <= 0) return hipSuccess;
-  hipLaunchKernelGGL(embed_kernel, dim3(T), dim3(256), 0, s, tok, embed, vocab, d, x);
+  launch_kernel(embed_kernel, dim3(T), dim3(256), 0, s, tok, embed, vocab, d, x);
   return hipGetLastError();
 }
 
@@ -96,10 +98,10 @@ hipError_t launch_rmsnorm(float* x, int ldx, const uint16_t* g, float eps, uint1
   if (rows <= 0) return hipSuccess;
   // one float4 per thread where the row allows
   if (d >= 4096)
-    hipLaunchKernelGGL(rmsnorm_kernel<1024>, dim3(rows), dim3(1024), 0, s, x, ldx, g, eps, h, ldh, d, parts, n_parts,
+    launch_kernel(rmsnorm_kernel<1024>, dim3(rows), dim3(1024), 0, s, x, ldx, g, eps, h, ldh, d, parts, n_parts,
                        rows);
   else
-    hipLaunchKernelGGL(rmsnorm_kernel<256>, dim3(rows), dim3(256), 0, s, x, ldx, g, eps, h, ldh, d, parts, n_parts,
+    launch_kernel(rmsnorm_kernel<256>, dim3(rows), dim3(256), 0, s, x, ldx, g, eps, h, ldh, d, parts, n_parts,
                        rows);
   return hipGetLastError();
 }
@@ -156,7 +158,7 @@ hipError_t launch_rope_kv(const float* qkv, int n_parts, int T, int nq, int nkv,
                           const int32_t* slot, const float2* rope, uint16_t* q, uint16_t* kv_layer,
                           hipStream_t s) {
   if (T <= 0) return hipSuccess;
-  hipLaunchKernelGGL(rope_kv_kernel, dim3(T * (nq + 2 * nkv)), dim3(64), 0, s, qkv, n_parts, T, nq, nkv, hd, pos,
+  launch_kernel(rope_kv_kernel, dim3(T * (nq + 2 * nkv)), dim3(64), 0, s, qkv, n_parts, T, nq, nkv, hd, pos,
                      slot, rope, q, kv_layer);
   return hipGetLastError();
 }
@@ -174,7 +176,7 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const float* __restric
 
 hipError_t launch_gather_rows(const float* x, int d, const int32_t* rows, int n, float* out, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(gather_rows_kernel, dim3(n), dim3(256), 0, s, x, d, rows, out);
+  launch_kernel(gather_rows_kernel, dim3(n), dim3(256), 0, s, x, d, rows, out);
   return hipGetLastError();
 }
 
@@ -228,7 +230,7 @@ __global__ __launch_bounds__(1024) void argmax_kernel(const float* __restrict__ 
 
 hipError_t launch_argmax(const float* logits, int vocab, int rows, int32_t* out, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(argmax_kernel, dim3(rows), dim3(1024), 0, s, logits, vocab, out);
+  launch_kernel(argmax_kernel, dim3(rows), dim3(1024), 0, s, logits, vocab, out);
   return hipGetLastError();
 }
 
@@ -244,7 +246,8 @@ __device__ __forceinline__ uint64_t splitmix64(uint64_t z) {
 }
 
 __global__ __launch_bounds__(256) void init_normal_kernel(uint16_t* __restrict__ dst, int64_t ld, int rows,
-                                                          int cols, int row_block, int row_shift, uint64_t key) {
+                                                          int cols, int row_block, int row_shift, uint64_t key,
+                                                          bool packed) {
   const int64_t n = static_cast<int64_t>(rows) * cols;
   for (int64_t e = blockIdx.x * 256ll + threadIdx.x; e < n; e += static_cast<int64_t>(gridDim.x) * 256) {
     const int r = static_cast<int>(e / cols), c = static_cast<int>(e % cols);
@@ -253,17 +256,52 @@ __global__ __launch_bounds__(256) void init_normal_kernel(uint16_t* __restrict__
     const float u2 = static_cast<float>((h >> 16) & 0xffffffull) * (1.0f / 16777216.0f);  // [0, 1)
     const float z = sqrtf(-2.0f * logf(u1)) * cosf(6.283185307179586f * u2);
     const int64_t pr = static_cast<int64_t>(r / 16) * row_block + row_shift + (r % 16);
-    dst[pr * ld + c] = f32_to_bf16(0.02f * z);
+    dst[packed ? packed_offset(pr, c, ld) : pr * ld + c] = f32_to_bf16(0.02f * z);
   }
 }
 
 hipError_t launch_init_normal(uint16_t* dst, int64_t ld, int rows, int cols, int row_block, int row_shift,
-                              uint64_t key, hipStream_t s) {
+                              uint64_t key, bool packed, hipStream_t s) {
   const int64_t n = static_cast<int64_t>(rows) * cols;
   const int64_t blocks = (n + 255) / 256;
   const int grid = static_cast<int>(blocks < 65536 ? blocks : 65536);
-  hipLaunchKernelGGL(init_normal_kernel, dim3(grid), dim3(256), 0, s, dst, ld, rows, cols, row_block, row_shift,
-                     key);
+  launch_kernel(init_normal_kernel, dim3(grid), dim3(256), 0, s, dst, ld, rows, cols, row_block, row_shift, key,
+                packed);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Row-major bf16 weight -> MFMA operand order (packed_offset): one thread per
+// 8-element chunk (row r, k .. k+7) of the destination's Kp columns, logical
+// row r going to row (r/16)*row_block + row_shift + r%16; k >= cols is zero.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void pack_weight_kernel(const uint16_t* __restrict__ src, int64_t ld_src,
+                                                          int rows, int cols, uint16_t* __restrict__ dst, int Kp,
+                                                          int row_block, int row_shift) {
+  const int kc = Kp / 8;
+  const int64_t n = static_cast<int64_t>(rows) * kc;
+  for (int64_t e = blockIdx.x * 256ll + threadIdx.x; e < n; e += static_cast<int64_t>(gridDim.x) * 256) {
+    const int r = static_cast<int>(e / kc), k = static_cast<int>(e % kc) * 8;
+    uint16_t v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = k + j < cols ? src[r * ld_src + k + j] : 0;
+    const int64_t pr = static_cast<int64_t>(r / 16) * row_block + row_shift + (r % 16);
+    uint4 o;
+    o.x = v[0] | (static_cast<uint32_t>(v[1]) << 16);
+    o.y = v[2] | (static_cast<uint32_t>(v[3]) << 16);
+    o.z = v[4] | (static_cast<uint32_t>(v[5]) << 16);
+    o.w = v[6] | (static_cast<uint32_t>(v[7]) << 16);
+    *reinterpret_cast<uint4*>(dst + packed_offset(pr, k, Kp)) = o;
+  }
+}
+
+hipError_t launch_pack_weight(const uint16_t* src, int64_t ld_src, int rows, int cols, uint16_t* dst, int Kp,
+                              int row_block, int row_shift, hipStream_t s) {
+  const int64_t n = static_cast<int64_t>(rows) * (Kp / 8);
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = (n + 255) / 256;
+  launch_kernel(pack_weight_kernel, dim3(static_cast<int>(blocks < 65536 ? blocks : 65536)), dim3(256), 0, s, src,
+                ld_src, rows, cols, dst, Kp, row_block, row_shift);
   return hipGetLastError();
 }
 
@@ -274,7 +312,7 @@ __global__ __launch_bounds__(256) void fill_bf16_kernel(uint16_t* __restrict__ d
 hipError_t launch_fill_bf16(uint16_t* dst, int64_t n, uint16_t value, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   const int64_t blocks = (n + 255) / 256;
-  hipLaunchKernelGGL(fill_bf16_kernel, dim3(static_cast<int>(blocks < 65536 ? blocks : 65536)), dim3(256), 0, s,
+  launch_kernel(fill_bf16_kernel, dim3(static_cast<int>(blocks < 65536 ? blocks : 65536)), dim3(256), 0, s,
                      dst, n, value);
   return hipGetLastError();
 }
@@ -292,7 +330,7 @@ __global__ __launch_bounds__(256) void page_copy_kernel(uint16_t* __restrict__ p
 
 hipError_t launch_page_copy(uint16_t* pool, int64_t layer_stride, int64_t page_elems, int layers, int src,
                             int dst, hipStream_t s) {
-  hipLaunchKernelGGL(page_copy_kernel, dim3(layers), dim3(256), 0, s, pool, layer_stride, page_elems, src, dst);
+  launch_kernel(page_copy_kernel, dim3(layers), dim3(256), 0, s, pool, layer_stride, page_elems, src, dst);
   return hipGetLastError();
 }
 

@@ -8,9 +8,9 @@
 // one activation row, so every epilogue store is a contiguous 16-byte (fp32)
 // or 8-byte (bf16) vector.
 //
-// Any fixed permutation of the reduction index is allowed as long as A and B
-// use the same one; the skinny kernel uses this to let each lane read 64
-// contiguous bytes of a W row per 128-wide k block.
+// W is stored in exactly that A-operand order (packed_offset in common.h): a
+// 16 x 32 tile of W is 1 KiB, lane l's 16 bytes at offset 16l, so a wave
+// loading an A operand from HBM issues one contiguous 1 KiB read.
 #include <algorithm>
 
 #include "common.h"
@@ -52,11 +52,11 @@ __device__ __forceinline__ void store_swiglu(f32x4 gt, f32x4 up, int m, int j, u
 // ---------------------------------------------------------------------------
 // Skinny GEMM (M <= 16*MT, decode batches).  Streaming W from HBM is the cost,
 // and every W row tile needs the activation rows of its k range, so each wave
-// owns NT = 4 row tiles (64 rows of W) to keep those activation reads at half
-// the W bytes.  A workgroup of 8 waves owns the 16*NT rows and a k slice
-// (grid.y = KS slices); wave w takes the 128-wide k blocks w, w+8, ... of the
-// slice.  Lane (r = l%16, g = l/16) reads W[n0 + r][k + 32i + 8g .. +7] for
-// MFMA i, so every load instruction covers 64 contiguous bytes of 16 rows.
+// owns NT row tiles (16*NT rows of W) to keep those activation reads well
+// below the W bytes.  A workgroup of NW waves owns the 16*NT rows and a k
+// slice (grid.y = KS slices); wave w takes the 128-wide k blocks w, w+NW, ...
+// of the slice.  A block is 4 packed 16 x 32 tiles per row tile, i.e. 4 KiB
+// contiguous in W, read as four 1 KiB wave loads.
 // Partial tiles of the 8 waves are summed through LDS in wave order; with
 // KS > 1 the slice sums go to part[slice][m][n] and the consumer kernel adds
 // the slices (in slice order) where it reads the result.
@@ -78,9 +78,11 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const uint16_t* __
 #pragma unroll
     for (int b = 0; b < MT; ++b) acc[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // packed tile (n0/16 + nt, k0/32) of W, this lane's chunk
   const uint16_t* wrow[NT];
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) wrow[nt] = W + static_cast<size_t>(n0 + nt * 16 + r) * Kp + k0 + 8 * g;
+  for (int nt = 0; nt < NT; ++nt)
+    wrow[nt] = W + (static_cast<size_t>(n0 / 16 + nt) * (Kp / 32) + k0 / 32) * 512 + lane * 8;
   const uint16_t* xrow[MT];
   bool xok[MT];
 #pragma unroll
@@ -102,7 +104,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const uint16_t* __
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) wv[sl][nt][i] = *reinterpret_cast<const uint4*>(wrow[nt] + k + 32 * i);
+        for (int i = 0; i < 4; ++i) wv[sl][nt][i] = *reinterpret_cast<const uint4*>(wrow[nt] + (k / 32 + i) * 512);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -197,8 +199,8 @@ __global__ __launch_bounds__(256) void reduce_parts_kernel(const float* __restri
 // ---------------------------------------------------------------------------
 // Tiled GEMM (M > 64: prefill chunks, large decode batches), bound by the
 // matrix cores.  Block tile 256 (n, rows of W) x 256 (m, activation rows) x 64
-// (k); 4 waves in 2x2, each 128x128 = 4x4 tiles of v_mfma_f32_32x32x16_bf16
-// (A = W rows, B = activation rows).  Lane l supplies A[l%32][8(l/32) .. +7]
+// (k); WN x WM waves (4 x 2: two per SIMD), each (256/WN) x (256/WM) = 2 x 4
+// tiles of v_mfma_f32_32x32x16_bf16 (A = W rows, B = activation rows).  Lane l supplies A[l%32][8(l/32) .. +7]
 // and B[8(l/32) .. +7][l%32] and receives D rows 8q + 4(l/32) + i (q = 0..3,
 // i = 0..3) of column l%32: four consecutive output features of one
 // activation row per q.  Operand tiles are staged through LDS, double
@@ -242,15 +244,20 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm_tiled_kernel(const uint16_t
 
   // global -> registers -> LDS
   uint4 wr[CPT], xr[CPT];
+  // W: chunk c is chunk q = c % 64 of packed tile t = c / 64, i.e. of row tile
+  // t / 2 and k tile t % 2 of this block: W row 16(t/2) + q%16, chunk
+  // 4(t%2) + q/16 of the 64-wide k tile.  X: chunk c is row c / 8, chunk c % 8.
   auto fetch = [&](int k) {
 #pragma unroll
     for (int j = 0; j < CPT; ++j) {
       const int c = tid + NTH * j;
-      const int row = c >> 3, ch = c & 7;
-      const int n = n0 + row, m = m0 + row;
-      wr[j] = n < N ? *reinterpret_cast<const uint4*>(W + static_cast<size_t>(n) * Kp + k + 8 * ch)
+      const int t = c >> 6, q = c & 63;
+      const int n = n0 + (t >> 1) * 16;
+      wr[j] = n < N ? *reinterpret_cast<const uint4*>(
+                          W + (static_cast<size_t>(n >> 4) * (Kp >> 5) + (k >> 5) + (t & 1)) * 512 + q * 8)
                     : make_uint4(0, 0, 0, 0);
-      xr[j] = m < M ? *reinterpret_cast<const uint4*>(X + static_cast<size_t>(m) * ldx + k + 8 * ch)
+      const int m = m0 + (c >> 3);
+      xr[j] = m < M ? *reinterpret_cast<const uint4*>(X + static_cast<size_t>(m) * ldx + k + 8 * (c & 7))
                     : make_uint4(0, 0, 0, 0);
     }
   };
@@ -258,9 +265,11 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm_tiled_kernel(const uint16_t
 #pragma unroll
     for (int j = 0; j < CPT; ++j) {
       const int c = tid + NTH * j;
-      const int row = c >> 3, ch = c & 7;
-      ws[buf][row * 8 + (ch ^ (row & 7))] = wr[j];
-      xs[buf][row * 8 + (ch ^ (row & 7))] = xr[j];
+      const int t = c >> 6, q = c & 63;
+      const int wrow = (t >> 1) * 16 + (q & 15), wch = (t & 1) * 4 + (q >> 4);
+      ws[buf][wrow * 8 + (wch ^ (wrow & 7))] = wr[j];
+      const int xrow = c >> 3, xch = c & 7;
+      xs[buf][xrow * 8 + (xch ^ (xrow & 7))] = xr[j];
     }
   };
 
@@ -355,7 +364,7 @@ int gemm_splits(int M, int N, int Kp, int epilogue) {
 template <int MT, int NT, int EPI>
 static void launch_skinny(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, float* outf,
                           uint16_t* outb, int ldo, float* part, int ks, hipStream_t s) {
-  hipLaunchKernelGGL((gemm_skinny_kernel<MT, NT, EPI, kSkinnyPF, kSkinnyWaves>), dim3(N / (16 * NT), ks),
+  launch_kernel((gemm_skinny_kernel<MT, NT, EPI, kSkinnyPF, kSkinnyWaves>), dim3(N / (16 * NT), ks),
                      dim3(kSkinnyWaves * 64), 0, s, X, ldx, W, Kp, M, N, outf, outb, ldo, part);
 }
 
@@ -380,7 +389,7 @@ static hipError_t launch_epi(const uint16_t* X, int ldx, const uint16_t* W, int 
       launch_skinny_m<2, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, ks, s);
   } else {
     const int tiles = ((N + TBN - 1) / TBN) * ((M + TBM - 1) / TBM);
-    hipLaunchKernelGGL((gemm_tiled_kernel<EPI, kTiledWN, kTiledWM>), dim3(tiles), dim3(kTiledWN * kTiledWM * 64), 0, s,
+    launch_kernel((gemm_tiled_kernel<EPI, kTiledWN, kTiledWM>), dim3(tiles), dim3(kTiledWN * kTiledWM * 64), 0, s,
                        X, ldx, W, Kp, M, N, outf, outb, ldo);
   }
   return hipGetLastError();
@@ -409,9 +418,9 @@ hipError_t launch_reduce_parts(const float* part, int KS, int M, int N, int epil
   const int64_t n4 = static_cast<int64_t>(M) * N / 4;
   const int grid = static_cast<int>(std::min<int64_t>((n4 + 255) / 256, 4096));
   if (epilogue == kEpiAddF32)
-    hipLaunchKernelGGL((reduce_parts_kernel<kEpiAddF32>), dim3(grid), dim3(256), 0, s, part, KS, M, N, out, ldo);
+    launch_kernel((reduce_parts_kernel<kEpiAddF32>), dim3(grid), dim3(256), 0, s, part, KS, M, N, out, ldo);
   else
-    hipLaunchKernelGGL((reduce_parts_kernel<kEpiStoreF32>), dim3(grid), dim3(256), 0, s, part, KS, M, N, out, ldo);
+    launch_kernel((reduce_parts_kernel<kEpiStoreF32>), dim3(grid), dim3(256), 0, s, part, KS, M, N, out, ldo);
   return hipGetLastError();
 }
 

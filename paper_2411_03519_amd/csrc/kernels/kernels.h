@@ -3,10 +3,28 @@
 // them (see each kernel's comment for what it requires).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace metro {
+
+// --- launch timing ----------------------------------------------------------
+
+// Events that the next kernel dispatch records its own start and end into
+// (hipExtLaunchKernel puts them on the dispatch packet, so the interval is the
+// kernel's execution alone, as a kernel trace reports it).  Set by the runtime
+// around one launcher call while that kernel class is timed; null otherwise.
+struct LaunchEvents {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+extern thread_local LaunchEvents launch_events;
+
+template <typename F, typename... Args>
+inline void launch_kernel(F kernel, dim3 grid, dim3 block, uint32_t shmem, hipStream_t s, Args... args) {
+  hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, launch_events.start, launch_events.stop, 0u, args...);
+}
 
 // --- elementwise / row kernels (elementwise.hip) ---------------------------
 
@@ -36,12 +54,18 @@ hipError_t launch_gather_rows(const float* x, int d, const int32_t* rows, int n,
 // non-NaN value.
 hipError_t launch_argmax(const float* logits, int vocab, int rows, int32_t* out, hipStream_t s);
 
-// Random initialisation of one logical weight tensor [rows, cols] into a
-// packed matrix with row stride ld: logical row r goes to packed row
-// map(r) = (r / 16) * row_block + row_shift + r % 16.  Values are
-// 0.02 * N(0, 1) from a SplitMix64-keyed Box-Muller draw, rounded to bf16.
+// Random initialisation of one logical weight tensor [rows, cols]: logical
+// row r goes to row map(r) = (r / 16) * row_block + row_shift + r % 16 of the
+// destination, which is row-major with row stride ld, or, with packed, in MFMA
+// operand order (packed_offset) with ld = Kp.  Values are 0.02 * N(0, 1) from
+// a SplitMix64-keyed Box-Muller draw, rounded to bf16.
 hipError_t launch_init_normal(uint16_t* dst, int64_t ld, int rows, int cols, int row_block, int row_shift,
-                              uint64_t key, hipStream_t s);
+                              uint64_t key, bool packed, hipStream_t s);
+
+// Row-major bf16 [rows, cols] (row stride ld_src, device) -> rows map(r) (as
+// above) of a packed [*, Kp] weight; columns cols .. Kp-1 are written as zero.
+hipError_t launch_pack_weight(const uint16_t* src, int64_t ld_src, int rows, int cols, uint16_t* dst, int Kp,
+                              int row_block, int row_shift, hipStream_t s);
 hipError_t launch_fill_bf16(uint16_t* dst, int64_t n, uint16_t value, hipStream_t s);
 
 // Copy page src to page dst in every layer (page_elems bf16 per layer).
@@ -57,8 +81,9 @@ enum GemmEpilogue {
                      // out_bf16[m, j] = bf16(silu(gate_j) * up_j), N = 2 * F
 };
 
-// Y = X[M, Kp] (bf16, row stride ldx) x W[N, Kp]^T (bf16, packed row stride
-// Kp, Kp % 128 == 0, N % 32 == 0), fp32 accumulation, then the epilogue.
+// Y = X[M, Kp] (bf16, row stride ldx) x W[N, Kp]^T (bf16 in MFMA operand
+// order, packed_offset; Kp % 128 == 0, N % 32 == 0), fp32 accumulation, then
+// the epilogue.
 // ldo is the row stride of the output in elements.  With a workspace `part`
 // ([8][M][N] fp32) a decode-sized GEMM (M <= 64, fp32 epilogue) may split K
 // over workgroups: it then writes *n_parts > 0 slices part[s][m][n] instead of

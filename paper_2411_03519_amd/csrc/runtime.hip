@@ -129,8 +129,9 @@ metro_status prof_harvest(metro_model* m, int i) {
   return METRO_OK;
 }
 
-// Launch through `fn` (returning hipError_t), bracketed by timing events when
-// this kernel class and call phase are being profiled.
+// Launch through `fn` (returning hipError_t); when this kernel class and call
+// phase are being profiled, the kernel records a pair of events on its own
+// dispatch (see metro::launch_events).
 template <class Fn>
 metro_status launch(metro_model* m, int cls, hipStream_t s, const char* what, Fn&& fn) {
   const bool timed = cls == m->prof_cls && (m->prof_phase == 0 || m->prof_phase == m->cur_phase);
@@ -140,14 +141,12 @@ metro_status launch(metro_model* m, int cls, hipStream_t s, const char* what, Fn
     m->prof_next = (i + 1) % kProfPairs;
     metro_status st = prof_harvest(m, i);
     if (st != METRO_OK) return st;
-    HIP_TRY(m, hipEventRecord(m->prof_ev[2 * i], s));
+    metro::launch_events = {m->prof_ev[2 * i], m->prof_ev[2 * i + 1]};
   }
   hipError_t e = fn();
+  metro::launch_events = {};
   if (e != hipSuccess) return hip_fail(m, e, what);
-  if (timed) {
-    HIP_TRY(m, hipEventRecord(m->prof_ev[2 * i + 1], s));
-    m->prof_used[i] = 1;
-  }
+  if (timed) m->prof_used[i] = 1;
   return METRO_OK;
 }
 
@@ -485,21 +484,22 @@ metro_status metro_create_model(const metro_config* cfg, uint64_t init_seed, met
     auto chk = [&](hipError_t x) {
       if (r == hipSuccess) r = x;
     };
-    chk(metro::launch_init_normal(m->embed, d, V, d, 16, 0, key(METRO_W_EMBED, -1), 0));
-    chk(metro::launch_init_normal(m->lm_head, d, V, d, 16, 0, key(METRO_W_LM_HEAD, -1), 0));
+    chk(metro::launch_init_normal(m->embed, d, V, d, 16, 0, key(METRO_W_EMBED, -1), false, 0));
+    chk(metro::launch_init_normal(m->lm_head, d, V, d, 16, 0, key(METRO_W_LM_HEAD, -1), true, 0));
     chk(metro::launch_fill_bf16(m->final_norm, d, one, 0));
     for (int l = 0; l < c.n_layers; ++l) {
       Layer& L = m->layers[l];
       chk(metro::launch_fill_bf16(L.attn_norm, d, one, 0));
       chk(metro::launch_fill_bf16(L.ffn_norm, d, one, 0));
-      chk(metro::launch_init_normal(L.wqkv, d, m->q_dim, d, 16, 0, key(METRO_W_WQ, l), 0));
-      chk(metro::launch_init_normal(L.wqkv, d, m->kv_dim, d, 16, m->q_dim, key(METRO_W_WK, l), 0));
-      chk(metro::launch_init_normal(L.wqkv, d, m->kv_dim, d, 16, m->q_dim + m->kv_dim, key(METRO_W_WV, l), 0));
-      chk(metro::launch_init_normal(L.wo, m->q_dim, d, m->q_dim, 16, 0, key(METRO_W_WO, l), 0));
-      chk(metro::launch_init_normal(L.wgu, d, F, d, 32, 0, key(METRO_W_WGATE, l), 0));
-      chk(metro::launch_init_normal(L.wgu, d, F, d, 32, 16, key(METRO_W_WUP, l), 0));
+      chk(metro::launch_init_normal(L.wqkv, d, m->q_dim, d, 16, 0, key(METRO_W_WQ, l), true, 0));
+      chk(metro::launch_init_normal(L.wqkv, d, m->kv_dim, d, 16, m->q_dim, key(METRO_W_WK, l), true, 0));
+      chk(metro::launch_init_normal(L.wqkv, d, m->kv_dim, d, 16, m->q_dim + m->kv_dim, key(METRO_W_WV, l), true,
+                                    0));
+      chk(metro::launch_init_normal(L.wo, m->q_dim, d, m->q_dim, 16, 0, key(METRO_W_WO, l), true, 0));
+      chk(metro::launch_init_normal(L.wgu, d, F, d, 32, 0, key(METRO_W_WGATE, l), true, 0));
+      chk(metro::launch_init_normal(L.wgu, d, F, d, 32, 16, key(METRO_W_WUP, l), true, 0));
       if (m->Fp != F) chk(metro::launch_fill_bf16(L.wdown, static_cast<int64_t>(d) * m->Fp, 0, 0));
-      chk(metro::launch_init_normal(L.wdown, m->Fp, d, F, 16, 0, key(METRO_W_WDOWN, l), 0));
+      chk(metro::launch_init_normal(L.wdown, m->Fp, d, F, 16, 0, key(METRO_W_WDOWN, l), true, 0));
     }
     if (r == hipSuccess) r = hipDeviceSynchronize();
     if (r != hipSuccess) return bail(hip_fail(nullptr, r, "weight initialisation"));
@@ -548,21 +548,21 @@ metro_status metro_load_weight(metro_model* m, int32_t id, int32_t layer, const 
   if (n != rows * cols)
     return fail(METRO_E_INVAL, "weight %d: %lld elements given, %lld expected", id, (long long)n,
                 (long long)(rows * cols));
-  if (rows == 1) {
-    HIP_TRY(m, hipMemcpy(base, src, cols * 2, hipMemcpyHostToDevice));
+  if (rows == 1 || id == METRO_W_EMBED) {  // norms and the embedding table stay row-major
+    HIP_TRY(m, hipMemcpy(base, src, rows * cols * 2, hipMemcpyHostToDevice));
     return METRO_OK;
   }
-  // rows go in runs of 16 consecutive logical rows to packed row
-  // (r / 16) * blk + shift + r % 16
-  if (blk == 16) {
-    HIP_TRY(m, hipMemcpy2D(base + shift * ld, ld * 2, src, cols * 2, cols * 2, rows, hipMemcpyHostToDevice));
-    return METRO_OK;
-  }
-  for (int64_t r0 = 0; r0 < rows; r0 += 16) {
-    const int64_t pr = (r0 / 16) * blk + shift;
-    const int64_t nr = std::min<int64_t>(16, rows - r0);
-    HIP_TRY(m, hipMemcpy2D(base + pr * ld, ld * 2, src + r0 * cols, cols * 2, cols * 2, nr, hipMemcpyHostToDevice));
-  }
+  // projections: row-major upload into a staging buffer, then rearranged into
+  // MFMA operand order, logical row r going to row (r / 16) * blk + shift + r % 16
+  uint16_t* stage = nullptr;
+  HIP_TRY(m, hipMalloc(&stage, rows * cols * 2));
+  hipError_t e = hipMemcpy(stage, src, rows * cols * 2, hipMemcpyHostToDevice);
+  if (e == hipSuccess)
+    e = metro::launch_pack_weight(stage, cols, static_cast<int>(rows), static_cast<int>(cols), base,
+                                  static_cast<int>(ld), static_cast<int>(blk), static_cast<int>(shift), nullptr);
+  if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
+  (void)hipFree(stage);
+  if (e != hipSuccess) return hip_fail(m, e, "weight upload");
   return METRO_OK;
 }
 
@@ -843,6 +843,16 @@ metro_status metro_profile_stop(metro_model* m, double* total_ms, int64_t* launc
 // ---------------------------------------------------------------------------
 // Single-op entry points (include/metro_ops.h)
 // ---------------------------------------------------------------------------
+
+metro_status metro_op_pack_weight(const uint16_t* W_rowmajor, int32_t ld, int32_t N, int32_t K, int32_t Kp,
+                                  uint16_t* W_packed, void* stream) {
+  g_err.clear();
+  if (!W_rowmajor || !W_packed || N <= 0 || N % 16 || Kp <= 0 || Kp % 128 || K <= 0 || K > Kp || ld < K)
+    return fail(METRO_E_INVAL, "pack_weight: bad shape (N %% 16, Kp %% 128, 0 < K <= Kp, ld >= K required)");
+  hipError_t e = metro::launch_pack_weight(W_rowmajor, ld, N, K, W_packed, Kp, 16, 0, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(nullptr, e, "launch_pack_weight");
+  return METRO_OK;
+}
 
 metro_status metro_op_gemm(const uint16_t* X, int32_t ldx, const uint16_t* W, int32_t Kp, int32_t M, int32_t N,
                            int32_t epilogue, float* out_f32, uint16_t* out_bf16, int32_t ldo, float* workspace,

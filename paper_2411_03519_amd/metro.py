@@ -66,6 +66,7 @@ _SIGS = {
     "metro_decode_step": (_i32, [_vp, _i32, _vp, _vp, _vp, _vp, _vp]),
     "metro_profile_start": (_i32, [_vp, _i32, _i32]),
     "metro_profile_stop": (_i32, [_vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_i64)]),
+    "metro_op_pack_weight": (_i32, [_vp, _i32, _i32, _i32, _i32, _vp, _vp]),
     "metro_op_gemm": (_i32, [_vp, _i32, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp]),
     "metro_op_rmsnorm": (_i32, [_vp, _vp, ctypes.c_float, _vp, _i32, _i32, _vp]),
     "metro_op_argmax": (_i32, [_vp, _i32, _i32, _vp, _vp]),
@@ -225,8 +226,15 @@ class Model:
 
 # -- single-op entry points -------------------------------------------------------
 
+def op_pack_weight(W, ld: int, N: int, K: int, Kp: int, out, stream=None):
+    """Row-major bf16 W [N, ld] (first K columns) -> out, the [N, Kp] matrix in
+    the matrix-core operand order op_gemm reads (columns K .. Kp-1 zero)."""
+    check(lib.metro_op_pack_weight(_ptr(W), ld, N, K, Kp, _ptr(out), _stream(stream)))
+
+
 def op_gemm(X, W, M: int, N: int, Kp: int, epilogue: int, out, ldo: int, ldx: int | None = None, workspace=None,
             stream=None):
+    """W is packed (op_pack_weight)."""
     f32 = out if epilogue != EPI_SWIGLU else None
     b16 = out if epilogue == EPI_SWIGLU else None
     check(lib.metro_op_gemm(_ptr(X), ldx if ldx is not None else Kp, _ptr(W), Kp, M, N, epilogue, _ptr(f32),

@@ -1,5 +1,6 @@
 """Single kernels of the HIP path against CPU references (through metro_ops.h).
 
+Weight packing: bit-exact against the operand-order layout written out.
 GEMM: every epilogue, in the skinny (M <= 64) and tiled (M > 64) kernels,
 with ragged M, K padded to 128 and N covering several tiles plus a tail.
 The reference products are exact-value float64 sums of the same bf16
@@ -34,6 +35,44 @@ def rand_bf16(rng, shape, scale=1.0):
     return synth.f32_to_bf16_bits(rng.standard_normal(shape).astype(np.float32) * np.float32(scale))
 
 
+def packed_layout(W, K, Kp):
+    """The operand-order layout of metro_ops.h written out element by element:
+    W[n, k] (k < K, else 0) at ((n/16 * Kp/32 + k/32) * 64 + n%16 + 16*((k/8)%4)) * 8 + k%8."""
+    N = W.shape[0]
+    n, k = np.meshgrid(np.arange(N), np.arange(Kp), indexing="ij")
+    idx = ((n // 16 * (Kp // 32) + k // 32) * 64 + n % 16 + 16 * ((k // 8) % 4)) * 8 + k % 8
+    out = np.zeros(N * Kp, np.uint16)
+    vals = np.zeros((N, Kp), np.uint16)
+    vals[:, :K] = W[:, :K]
+    out[idx.ravel()] = vals.ravel()
+    return out
+
+
+def pack_dev(metro, W, K, Kp):
+    """Device copy of row-major W [N, ld] in the GEMM's packed layout."""
+    N, ld = W.shape
+    out = torch.zeros(N * Kp, dtype=torch.int16, device="cuda")
+    metro.op_pack_weight(dev_u16(W), ld, N, K, Kp, out)
+    return out
+
+
+@pytest.mark.parametrize("N,K,ld,Kp", [(16, 128, 128, 128), (48, 200, 208, 256), (96, 688, 700, 768)])
+def test_pack_weight_layout(metro, N, K, ld, Kp):
+    rng = np.random.default_rng(N + K)
+    W = rng.integers(0, 1 << 16, size=(N, ld), dtype=np.uint16)
+    got = pack_dev(metro, W, K, Kp)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(got.cpu().numpy().view(np.uint16), packed_layout(W, K, Kp))
+
+
+def test_pack_weight_rejects_bad_shapes(metro):
+    W = torch.zeros(64 * 256, dtype=torch.int16, device="cuda")
+    out = torch.zeros(64 * 256, dtype=torch.int16, device="cuda")
+    for N, K, ld, Kp in [(24, 128, 128, 128), (16, 100, 128, 120), (16, 300, 300, 256), (16, 128, 64, 128)]:
+        with pytest.raises(metro.MetroError):
+            metro.op_pack_weight(W, ld, N, K, Kp, out)
+
+
 GEMM_CASES = [(1, 256, 64), (7, 640, 96), (16, 256, 32), (25, 4096, 512), (33, 768, 160), (64, 384, 1376),
               (65, 256, 160), (200, 1152, 416), (129, 128, 96), (300, 4096, 256)]
 
@@ -54,7 +93,7 @@ def test_gemm_f32_epilogues(metro, M, K, N, epi, split):
     init = rng.standard_normal((M, ldo)).astype(np.float32)
     out = torch.from_numpy(init.copy()).cuda()
     ws = torch.full((8, M, N), float("nan"), device="cuda") if split else None
-    metro.op_gemm(dev_u16(X), dev_u16(W), M, N, Kp, epi, out, ldo, workspace=ws)
+    metro.op_gemm(dev_u16(X), pack_dev(metro, W, Kp, Kp), M, N, Kp, epi, out, ldo, workspace=ws)
     torch.cuda.synchronize()
     got = out.cpu().numpy().astype(np.float64)
     want = ref + (init[:, :N] if epi == 1 else 0.0)
@@ -76,7 +115,7 @@ def test_gemm_swiglu_epilogue(metro, M, K, F):
         packed[32 * b + 16:32 * b + 32] = Wu[16 * b:16 * b + 16]
     ldo = (F + 127) // 128 * 128
     out = torch.zeros((M, ldo), dtype=torch.int16, device="cuda")
-    metro.op_gemm(dev_u16(X), dev_u16(packed), M, 2 * F, K, 2, out, ldo)
+    metro.op_gemm(dev_u16(X), pack_dev(metro, packed, K, K), M, 2 * F, K, 2, out, ldo)
     torch.cuda.synchronize()
     got = bf16_bits_to_f64(out.cpu().numpy().view(np.uint16))
     xf, wg, wu = bf16_bits_to_f64(X), bf16_bits_to_f64(Wg), bf16_bits_to_f64(Wu)
