@@ -8,6 +8,7 @@ time, with no batching, blocking or fusion.
 from __future__ import annotations
 
 import math
+import os
 from dataclasses import dataclass
 
 import numpy as np
@@ -227,21 +228,71 @@ class OracleModel:
     moves the result (the noise floor a tolerance must allow for).
     """
 
-    def __init__(self, shape: LlamaShape, weights: dict, quantize: bool = True, dtype=np.float64):
+    def __init__(self, shape: LlamaShape, weights: dict, quantize: bool = True, dtype=np.float64,
+                 lazy: bool = False):
+        """``lazy``: keep ``weights`` as given and convert each layer's matrices
+        (and the embedding rows and LM-head rows in use) to the arithmetic dtype
+        when they are used, so that a full-depth 8B or 70B model fits in host
+        memory.  The values, and so every result, are the same either way."""
         self.shape = shape
         self.quantize = quantize
         self.dtype = np.dtype(dtype)
+        self.lazy = lazy
+        assert len(weights["layers"]) == shape.n_layers
+        self.final_norm = self.load(weights["final_norm"])
+        if lazy:
+            self._raw = weights
+            self._cur = (-1, None)
+        else:
+            self.embed = self.load(weights["embed"])
+            self.lm_head = self.load(weights["lm_head"])
+            self.layers = [{k: self.load(lw[k]) for k in _LAYER_KEYS} for lw in weights["layers"]]
 
-        def load(a):
-            a = np.asarray(a)
-            w = bf16_bits_to_f64(a) if a.dtype == np.uint16 else a.astype(np.float64)
-            return self.q(w)
+    def load(self, a) -> np.ndarray:
+        """Weights in the arithmetic dtype.  uint16 arrays are bf16 bit patterns,
+        whose values bf16 rounding leaves unchanged; other arrays are real
+        values, rounded to bf16 when ``quantize``."""
+        a = np.asarray(a)
+        if a.dtype != np.uint16:
+            return self.q(a.astype(np.float64))
+        if a.size < (1 << 22):
+            return bf16_bits_to_f64(a).astype(self.dtype, copy=False)
+        # large matrices: decode row blocks on several threads (numpy releases the GIL)
+        from concurrent.futures import ThreadPoolExecutor
+        out = np.empty(a.shape, dtype=self.dtype)
+        rows = a.reshape(a.shape[0], -1)
+        flat = out.reshape(a.shape[0], -1)
+        step = max(1, rows.shape[0] // 64)
 
-        self.embed = load(weights["embed"])
-        self.final_norm = load(weights["final_norm"])
-        self.lm_head = load(weights["lm_head"])
-        self.layers = [{k: load(lw[k]) for k in _LAYER_KEYS} for lw in weights["layers"]]
-        assert len(self.layers) == shape.n_layers
+        def work(r0):
+            flat[r0:r0 + step] = bf16_bits_to_f64(rows[r0:r0 + step])
+        with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+            list(ex.map(work, range(0, rows.shape[0], step)))
+        return out
+
+    def layer(self, li: int) -> dict:
+        if not self.lazy:
+            return self.layers[li]
+        if self._cur[0] != li:
+            self._cur = (-1, None)  # free the previous layer first
+            self._cur = (li, {k: self.load(self._raw["layers"][li][k]) for k in _LAYER_KEYS})
+        return self._cur[1]
+
+    def embed_rows(self, tokens) -> np.ndarray:
+        if not self.lazy:
+            return self.embed[tokens]
+        return self.load(np.asarray(self._raw["embed"])[tokens])
+
+    def lm_head_logits(self, hf) -> np.ndarray:
+        """``hf @ W_lm^T``; in lazy mode one block of vocabulary rows at a time
+        (each logit is the same dot product either way)."""
+        if not self.lazy:
+            return hf @ self.lm_head.T
+        W = np.asarray(self._raw["lm_head"])
+        out = np.empty((hf.shape[0], W.shape[0]), dtype=np.result_type(hf.dtype, self.dtype))
+        for r0 in range(0, W.shape[0], 16384):
+            out[:, r0:r0 + 16384] = hf @ self.load(W[r0:r0 + 16384]).T
+        return out
 
     def q(self, x):
         """The bf16 storage points of the precision contract (identity if not
@@ -254,7 +305,7 @@ class OracleModel:
     # -- one decoder block ----------------------------------------------------
     def block(self, li: int, x: np.ndarray, cache, positions: np.ndarray) -> np.ndarray:
         S = self.shape
-        W = self.layers[li]
+        W = self.layer(li)
         n = x.shape[0]
         h = self.q(rms_norm(x, W["attn_norm"], S.rms_eps))
         q = (h @ W["wq"].T).reshape(n, S.n_heads, S.head_dim)
@@ -272,24 +323,27 @@ class OracleModel:
         return x + a @ W["wdown"].T
 
     # -- forward over new tokens of one sequence --------------------------------
-    def forward(self, cache, tokens) -> np.ndarray:
+    def forward(self, cache, tokens, logits_for=None) -> np.ndarray:
         """Append ``tokens`` to the sequence held by ``cache``; return float32
-        logits ``[len(tokens), V]`` for every new position."""
+        logits ``[len(tokens), V]`` for every new position, or only for the
+        new positions indexed by ``logits_for``."""
         tokens = np.asarray(tokens, dtype=np.int64)
         positions = np.arange(cache.length, cache.length + len(tokens))
-        x = self.embed[tokens]
+        x = self.embed_rows(tokens)
         for li in range(self.shape.n_layers):
             x = self.block(li, x, cache, positions)
         cache.advance(len(tokens))
+        if logits_for is not None:
+            x = x[logits_for]
         hf = self.q(rms_norm(x, self.final_norm, self.shape.rms_eps))
-        return (hf @ self.lm_head.T).astype(np.float32)
+        return self.lm_head_logits(hf).astype(np.float32)
 
     def hidden_layers(self, cache, tokens, n_layers: int) -> np.ndarray:
         """Residual stream after the first ``n_layers`` blocks (for sampling the
         cost of the full model on the CPU; no logits)."""
         tokens = np.asarray(tokens, dtype=np.int64)
         positions = np.arange(cache.length, cache.length + len(tokens))
-        x = self.embed[tokens]
+        x = self.embed_rows(tokens)
         for li in range(n_layers):
             x = self.block(li, x, cache, positions)
         cache.advance(len(tokens))
@@ -302,7 +356,7 @@ class OracleModel:
         step = len(prompt) if chunk is None else chunk
         last = None
         for s in range(0, len(prompt), step):
-            last = self.forward(cache, prompt[s:s + step])[-1]
+            last = self.forward(cache, prompt[s:s + step], logits_for=[-1])[0]
         return last
 
     def generate(self, prompt, n_new: int, chunk: int | None = None):

@@ -77,14 +77,25 @@ def draw_tensor(cfg: dict, name: str, layer: int, seed: int, norm: str = "ones")
     return f32_to_bf16_bits(w)
 
 
-def llama_weights(cfg: dict, seed: int, norm: str = "ones") -> dict:
-    """All weights of a Llama-style decoder as bf16 bit arrays ([out, in] row-major)."""
+def llama_weights(cfg: dict, seed: int, norm: str = "ones", workers: int = 1) -> dict:
+    """All weights of a Llama-style decoder as bf16 bit arrays ([out, in] row-major).
+
+    Every tensor has its own random stream, so ``workers`` > 1 (tensors drawn
+    on that many threads) gives the same arrays."""
+    jobs = [("embed", -1), ("final_norm", -1), ("lm_head", -1)]
+    jobs += [(n, li) for li in range(cfg["n_layers"]) for n in LAYER_TENSORS]
+    if workers > 1:
+        from concurrent.futures import ThreadPoolExecutor
+        with ThreadPoolExecutor(max_workers=workers) as ex:
+            arrs = list(ex.map(lambda j: draw_tensor(cfg, j[0], j[1], seed, norm), jobs))
+    else:
+        arrs = [draw_tensor(cfg, n, li, seed, norm) for n, li in jobs]
+    got = dict(zip(jobs, arrs))
     return {
-        "embed": draw_tensor(cfg, "embed", -1, seed, norm),
-        "final_norm": draw_tensor(cfg, "final_norm", -1, seed, norm),
-        "lm_head": draw_tensor(cfg, "lm_head", -1, seed, norm),
-        "layers": [{n: draw_tensor(cfg, n, li, seed, norm) for n in LAYER_TENSORS}
-                   for li in range(cfg["n_layers"])],
+        "embed": got[("embed", -1)],
+        "final_norm": got[("final_norm", -1)],
+        "lm_head": got[("lm_head", -1)],
+        "layers": [{n: got[(n, li)] for n in LAYER_TENSORS} for li in range(cfg["n_layers"])],
     }
 
 

@@ -263,6 +263,32 @@ def tiny_model():
     return OracleModel(shape_of(synth.TINY), synth.llama_weights(synth.TINY, 3, norm="random"))
 
 
+@pytest.mark.parametrize("dtype", [np.float64, np.float32])
+def test_lazy_weight_conversion_is_bitwise_the_same(dtype):
+    # vocabulary large enough for the threaded decode and several LM-head blocks
+    cfg = dict(MICRO, vocab=140_000)
+    W = synth.llama_weights(cfg, 21, norm="random")
+    eager = OracleModel(shape_of(cfg), W, dtype=dtype)
+    lazy = OracleModel(shape_of(cfg), W, dtype=dtype, lazy=True)
+    prompt = np.random.default_rng(22).integers(0, cfg["vocab"], 19)
+    t1, l1 = eager.generate(prompt, 3)
+    t2, l2 = lazy.generate(prompt, 3)
+    np.testing.assert_array_equal(t1, t2)
+    np.testing.assert_array_equal(l1, l2)
+    assert lazy.load(W["lm_head"]).dtype == dtype
+    # the threaded draw gives the same tensors
+    W4 = synth.llama_weights(cfg, 21, norm="random", workers=4)
+    for name in ("embed", "lm_head", "final_norm"):
+        np.testing.assert_array_equal(W4[name], W[name])
+    for a, b in zip(W4["layers"], W["layers"]):
+        for name in a:
+            np.testing.assert_array_equal(a[name], b[name])
+    # logits of selected positions only are the same rows
+    rows = lazy.forward(lazy.new_cache(), prompt, logits_for=[3, -1])
+    full = lazy.forward(lazy.new_cache(), prompt)
+    np.testing.assert_array_equal(rows, full[[3, -1]])
+
+
 def test_paged_kv_equals_contiguous_bitwise(tiny_model):
     S = tiny_model.shape
     prompt = np.random.default_rng(13).integers(0, S.vocab, 45)
