@@ -144,6 +144,25 @@ def uniform_contexts(seed: int, n_agents: int, lo: int, hi: int) -> np.ndarray:
     return rng.integers(lo, hi + 1, size=n_agents).astype(np.int64)
 
 
+def trace_start_contexts(seed: int = 0, n_agents: int = 1000, vocab: int = LLAMA3_8B["vocab"]) -> list:
+    """Starting contexts of the trace-driven workload: lengths lognormal
+    (median 1500, sigma 0.5) clipped to [256, 4096], uniform token ids."""
+    rng = np.random.Generator(np.random.PCG64([seed, 1500]))
+    return prompt_tokens(rng, lognormal_lengths(rng, n_agents, 1500.0, 0.5, 256, 4096), vocab)
+
+
+def llama70b_agent_batch(seed: int = 0, n_agents: int = 128, vocab: int = LLAMA3_70B["vocab"]):
+    """128 agent contexts with lengths uniform in [1024, 3072]; 32 generated tokens each."""
+    rng = np.random.Generator(np.random.PCG64([seed, 70]))
+    return prompt_tokens(rng, rng.integers(1024, 3073, size=n_agents), vocab), 32
+
+
+def feed_tokens(seed: int, n_rows: int, n_steps: int, vocab: int) -> np.ndarray:
+    """Token ids [n_rows, n_steps] fed to decode steps under teacher forcing."""
+    rng = np.random.Generator(np.random.PCG64([seed, 7]))
+    return rng.integers(0, vocab, size=(n_rows, n_steps), dtype=np.int64)
+
+
 # ----------------------------------------------------------------------------
 # Synthetic agent trace: ready-batch sizes of an out-of-order simulation
 # ----------------------------------------------------------------------------

@@ -3,13 +3,14 @@
 Logits: max-abs <= 2e-2 over all compared values and, per row,
 ||gpu - oracle||_2 / ||oracle||_2 <= 1e-2.
 
-At Llama-3 widths the max-abs figure is below what fp32 arithmetic can reach:
+At Llama-3 widths these figures are below what fp32 arithmetic can reach:
 every bf16 re-quantisation point (h, q/k/v, o, the SwiGLU product) turns a
 perturbation of relative size delta into about sqrt(delta * ulp), so the
 oracle evaluated in float32 already differs from its float64 evaluation by
-max-abs ~3.4e-2 (rel-L2 ~5.6e-3) at 8B widths and depth 2.  There the max-abs
-bound is twice that measured float32-vs-float64 spread on the same inputs
-(``noise_floor``); rel-L2 stays 1e-2.
+max-abs ~3.4e-2 (rel-L2 ~5.6e-3) at 8B widths and depth 2, and by max-abs
+~1.2e-1, rel-L2 ~2.1e-2 at full depth (32 layers).  Each bound is therefore
+the larger of the fixed figure and twice that measured float32-vs-float64
+spread of the oracle on the same inputs (``noise_floor``).
 
 Greedy tokens: compared step by step under teacher forcing (both sides are fed
 the oracle's tokens).  A different choice is a failure when the oracle's top-2
@@ -33,19 +34,22 @@ def logits_errors(got: np.ndarray, want: np.ndarray):
     return max_abs, float(np.max(rel))
 
 
-def assert_logits_close(got, want, what="", max_abs_bound=MAX_ABS):
+def assert_logits_close(got, want, what="", max_abs_bound=MAX_ABS, rel_bound=REL_L2):
     assert np.all(np.isfinite(got)), f"{what}: non-finite logits"
     max_abs, rel = logits_errors(got, want)
-    print(f"{what}: max-abs {max_abs:.3e} (bound {max_abs_bound:.3e}), max rel-L2 {rel:.3e}", flush=True)
-    assert max_abs <= max_abs_bound and rel <= REL_L2, \
-        f"{what}: max-abs {max_abs:.3e} (bound {max_abs_bound:.3e}), max rel-L2 {rel:.3e}"
+    msg = (f"{what}: max-abs {max_abs:.3e} (bound {max_abs_bound:.3e}), "
+           f"max rel-L2 {rel:.3e} (bound {rel_bound:.3e})")
+    print(msg, flush=True)
+    assert max_abs <= max_abs_bound and rel <= rel_bound, msg
     return max_abs, rel
 
 
-def noise_floor(f64_logits, f32_logits) -> float:
-    """Max-abs bound from the float32-vs-float64 spread of the oracle itself."""
-    spread, _ = logits_errors(f32_logits, f64_logits)
-    return max(MAX_ABS, 2.0 * spread)
+def noise_floor(f64_logits, f32_logits):
+    """(max-abs bound, rel-L2 bound) from the float32-vs-float64 spread of the
+    oracle itself: each the larger of the fixed figure and twice the spread."""
+    spread, rel = logits_errors(f32_logits, f64_logits)
+    print(f"oracle float32 vs float64: max-abs {spread:.3e}, max rel-L2 {rel:.3e}", flush=True)
+    return max(MAX_ABS, 2.0 * spread), max(REL_L2, 2.0 * rel)
 
 
 def top2_margin(logits: np.ndarray) -> np.ndarray:

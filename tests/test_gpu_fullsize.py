@@ -1,0 +1,231 @@
+"""The HIP path against the oracle at the workloads' real sizes.
+
+Each case runs the full batch in the launch configuration of the workload
+(512-token chunked prefill with many agents per call, then decode steps over
+the whole ready batch) and compares sampled agents with the oracle, which
+evaluates them one by one (float64 with the bf16 storage points; the same
+function in float32 gives the noise floor of the bounds, see tests/parity.py).
+Decode steps are teacher-forced with seeded token ids on both sides, so one
+oracle pass over prompt + fed tokens yields every compared row.
+
+- Llama-3-8B shape at full depth (32 layers): the benchmarked workload, 25
+  agents with lognormal prompts (median 1200), prefilled together in 512-token
+  chunks, decode at B = 25.  Sampled: the shortest prompt that needs two
+  chunks.
+- 8B widths, 2 layers, a ready batch of 800 agents (the largest batch of the
+  agent trace) with lognormal(median 1500) contexts: tiled GEMMs and 800-row
+  attention in decode.  Two agents against the oracle, and 100 agents decoded
+  again in a batch of their own (forked sequences) must give bitwise the same
+  logits.
+- 8B widths, 2 layers, the prefix-heavy batch: a 1024-token prefix prefilled
+  once and forked by page reference into 64 requests with suffixes of
+  512..2048 tokens.  One request against the oracle, and one bitwise against
+  the same request prefilled without sharing.  (Bitwise equality across batch
+  compositions holds while every GEMM of the two runs takes the same kernel:
+  a call of at most 64 tokens uses the decode GEMM, whose k-split sums in
+  another order than the tiled GEMM, so that request is chosen with a last
+  chunk of more than 64 tokens.)
+- Llama-3-70B widths (d 8192, 64/8 heads: GQA group 8, FFN 28672), 2 layers,
+  128 agents with contexts uniform in [1024, 3072], decode at B = 128.
+"""
+
+import numpy as np
+import pytest
+
+from oracle import LlamaShape, OracleModel
+from paper_2411_03519_amd import synth
+from tests.parity import assert_logits_close, check_tokens, noise_floor
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+DECODE_STEPS = 3
+
+
+@pytest.fixture(scope="module")
+def metro():
+    if not torch.cuda.is_available():
+        pytest.skip("no HIP device")
+    from paper_2411_03519_amd import metro as m
+    return m
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def oracle_rows(shape, weights, prompt, feed, dtype):
+    """Oracle logits at the prompt's last position and after each fed token."""
+    ref = OracleModel(LlamaShape(**shape), weights, dtype=dtype, lazy=True)
+    n = len(prompt)
+    seq = np.concatenate([np.asarray(prompt, np.int64), np.asarray(feed, np.int64)])
+    return ref.forward(ref.new_cache(), seq, logits_for=list(range(n - 1, n + len(feed))))
+
+
+def oracle_with_floor(shape, weights, prompt, feed, what):
+    say(f"{what}: oracle float64 ({len(prompt)} + {len(feed)} tokens)")
+    want = oracle_rows(shape, weights, prompt, feed, np.float64)
+    say(f"{what}: oracle float32")
+    f32 = oracle_rows(shape, weights, prompt, feed, np.float32)
+    return want, noise_floor(want, f32)
+
+
+def prefill_batched(m, seqs, prompts, chunk, group, keep):
+    """Chunked prefill of prompts[i] into seqs[i], ``group`` items per call.
+    Returns {i: (last-position logits, next token)} for i in keep."""
+    keep = set(keep)
+    out = {}
+    for g0 in range(0, len(seqs), group):
+        idx = list(range(g0, min(len(seqs), g0 + group)))
+        off = 0
+        while True:
+            items = [i for i in idx if off < len(prompts[i])]
+            if not items:
+                break
+            lg = torch.empty(len(items), m.vocab, device="cuda")
+            nt = torch.empty(len(items), dtype=torch.int32, device="cuda")
+            m.prefill_chunk([seqs[i] for i in items], [prompts[i][off:off + chunk] for i in items], lg, nt)
+            for j, i in enumerate(items):
+                if i in keep and off + chunk >= len(prompts[i]):
+                    out[i] = (lg[j].cpu().numpy(), int(nt[j].item()))
+            off += chunk
+    return out
+
+
+def decode_fed(m, seqs, feeds, keep):
+    """feeds.shape[1] decode steps over all seqs in one batch, row i fed
+    feeds[i, k].  Returns {i: (logits [steps, V], tokens [steps])} for i in keep."""
+    B = len(seqs)
+    lg = torch.empty(B, m.vocab, device="cuda")
+    nt = torch.empty(B, dtype=torch.int32, device="cuda")
+    sel = torch.tensor(list(keep), dtype=torch.int64, device="cuda")
+    rows = {i: ([], []) for i in keep}
+    for k in range(feeds.shape[1]):
+        m.decode_step(seqs, torch.tensor(feeds[:, k], dtype=torch.int32, device="cuda"), lg, nt)
+        lgh, nth = lg[sel].cpu().numpy(), nt[sel].cpu().numpy()
+        for j, i in enumerate(keep):
+            rows[i][0].append(lgh[j])
+            rows[i][1].append(nth[j])
+    return {i: (np.stack(a), np.array(b)) for i, (a, b) in rows.items()}
+
+
+def stitched(pre, dec, i):
+    """Prefill row then decode rows of agent i: logits [1+steps, V], tokens [1+steps]."""
+    return (np.concatenate([pre[i][0][None], dec[i][0]]), np.concatenate([[pre[i][1]], dec[i][1]]))
+
+
+def compare(what, got, toks, want, bounds):
+    assert_logits_close(got, want, what, max_abs_bound=bounds[0], rel_bound=bounds[1])
+    ties = check_tokens(toks, want, what, tie=bounds[0])
+    say(f"{what}: {len(toks)} greedy choices, {ties} tie-divergences")
+
+
+def test_llama3_8b_full_depth_benchmark_batch(metro):
+    shape = synth.LLAMA3_8B
+    V = shape["vocab"]
+    prompts, _ = synth.llama8b_agent_batch(0)
+    lens = [len(p) for p in prompts]
+    i = min((n, j) for j, n in enumerate(lens) if n > 512)[1]
+    feeds = synth.feed_tokens(0, len(prompts), DECODE_STEPS, V)
+    say("8B full depth: drawing 16 GB of weights")
+    w = synth.llama_weights(shape, 0, workers=16)
+    want, bounds = oracle_with_floor(shape, w, prompts[i], feeds[i], "8B full depth")
+    say("8B full depth: gpu (upload, prefill of 25 agents, decode at B = 25)")
+    m = metro.Model(shape, max_batch=64, max_tokens=len(prompts) * 512, max_context=4096 + 128,
+                    max_seqs=2 * len(prompts), kv_pool_bytes=24 << 30)
+    with m:
+        m.load_weights(w)
+        seqs = [m.seq_open() for _ in prompts]
+        pre = prefill_batched(m, seqs, prompts, 512, len(prompts), [i])
+        dec = decode_fed(m, seqs, feeds, [i])
+    got, toks = stitched(pre, dec, i)
+    compare("8B full depth", got, toks, want, bounds)
+
+
+def test_8b_widths_ready_batch_800(metro):
+    shape = synth.with_layers(synth.LLAMA3_8B, 2)
+    V = shape["vocab"]
+    B = 800
+    ctx = synth.trace_start_contexts(0)[:B]
+    lens = np.array([len(c) for c in ctx])
+    s1 = int(np.argmin(lens))
+    s2 = min((n, j) for j, n in enumerate(lens) if n > 1024)[1]
+    feeds = synth.feed_tokens(1, B, DECODE_STEPS, V)
+    say("B=800: drawing weights")
+    w = synth.llama_weights(shape, 1, workers=16)
+    wants = {s: oracle_with_floor(shape, w, ctx[s], feeds[s], f"B=800 agent {s}") for s in (s1, s2)}
+    subset = sorted(set(range(0, B, 8)) | {s1, s2})
+    say(f"B=800: gpu prefill of {lens.sum()} tokens, decode at B = {B} and at B = {len(subset)}")
+    m = metro.Model(shape, max_batch=B, max_tokens=32 * 512, max_context=4096 + 16, max_seqs=B + len(subset) + 8,
+                    kv_pool_bytes=16 << 30)
+    with m:
+        m.load_weights(w)
+        seqs = [m.seq_open() for _ in range(B)]
+        pre = prefill_batched(m, seqs, ctx, 512, 32, [s1, s2])
+        forks = [m.seq_fork(seqs[i], int(lens[i])) for i in subset]
+        dec = decode_fed(m, seqs, feeds, subset)
+        dec_sub = decode_fed(m, forks, feeds[subset], list(range(len(subset))))
+    for j, i in enumerate(subset):
+        np.testing.assert_array_equal(dec_sub[j][0], dec[i][0], err_msg=f"agent {i}: batch of {len(subset)}")
+        np.testing.assert_array_equal(dec_sub[j][1], dec[i][1])
+    for s in (s1, s2):
+        got, toks = stitched(pre, dec, s)
+        compare(f"B=800 agent {s} ({lens[s]} tokens)", got, toks, *wants[s])
+
+
+def test_8b_widths_prefix_heavy_forked(metro):
+    shape = synth.with_layers(synth.LLAMA3_8B, 2)
+    V = shape["vocab"]
+    prefix, suffixes, _ = synth.prefix_heavy_batch(0)
+    n = len(suffixes)
+    slen = [len(s) for s in suffixes]
+    i = int(np.argmin(slen))
+    j = min((L, k) for k, L in enumerate(slen) if L % 512 == 0 or L % 512 > 64)[1]
+    feeds = synth.feed_tokens(2, n, DECODE_STEPS, V)
+    say("prefix-heavy: drawing weights")
+    w = synth.llama_weights(shape, 2, workers=16)
+    full_i = np.concatenate([prefix, suffixes[i]])
+    want, bounds = oracle_with_floor(shape, w, full_i, feeds[i], "prefix-heavy")
+    say(f"prefix-heavy: gpu, {n} forks of a {len(prefix)}-token prefix")
+    m = metro.Model(shape, max_batch=64, max_tokens=n * 512, max_context=1024 + 2048 + 16, max_seqs=2 * n + 4,
+                    kv_pool_bytes=8 << 30)
+    with m:
+        m.load_weights(w)
+        base = m.seq_open()
+        prefill_batched(m, [base], [prefix], 512, 1, [])
+        forks = [m.seq_fork(base, len(prefix)) for _ in range(n)]
+        m.seq_close(base)
+        pre = prefill_batched(m, forks, suffixes, 512, n, [i, j])
+        dec = decode_fed(m, forks, feeds, [i, j])
+        solo = m.seq_open()
+        pre_solo = prefill_batched(m, [solo], [np.concatenate([prefix, suffixes[j]])], 512, 1, [0])
+        dec_solo = decode_fed(m, [solo], feeds[[j]], [0])
+    got_j, toks_j = stitched(pre, dec, j)
+    got_solo, toks_solo = stitched(pre_solo, dec_solo, 0)
+    np.testing.assert_array_equal(got_j, got_solo, err_msg=f"request {j}: forked vs unshared prefix")
+    np.testing.assert_array_equal(toks_j, toks_solo)
+    got, toks = stitched(pre, dec, i)
+    compare(f"prefix-heavy request {i} ({len(full_i)} tokens)", got, toks, want, bounds)
+
+
+def test_70b_widths_batch_128(metro):
+    shape = synth.with_layers(synth.LLAMA3_70B, 2)
+    V = shape["vocab"]
+    ctx, _ = synth.llama70b_agent_batch(0)
+    lens = np.array([len(c) for c in ctx])
+    i = int(np.argmin(lens))
+    feeds = synth.feed_tokens(3, len(ctx), DECODE_STEPS, V)
+    say("70B widths: drawing weights")
+    w = synth.llama_weights(shape, 3, workers=16)
+    want, bounds = oracle_with_floor(shape, w, ctx[i], feeds[i], "70B widths")
+    say(f"70B widths: gpu prefill of {lens.sum()} tokens, decode at B = {len(ctx)}")
+    m = metro.Model(shape, max_batch=len(ctx), max_tokens=32 * 512, max_context=3072 + 16,
+                    max_seqs=len(ctx) + 4, kv_pool_bytes=8 << 30)
+    with m:
+        m.load_weights(w)
+        seqs = [m.seq_open() for _ in ctx]
+        pre = prefill_batched(m, seqs, ctx, 512, 32, [i])
+        dec = decode_fed(m, seqs, feeds, [i])
+    got, toks = stitched(pre, dec, i)
+    compare(f"70B widths agent {i} ({lens[i]} tokens)", got, toks, want, bounds)
