@@ -27,6 +27,8 @@ import os
 import sys
 import time
 
+import numpy as np
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -167,6 +169,281 @@ def calibrate_copy(torch):
     print(json.dumps({"copy_bytes": nbytes, "copies": 3}), flush=True)
 
 
+# ---------------------------------------------------------------------------
+# Algorithmic work of the Llama forward (bf16 weights and KV, fp32 logits)
+# ---------------------------------------------------------------------------
+
+def layer_params(shape) -> int:
+    d, F, hd = shape["d_model"], shape["ffn_dim"], shape["head_dim"]
+    q, kv = shape["n_heads"] * hd, shape["n_kv_heads"] * hd
+    return (q + 2 * kv) * d + d * q + 2 * F * d + d * F
+
+
+def decode_weight_bytes(shape) -> int:
+    """Weight bytes one decode step streams: every layer's projections and the
+    LM head (the embedding is a gather of B rows, norms are negligible)."""
+    return 2 * (shape["n_layers"] * layer_params(shape) + shape["vocab"] * shape["d_model"])
+
+
+def kv_token_bytes(shape) -> int:
+    return 2 * 2 * shape["n_kv_heads"] * shape["head_dim"] * shape["n_layers"]
+
+
+def decode_step_bytes(shape, ctx_lens) -> int:
+    """Weights + KV read of every row's context + KV write of the new token +
+    fp32 logits, for one decode step over rows with these context lengths."""
+    B = len(ctx_lens)
+    return (decode_weight_bytes(shape) + (int(sum(ctx_lens)) + B) * kv_token_bytes(shape)
+            + B * shape["vocab"] * 4)
+
+
+def prefill_flops(shape, positions_per_item, logit_rows) -> float:
+    """Linear layers per token + causal attention per (query, visible key) +
+    the LM head for the rows that return logits."""
+    L, hd, nq = shape["n_layers"], shape["head_dim"], shape["n_heads"]
+    tokens = sum(len(p) for p in positions_per_item)
+    keys = sum(int(np.sum(np.asarray(p, np.int64) + 1)) for p in positions_per_item)
+    return (2.0 * L * layer_params(shape) * tokens + 4.0 * L * nq * hd * keys
+            + 2.0 * logit_rows * shape["vocab"] * shape["d_model"])
+
+
+def prefill_all(model, seqs, prompts, chunk, group, torch, next_tok=None):
+    """Chunked prefill of prompts[i] into seqs[i], ``group`` items per call;
+    the greedy token of each finished item goes to next_tok[i] (device)."""
+    for g0 in range(0, len(seqs), group):
+        idx = list(range(g0, min(len(seqs), g0 + group)))
+        off = 0
+        while True:
+            items = [i for i in idx if off < len(prompts[i])]
+            if not items:
+                break
+            nt = torch.empty(len(items), dtype=torch.int32, device="cuda")
+            model.prefill_chunk([seqs[i] for i in items], [prompts[i][off:off + chunk] for i in items], None, nt)
+            done = [j for j, i in enumerate(items) if off + chunk >= len(prompts[i])]
+            if done and next_tok is not None:
+                dst = torch.tensor([items[j] for j in done], dtype=torch.int64, device="cuda")
+                next_tok[dst] = nt[torch.tensor(done, dtype=torch.int64, device="cuda")]
+            off += chunk
+
+
+def hbm_roofline(bytes_total, seconds, what):
+    achieved = bytes_total / seconds / 1e9
+    return {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": what}
+
+
+def bench_trace(args, torch, metro, synth):
+    """Decode driven by the seeded agent trace: 1000 agents with lognormal
+    (median 1500) starting contexts, prefilled before timing; each of 200 ticks
+    decodes one token for every ready agent (ready batches of ~50..800); then a
+    fixed-batch sweep over agents 0..B-1."""
+    shape = synth.LLAMA3_8B
+    V = shape["vocab"]
+    ctx = synth.trace_start_contexts(args.seed)
+    n = len(ctx)
+    batches = [b for b in synth.agent_trace(args.seed) if len(b)]
+    sweep, sweep_steps = [50, 100, 200, 400, 800], 3
+    lens = np.array([len(c) for c in ctx], np.int64)
+    extra = np.zeros(n, np.int64)
+    for b in batches:
+        extra[b] += 1
+    extra[:max(sweep)] += (1 + sweep_steps) * len(sweep)
+    page_bytes = 16 * kv_token_bytes(shape)
+    pages = int(np.sum((lens + extra + 15) // 16)) + 64
+    log(f"trace: {n} agents, {lens.sum()} context tokens, {len(batches)} ticks, "
+        f"{sum(len(b) for b in batches)} decode tokens; KV pool {pages * page_bytes / 1e9:.1f} GB")
+    model = metro.Model(shape, max_batch=n, max_tokens=32 * 512, max_context=int((lens + extra).max()) + 16,
+                        max_seqs=n + 8, kv_pool_bytes=pages * page_bytes, seed=args.seed)
+    seqs = np.array([model.seq_open() for _ in range(n)], np.int64)
+    last = torch.zeros(n, dtype=torch.int32, device="cuda")
+    t0 = time.time()
+    prefill_all(model, list(seqs), ctx, 512, 32, torch, last)
+    torch.cuda.synchronize()
+    log(f"trace: contexts prefilled in {time.time() - t0:.1f}s")
+    logits = torch.empty(n, V, dtype=torch.float32, device="cuda")
+    nxt = torch.empty(n, dtype=torch.int32, device="cuda")
+    cur = lens.copy()
+
+    def timed_step(rows):
+        """One decode step over agent ids ``rows``; returns (GPU ms, algorithmic bytes)."""
+        B = len(rows)
+        idx = torch.from_numpy(rows).cuda()
+        tok = last[idx]
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        model.decode_step(seqs[rows], tok, logits[:B], nxt[:B])
+        e1.record()
+        last[idx] = nxt[:B]
+        nbytes = decode_step_bytes(shape, cur[rows])
+        cur[rows] += 1
+        return e0, e1, nbytes
+
+    recs = [timed_step(b) for b in batches]
+    torch.cuda.synchronize()
+    ms = [a.elapsed_time(b) for a, b, _ in recs]
+    tokens = sum(len(b) for b in batches)
+    value = tokens / (sum(ms) / 1e3)
+    roof = hbm_roofline(sum(r[2] for r in recs), sum(ms) / 1e3, "whole decode step (weights + KV + logits)")
+    sizes = np.array([len(b) for b in batches])
+    log(f"trace: {tokens} tokens in {sum(ms):.1f} ms GPU time -> {value:.0f} tok/s, "
+        f"{roof['frac'] * 100:.1f}% of HBM peak")
+    fixed = {}
+    for B in sweep:
+        rows = np.arange(B, dtype=np.int64)
+        timed_step(rows)
+        r = [timed_step(rows) for _ in range(sweep_steps)]
+        torch.cuda.synchronize()
+        t = sum(a.elapsed_time(b) for a, b, _ in r) / 1e3
+        fixed[str(B)] = {"tokens_per_s": round(B * sweep_steps / t, 1),
+                         "hbm_frac": round(sum(x[2] for x in r) / t / 1e9 / HBM_PEAK_GBS, 4),
+                         "ms_per_step": round(t * 1e3 / sweep_steps, 3)}
+        log(f"trace sweep B={B}: {fixed[str(B)]}")
+    model.close()
+    return {"metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": 1, "warmup": 0,
+            "ms_per_step": round(sum(ms), 2), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": "bf16", "data": "synthetic: seeded agent trace and token ids, random N(0,0.02) bf16 weights",
+            "config": {"workload": "Llama-3-8B-shaped decoder driven by a seeded agent trace: 1000 agents on a "
+                                   "100x140 grid, Chebyshev radius 5, 200 ticks; contexts lognormal(median 1500) "
+                                   "clipped to [256,4096], prefilled before timing",
+                       "ticks": len(batches), "decode_tokens": tokens, "batch_min": int(sizes.min()),
+                       "batch_median": float(np.median(sizes)), "batch_max": int(sizes.max()),
+                       "context_tokens": int(lens.sum())},
+            "roofline": roof, "fixed_batch": fixed}
+
+
+def bench_prefix(args, torch, metro, synth):
+    """Prefix-heavy requests: a 1024-token prefix prefilled once and forked by
+    page reference into 64 requests, their suffixes (512..2048 tokens)
+    prefilled in 512-token chunks, then 31 decode steps at B = 64."""
+    shape = synth.LLAMA3_8B
+    V = shape["vocab"]
+    prefix, suffixes, n_new = synth.prefix_heavy_batch(args.seed)
+    n = len(suffixes)
+    slen = np.array([len(s) for s in suffixes], np.int64)
+    page_bytes = 16 * kv_token_bytes(shape)
+    pages = 64 + int(np.sum((slen + n_new + 15) // 16)) + n + 64
+    model = metro.Model(shape, max_batch=n, max_tokens=n * 512, max_context=1024 + int(slen.max()) + n_new + 16,
+                        max_seqs=2 * n + 8, kv_pool_bytes=pages * page_bytes, seed=args.seed)
+    positions = [np.arange(len(prefix))] + [np.arange(len(prefix), len(prefix) + L) for L in slen]
+    flops = prefill_flops(shape, positions, 2 + n)
+    tok = torch.zeros(n, dtype=torch.int32, device="cuda")
+    tok2 = torch.empty_like(tok)
+    logits = torch.empty(n, V, dtype=torch.float32, device="cuda")
+
+    def step():
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev[0].record()
+        base = model.seq_open()
+        prefill_all(model, [base], [prefix], 512, 1, torch)
+        forks = [model.seq_fork(base, len(prefix)) for _ in range(n)]
+        model.seq_close(base)
+        prefill_all(model, forks, suffixes, 512, n, torch, tok)
+        ev[1].record()
+        cur = [tok, tok2]
+        for _ in range(n_new - 1):
+            model.decode_step(forks, cur[0], logits, cur[1])
+            cur.reverse()
+        ev[2].record()
+        for f in forks:
+            model.seq_close(f)
+        return ev
+
+    for _ in range(args.warmup):
+        step()
+    evs = [step() for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    pre = sum(e[0].elapsed_time(e[1]) for e in evs) / 1e3
+    dec = sum(e[1].elapsed_time(e[2]) for e in evs) / 1e3
+    unique = len(prefix) + int(slen.sum())
+    tflops = flops * args.steps / pre / 1e12
+    value = n * (n_new - 1) * args.steps / dec
+    log(f"prefix: prefill {pre / args.steps * 1e3:.1f} ms/step ({unique * args.steps / pre:.0f} tok/s, "
+        f"{tflops:.0f} TFLOP/s), decode {dec / args.steps * 1e3:.1f} ms/step ({value:.0f} tok/s)")
+    model.close()
+    return {"metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": round((pre + dec) / args.steps * 1e3, 2), "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+            "data": "synthetic: seeded token ids, random N(0,0.02) bf16 weights",
+            "config": {"workload": "Llama-3-8B-shaped decoder, 64 requests sharing a 1024-token prefix (prefilled "
+                                   "once, forked by page reference) plus suffixes uniform in [512,2048], chunked "
+                                   "prefill 512, 32 greedy tokens each",
+                       "requests": n, "unique_prefill_tokens": unique, "decode_steps": n_new - 1,
+                       "ready_batch": n},
+            "prefill_tokens_per_s": round(unique * args.steps / pre, 1),
+            "roofline": {"bound": "mfma", "achieved": round(tflops, 1), "peak": BF16_PEAK_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(tflops / BF16_PEAK_TFLOPS, 4), "traffic": None,
+                         "kernel": "whole prefill (linear layers + causal attention + LM head rows)"},
+            "decode_hbm_frac": round(sum(decode_step_bytes(shape, slen + 1024 + k) for k in range(n_new - 1))
+                                     * args.steps / dec / 1e9 / HBM_PEAK_GBS, 4)}
+
+
+def bench_70b(args, torch, metro, synth):
+    """Llama-3-70B shape unsharded on one GPU: 128 agents with contexts uniform
+    in [1024, 3072] prefilled before timing; each timed step forks the 128
+    sequences (prefix sharing, outside the timed region) and decodes 31 tokens
+    at B = 128."""
+    shape = synth.LLAMA3_70B
+    V = shape["vocab"]
+    ctx, n_new = synth.llama70b_agent_batch(args.seed)
+    n = len(ctx)
+    lens = np.array([len(c) for c in ctx], np.int64)
+    page_bytes = 16 * kv_token_bytes(shape)
+    runs = args.steps + args.warmup
+    pages = int(np.sum((lens + 15) // 16)) + runs * n * (2 + (n_new + 15) // 16) + 64
+    log(f"70b: {n} agents, {lens.sum()} context tokens; KV pool {pages * page_bytes / 1e9:.1f} GB")
+    t0 = time.time()
+    model = metro.Model(shape, max_batch=n, max_tokens=16 * 512, max_context=int(lens.max()) + n_new + 16,
+                        max_seqs=2 * n + 8, kv_pool_bytes=pages * page_bytes, seed=args.seed)
+    info = model.info()
+    log(f"70b: model ready in {time.time() - t0:.1f}s, weights {info.weight_bytes / 1e9:.1f} GB")
+    seqs = [model.seq_open() for _ in range(n)]
+    first = torch.zeros(n, dtype=torch.int32, device="cuda")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    prefill_all(model, seqs, ctx, 512, 16, torch, first)
+    e1.record()
+    torch.cuda.synchronize()
+    pre_s = e0.elapsed_time(e1) / 1e3
+    log(f"70b: contexts prefilled in {pre_s:.1f}s GPU time ({lens.sum() / pre_s:.0f} tok/s)")
+    logits = torch.empty(n, V, dtype=torch.float32, device="cuda")
+
+    def step():
+        forks = [model.seq_fork(s, int(L)) for s, L in zip(seqs, lens)]
+        tok, tok2 = first.clone(), torch.empty_like(first)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record()
+        for _ in range(n_new - 1):
+            model.decode_step(forks, tok, logits, tok2)
+            tok, tok2 = tok2, tok
+        ev[1].record()
+        torch.cuda.synchronize()
+        for f in forks:
+            model.seq_close(f)
+        return ev[0].elapsed_time(ev[1]) / 1e3
+
+    for _ in range(args.warmup):
+        step()
+    dec = sum(step() for _ in range(args.steps))
+    value = n * (n_new - 1) * args.steps / dec
+    nbytes = sum(decode_step_bytes(shape, lens + k) for k in range(n_new - 1)) * args.steps
+    roof = hbm_roofline(nbytes, dec, "whole decode step (weights + KV + logits)")
+    log(f"70b: decode {dec / args.steps * 1e3:.1f} ms per 31 steps ({value:.0f} tok/s), "
+        f"{roof['frac'] * 100:.1f}% of HBM peak")
+    model.close()
+    flops = prefill_flops(shape, [np.arange(L) for L in lens], n)
+    return {"metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": round(dec / args.steps * 1e3, 2), "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+            "data": "synthetic: seeded token ids, random N(0,0.02) bf16 weights",
+            "config": {"workload": "Llama-3-70B-shaped decoder unsharded on one GPU, 128 agents with contexts "
+                                   "uniform in [1024,3072] (prefilled before timing), 32 greedy tokens each",
+                       "agents": n, "context_tokens": int(lens.sum()), "decode_steps": n_new - 1,
+                       "ready_batch": n},
+            "roofline": roof,
+            "prefill_tokens_per_s": round(lens.sum() / pre_s, 1),
+            "prefill_mfma_frac": round(flops / pre_s / 1e12 / BF16_PEAK_TFLOPS, 4)}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -175,6 +452,9 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--agents", type=int, default=25)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload", choices=["agents", "trace", "prefix", "70b"], default="agents",
+                    help="agents (default): 25 agents, the benchmarked workload; trace: decode driven by the "
+                         "seeded agent trace; prefix: prefix-heavy requests; 70b: Llama-3-70B shape at B=128")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device copy three times (counter calibration) and exit")
     args = ap.parse_args()
@@ -193,6 +473,10 @@ def main():
     torch.cuda.set_device(0)
     if args.calibrate_copy:
         calibrate_copy(torch)
+        return
+    if args.workload != "agents":
+        fn = {"trace": bench_trace, "prefix": bench_prefix, "70b": bench_70b}[args.workload]
+        print(json.dumps(fn(args, torch, metro, synth)), flush=True)
         return
     shape = synth.LLAMA3_8B
     prompts, n_new = synth.llama8b_agent_batch(args.seed, n_agents=args.agents)

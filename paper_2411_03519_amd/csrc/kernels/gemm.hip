@@ -65,10 +65,14 @@ template <int MT, int NT, int EPI, int PF, int NW>
 __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const uint16_t* __restrict__ X, int ldx,
                                                               const uint16_t* __restrict__ W, int Kp, int M, int N,
                                                               float* __restrict__ outf, uint16_t* __restrict__ outb,
-                                                              int ldo, float* __restrict__ part) {
+                                                              int ldo, float* __restrict__ part, int mchunks) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r = lane & 15, g = lane >> 4;
-  const int n0 = blockIdx.x * 16 * NT;
+  // blockIdx.x = (W row block) * mchunks + (chunk of 16*MT activation rows):
+  // the chunks of one W block are dispatched together, so all but the first
+  // read that block from the caches
+  const int mbase = (blockIdx.x % mchunks) * 16 * MT;
+  const int n0 = (blockIdx.x / mchunks) * 16 * NT;
   const int KS = gridDim.y, slice = blockIdx.y;
   const int kslice = Kp / KS, k0 = slice * kslice;
 
@@ -87,7 +91,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const uint16_t* __
   bool xok[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
-    const int m = mt * 16 + r;
+    const int m = mbase + mt * 16 + r;
     xok[mt] = m < M;
     xrow[mt] = X + static_cast<size_t>(xok[mt] ? m : 0) * ldx + k0 + 8 * g;
   }
@@ -150,7 +154,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const uint16_t* __
         gs += red[w][2 * pr * MT + mt][lane];
         us += red[w][(2 * pr + 1) * MT + mt][lane];
       }
-      const int m = mt * 16 + m_lane;
+      const int m = mbase + mt * 16 + m_lane;
       if (m < M) store_swiglu(gs, us, m, (n0 / 32 + pr) * 16 + n_lane, outb, ldo);
     }
   } else {
@@ -159,7 +163,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const uint16_t* __
 #pragma unroll
       for (int w = 1; w < NW; ++w) sum += red[w][t][lane];
       const int nt = t / MT, mt = t % MT;
-      const int m = mt * 16 + m_lane;
+      const int m = mbase + mt * 16 + m_lane;
       if (m >= M) continue;
       if (KS > 1)
         store_tile<kEpiStoreF32>(sum, m, n0 + nt * 16 + n_lane, part + static_cast<size_t>(slice) * M * N, N);
@@ -351,10 +355,21 @@ constexpr int kSkinnyPF = METRO_SKINNY_PF;  // k blocks in flight per wave
 constexpr int kSkinnyWaves = 8;             // waves per workgroup (k split inside it)
 constexpr int kTiledWN = 4, kTiledWM = 2;   // wave grid of the tiled GEMM (8 waves, 2 per SIMD)
 
+// Which kernel serves an M x N product (crossovers measured on MI355X with
+// K = 4096 .. 14336): the weight-streaming kernel, in 64-row chunks above 64
+// rows, keeps more workgroups busy than 256 x 256 tiles until the tiles are
+// both numerous (large N) and full enough (large M) to win.
+bool gemm_uses_skinny(int M, int N) {
+  if (M <= 64) return true;
+  if (N >= 65536) return false;  // LM head
+  if (N >= 16384) return M <= 128;
+  return M <= kSkinnyMaxRows;
+}
+
 int gemm_splits(int M, int N, int Kp, int epilogue) {
-  if (M > 64 || epilogue == kEpiSwiGLU) return 1;
+  if (!gemm_uses_skinny(M, N) || M > kSplitMaxRows || epilogue == kEpiSwiGLU) return 1;
   const int nt = N % 64 == 0 ? 4 : 2;
-  const int wgs = N / (16 * nt);
+  const int wgs = N / (16 * nt) * (M > 64 ? (M + 63) / 64 : 1);
   int ks = 1;
   // enough workgroups to cover the 256 CUs; each slice a multiple of 128
   while (wgs * ks < 256 && ks < 8 && (Kp / (2 * ks)) % 128 == 0) ks *= 2;
@@ -364,8 +379,9 @@ int gemm_splits(int M, int N, int Kp, int epilogue) {
 template <int MT, int NT, int EPI>
 static void launch_skinny(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, float* outf,
                           uint16_t* outb, int ldo, float* part, int ks, hipStream_t s) {
-  launch_kernel((gemm_skinny_kernel<MT, NT, EPI, kSkinnyPF, kSkinnyWaves>), dim3(N / (16 * NT), ks),
-                     dim3(kSkinnyWaves * 64), 0, s, X, ldx, W, Kp, M, N, outf, outb, ldo, part);
+  const int mchunks = (M + 16 * MT - 1) / (16 * MT);
+  launch_kernel((gemm_skinny_kernel<MT, NT, EPI, kSkinnyPF, kSkinnyWaves>), dim3(N / (16 * NT) * mchunks, ks),
+                dim3(kSkinnyWaves * 64), 0, s, X, ldx, W, Kp, M, N, outf, outb, ldo, part, mchunks);
 }
 
 template <int NT, int EPI>
@@ -382,7 +398,7 @@ static void launch_skinny_m(const uint16_t* X, int ldx, const uint16_t* W, int K
 template <int EPI>
 static hipError_t launch_epi(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, float* outf,
                              uint16_t* outb, int ldo, float* part, int ks, hipStream_t s) {
-  if (M <= 64) {
+  if (gemm_uses_skinny(M, N)) {
     if (N % 64 == 0)
       launch_skinny_m<4, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, ks, s);
     else

@@ -85,9 +85,15 @@ enum GemmEpilogue {
 // order, packed_offset; Kp % 128 == 0, N % 32 == 0), fp32 accumulation, then
 // the epilogue.
 // ldo is the row stride of the output in elements.  With a workspace `part`
-// ([8][M][N] fp32) a decode-sized GEMM (M <= 64, fp32 epilogue) may split K
+// ([8][M][N] fp32) a decode-sized GEMM (M <= kSplitMaxRows, fp32 epilogue) may split K
 // over workgroups: it then writes *n_parts > 0 slices part[s][m][n] instead of
 // applying the epilogue, and the consumer sums them in slice order.
+// Small batches run the weight-streaming decode GEMM (in chunks of 64 rows
+// above 64, at most kSkinnyMaxRows), large ones the tiled GEMM
+// (gemm_uses_skinny); k-split slices are only written for M <= kSplitMaxRows.
+constexpr int kSkinnyMaxRows = 1024;
+constexpr int kSplitMaxRows = 256;
+bool gemm_uses_skinny(int M, int N);
 hipError_t launch_gemm(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, int epilogue,
                        float* out_f32, uint16_t* out_bf16, int ldo, float* part, int* n_parts, hipStream_t s);
 int gemm_splits(int M, int N, int Kp, int epilogue);

@@ -73,8 +73,11 @@ def test_pack_weight_rejects_bad_shapes(metro):
             metro.op_pack_weight(W, ld, N, K, Kp, out)
 
 
+# (M, K, N): decode kernel at M <= 64 and in 64-row chunks above (small N up
+# to 1024 rows), tiled kernel for large M or large N (gemm_uses_skinny)
 GEMM_CASES = [(1, 256, 64), (7, 640, 96), (16, 256, 32), (25, 4096, 512), (33, 768, 160), (64, 384, 1376),
-              (65, 256, 160), (200, 1152, 416), (129, 128, 96), (300, 4096, 256)]
+              (65, 256, 160), (200, 1152, 416), (129, 128, 96), (300, 4096, 256), (1100, 384, 160),
+              (200, 256, 16384), (70, 128, 65536)]
 
 
 @pytest.mark.parametrize("M,K,N", GEMM_CASES + [(25, 14336, 512), (3, 1024, 4096)])
@@ -102,7 +105,8 @@ def test_gemm_f32_epilogues(metro, M, K, N, epi, split):
     np.testing.assert_array_equal(got[:, N:], init[:, N:])  # padding columns untouched
 
 
-@pytest.mark.parametrize("M,K,F", [(3, 256, 688), (25, 256, 48), (64, 512, 112), (96, 256, 688), (130, 384, 80)])
+@pytest.mark.parametrize("M,K,F", [(3, 256, 688), (25, 256, 48), (64, 512, 112), (96, 256, 688), (130, 384, 80),
+                                   (150, 128, 8192)])
 def test_gemm_swiglu_epilogue(metro, M, K, F):
     print(f"swiglu M={M} K={K} F={F}", flush=True)
     rng = np.random.default_rng(M + K + F)
