@@ -201,42 +201,66 @@ __global__ __launch_bounds__(256) void reduce_parts_kernel(const float* __restri
 }
 
 // ---------------------------------------------------------------------------
-// Tiled GEMM (M > 64: prefill chunks, large decode batches), bound by the
-// matrix cores.  Block tile 256 (n, rows of W) x 256 (m, activation rows) x 64
-// (k); WN x WM waves (4 x 2: two per SIMD), each (256/WN) x (256/WM) = 2 x 4
-// tiles of v_mfma_f32_32x32x16_bf16 (A = W rows, B = activation rows).  Lane l supplies A[l%32][8(l/32) .. +7]
-// and B[8(l/32) .. +7][l%32] and receives D rows 8q + 4(l/32) + i (q = 0..3,
-// i = 0..3) of column l%32: four consecutive output features of one
-// activation row per q.  Operand tiles are staged through LDS, double
-// buffered, with the 16-byte chunk index of each 128-byte row XOR-ed with the
-// row (mod 8) so the 32 rows one MFMA operand read touches fall in distinct
-// banks; the next k tile is fetched into registers while the current one is
-// consumed.
+// Tiled GEMM (prefill chunks, large decode batches), bound by the matrix
+// cores.  Block tile 256 (n, rows of W) x 256 (m, activation rows); 8 waves in
+// 4 x 2 (two per SIMD), each 64 x 128 = 2 x 4 tiles of
+// v_mfma_f32_32x32x16_bf16 (A = W rows, B = activation rows).  Lane l
+// supplies A[l%32][8(l/32) .. +7] and B[8(l/32) .. +7][l%32] and receives D
+// rows 8q + 4(l/32) + i (q = 0..3, i = 0..3) of column l%32: four consecutive
+// output features of one activation row per q.
+//
+// Operands reach LDS by direct loads (global_load_lds_dwordx4: each lane's 16
+// bytes land at LDS base + 16 * lane), through a ring of 4 stages of 32-wide
+// k; the loads of three stages are in flight while one is consumed, with no
+// staging registers.  In LDS both operands are kept as 16 x 32 tiles in lane
+// order (the packed weight layout; activations are gathered into the same
+// form, 64 contiguous bytes of each of 16 rows per wave load), so every MFMA
+// operand read by 16 lanes is 256 contiguous bytes, free of bank conflicts.
+// The loads and their waits are issued as inline assembly: the compiler
+// would otherwise guard every LDS read with a wait for all of them.  The
+// stage consumed in step kt is refilled (with stage kt + 4) in step kt + 1,
+// after the barrier that every wave passes only once done reading it.
 // ---------------------------------------------------------------------------
-constexpr int TBM = 256, TBN = 256, TBK = 64;
+constexpr int TBM = 256, TBN = 256, TBK = 32;
 
 __device__ __forceinline__ f32x16 mfma32(uint4 a, uint4 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
 }
 
-template <int EPI, int WN, int WM>
-__global__ __launch_bounds__(WN * WM * 64) void gemm_tiled_kernel(const uint16_t* __restrict__ X, int ldx,
-                                                                  const uint16_t* __restrict__ W, int Kp, int M, int N,
-                                                                  float* __restrict__ outf,
-                                                                  uint16_t* __restrict__ outb, int ldo) {
-  constexpr int NTH = WN * WM * 64;
-  constexpr int TN = TBN / WN / 32, TM = TBM / WM / 32;  // 32x32 tiles per wave
-  constexpr int CPT = TBN * 8 / NTH;                     // 16-byte chunks per thread per operand
-  __shared__ uint4 ws[2][TBN * 8];  // [row][8 chunks of 16 B], chunk swizzled
-  __shared__ uint4 xs[2][TBM * 8];
-  const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
-  const int wn = wave / WM, wm = wave % WM;  // the wave's (TN*32) x (TM*32) tile
+template <int N_>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N_) : "memory");
+}
+
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// 16 bytes per lane from gptr into LDS bytes lds_base + 16 * lane; lds_base is
+// wave-uniform.  One wait state separates the M0 write from the load that reads it.
+__device__ __forceinline__ void lds_load16(const void* gptr, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(lds_base)
+               : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void*)p));
+}
+
+template <int EPI>
+__global__ __launch_bounds__(512) void gemm_tiled_kernel(const uint16_t* __restrict__ X, int ldx,
+                                                         const uint16_t* __restrict__ W, int Kp, int M, int N,
+                                                         float* __restrict__ outf, uint16_t* __restrict__ outb,
+                                                         int ldo) {
+  constexpr int WM = 2, TN = 2, TM = 4;
+  // one array per stage and operand: 16 tiles of 16 x 32 (1 KiB each)
+  __shared__ uint4 w0[1024], w1[1024], w2[1024], w3[1024];
+  __shared__ uint4 x0[1024], x1[1024], x2[1024], x3[1024];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int wn = wave / WM, wm = wave % WM;  // the wave's 64 x 128 tile
   const int lr = lane & 31, lh = lane >> 5;
 
   // Grouped tile order: blocks in launch order sweep groups of kGroupM m-tiles,
   // m fastest within a group, so the ~256 blocks in flight cover a compact
-  // 16 x 16 patch of tiles and share their W and X tiles through the caches.
+  // patch of tiles and share their W and X tiles through the caches.
   constexpr int kGroupM = 16;
   const int mt = (M + TBM - 1) / TBM, nt = (N + TBN - 1) / TBN;
   const int b = blockIdx.x;
@@ -246,34 +270,25 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm_tiled_kernel(const uint16_t
   const int in = b % (kGroupM * nt);
   const int n0 = (in / gm) * TBN, m0 = (first_m + in % gm) * TBM;
 
-  // global -> registers -> LDS
-  uint4 wr[CPT], xr[CPT];
-  // W: chunk c is chunk q = c % 64 of packed tile t = c / 64, i.e. of row tile
-  // t / 2 and k tile t % 2 of this block: W row 16(t/2) + q%16, chunk
-  // 4(t%2) + q/16 of the 64-wide k tile.  X: chunk c is row c / 8, chunk c % 8.
-  auto fetch = [&](int k) {
+  // Wave w loads tiles 2w, 2w+1 of each operand of every stage.  Rows past N
+  // or M re-read the last valid row: finite values whose products only reach
+  // outputs that are not stored.
+  const uint16_t* wsrc[2];
+  const uint16_t* xsrc[2];
 #pragma unroll
-    for (int j = 0; j < CPT; ++j) {
-      const int c = tid + NTH * j;
-      const int t = c >> 6, q = c & 63;
-      const int n = n0 + (t >> 1) * 16;
-      wr[j] = n < N ? *reinterpret_cast<const uint4*>(
-                          W + (static_cast<size_t>(n >> 4) * (Kp >> 5) + (k >> 5) + (t & 1)) * 512 + q * 8)
-                    : make_uint4(0, 0, 0, 0);
-      const int m = m0 + (c >> 3);
-      xr[j] = m < M ? *reinterpret_cast<const uint4*>(X + static_cast<size_t>(m) * ldx + k + 8 * (c & 7))
-                    : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto stash = [&](int buf) {
+  for (int j = 0; j < 2; ++j) {
+    const int rt = min(n0 / 16 + 2 * wave + j, N / 16 - 1);
+    wsrc[j] = W + static_cast<size_t>(rt) * (Kp / 32) * 512 + lane * 8;
+    const int row = min(m0 + 16 * (2 * wave + j) + (lane & 15), M - 1);
+    xsrc[j] = X + static_cast<size_t>(row) * ldx + 8 * (lane >> 4);
+  }
+  const uint32_t wave_off = __builtin_amdgcn_readfirstlane(wave) * 2 * 1024;
+  auto issue = [&](const uint4* ws, const uint4* xs, int kt) __attribute__((always_inline)) {
+    const uint32_t wb = lds_address(ws) + wave_off, xb = lds_address(xs) + wave_off;
 #pragma unroll
-    for (int j = 0; j < CPT; ++j) {
-      const int c = tid + NTH * j;
-      const int t = c >> 6, q = c & 63;
-      const int wrow = (t >> 1) * 16 + (q & 15), wch = (t & 1) * 4 + (q >> 4);
-      ws[buf][wrow * 8 + (wch ^ (wrow & 7))] = wr[j];
-      const int xrow = c >> 3, xch = c & 7;
-      xs[buf][xrow * 8 + (xch ^ (xrow & 7))] = xr[j];
+    for (int j = 0; j < 2; ++j) {
+      lds_load16(wsrc[j] + kt * 512, wb + j * 1024);
+      lds_load16(xsrc[j] + kt * TBK, xb + j * 1024);
     }
   };
 
@@ -285,34 +300,49 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm_tiled_kernel(const uint16_t
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  const int nk = Kp / TBK;
-  fetch(0);
-  stash(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) fetch((kt + 1) * TBK);
+  auto compute = [&](const uint4* ws, const uint4* xs) __attribute__((always_inline)) {
 #pragma unroll
     for (int ks = 0; ks < TBK / 16; ++ks) {
-      const int ch = 2 * ks + lh;
+      const int q = 16 * (2 * ks + lh);  // chunk of the lane's 8 k values within the tile
       uint4 af[TN], bf[TM];
 #pragma unroll
       for (int i = 0; i < TN; ++i) {
         const int row = wn * TN * 32 + i * 32 + lr;
-        af[i] = ws[buf][row * 8 + (ch ^ (row & 7))];
+        af[i] = ws[(row >> 4) * 64 + (row & 15) + q];
       }
 #pragma unroll
       for (int j = 0; j < TM; ++j) {
         const int row = wm * TM * 32 + j * 32 + lr;
-        bf[j] = xs[buf][row * 8 + (ch ^ (row & 7))];
+        bf[j] = xs[(row >> 4) * 64 + (row & 15) + q];
       }
 #pragma unroll
       for (int i = 0; i < TN; ++i)
 #pragma unroll
         for (int j = 0; j < TM; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
     }
-    if (kt + 1 < nk) stash(buf ^ 1);
-    __syncthreads();
+  };
+
+  const int nk = Kp / TBK;  // a multiple of 4 (Kp % 128 == 0)
+  // step kt: wait for stage kt (each wave has 4 loads per stage; those of
+  // kt+1 and kt+2 may stay in flight), barrier, refill the stage consumed in
+  // step kt-1 with kt+3, then compute stage kt
+  auto step = [&](int kt, const uint4* ws, const uint4* xs, const uint4* wr, const uint4* xr)
+                  __attribute__((always_inline)) {
+    if (kt + 2 < nk) wait_vmcnt<8>();
+    else if (kt + 1 < nk) wait_vmcnt<4>();
+    else wait_vmcnt<0>();
+    lds_barrier();
+    if (kt + 3 < nk) issue(wr, xr, kt + 3);
+    compute(ws, xs);
+  };
+  issue(w0, x0, 0);
+  issue(w1, x1, 1);
+  issue(w2, x2, 2);
+  for (int kt = 0; kt < nk; kt += 4) {
+    step(kt, w0, x0, w3, x3);
+    step(kt + 1, w1, x1, w0, x0);
+    step(kt + 2, w2, x2, w1, x1);
+    step(kt + 3, w3, x3, w2, x2);
   }
 
   // fully unrolled (acc must stay in registers); the scheduling barriers keep
@@ -353,7 +383,6 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm_tiled_kernel(const uint16_t
 #endif
 constexpr int kSkinnyPF = METRO_SKINNY_PF;  // k blocks in flight per wave
 constexpr int kSkinnyWaves = 8;             // waves per workgroup (k split inside it)
-constexpr int kTiledWN = 4, kTiledWM = 2;   // wave grid of the tiled GEMM (8 waves, 2 per SIMD)
 
 // Which kernel serves an M x N product (crossovers measured on MI355X with
 // K = 4096 .. 14336): the weight-streaming kernel, in 64-row chunks above 64
@@ -405,8 +434,7 @@ static hipError_t launch_epi(const uint16_t* X, int ldx, const uint16_t* W, int 
       launch_skinny_m<2, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, ks, s);
   } else {
     const int tiles = ((N + TBN - 1) / TBN) * ((M + TBM - 1) / TBM);
-    launch_kernel((gemm_tiled_kernel<EPI, kTiledWN, kTiledWM>), dim3(tiles), dim3(kTiledWN * kTiledWM * 64), 0, s,
-                       X, ldx, W, Kp, M, N, outf, outb, ldo);
+    launch_kernel((gemm_tiled_kernel<EPI>), dim3(tiles), dim3(512), 0, s, X, ldx, W, Kp, M, N, outf, outb, ldo);
   }
   return hipGetLastError();
 }
