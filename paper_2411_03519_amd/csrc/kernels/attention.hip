@@ -29,8 +29,9 @@
 // count depends on the row's own context length only, never on the batch.
 //
 // Prefill (flash attention): one workgroup = (query block, kv head); the K and
-// V pages of the block's visible context go through LDS in pairs (double
-// buffered) and are shared by the four waves; causal masking per element.
+// V pages of the block's visible context go through LDS in pairs, by direct
+// loads into a 4-stage ring (three pairs in flight while one is consumed), and
+// are shared by the four waves; causal masking per element.
 #include "common.h"
 #include "kernels.h"
 
@@ -52,9 +53,8 @@ __device__ __forceinline__ f32x4 mfma_k16(uint2 a, uint2 b, f32x4 c) {
 
 // p -> (hi, lo) bf16 pairs packed two per word
 __device__ __forceinline__ void split_bf16(float p0, float p1, uint32_t& hi, uint32_t& lo) {
-  const uint16_t h0 = f32_to_bf16(p0), h1 = f32_to_bf16(p1);
-  hi = static_cast<uint32_t>(h0) | (static_cast<uint32_t>(h1) << 16);
-  lo = pack_bf16x2(p0 - bf16_to_f32(h0), p1 - bf16_to_f32(h1));
+  hi = pack_bf16x2(p0, p1);
+  lo = pack_bf16x2(p0 - lo_bf16(hi), p1 - hi_bf16(hi));
 }
 
 // ===========================================================================
@@ -236,21 +236,23 @@ template <int HD, int G>
 __global__ __launch_bounds__(256) void attn_prefill_kernel(PrefillAttnArgs a) {
   constexpr int KQ = HD / 32;
   constexpr int NT = HD / 16;
-  constexpr int NQ = 4;             // query tiles per wave
-  constexpr int TPT = 16 / G;       // tokens per tile
-  constexpr int TPW = NQ * TPT;     // tokens per wave
-  constexpr int TPB = 4 * TPW;      // tokens per workgroup
-  constexpr int PAGE = kPage * HD;  // bf16 elements of one K (or V^T) page
+  constexpr int NQ = 4;               // query tiles per wave
+  constexpr int TPT = 16 / G;         // tokens per tile
+  constexpr int TPW = NQ * TPT;       // tokens per wave
+  constexpr int PCH = kPage * HD / 8;  // 16-byte chunks of one K (or V^T) page tile
+  constexpr int LPW = PCH / 64;       // direct loads per wave per stage
+  constexpr int NS = 4;               // stages of the LDS ring
+  // stage = one page pair: [K page 0, K page 1, V^T page 0, V^T page 1]
+  __shared__ uint4 ring[NS][4][PCH];
 
-  __shared__ uint16_t ks[2][2][PAGE];  // [buffer][page of the pair]
-  __shared__ uint16_t vs[2][2][PAGE];
-
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 15, grp = lane >> 4;
   const int bi = blockIdx.x / a.nkv, h = blockIdx.x % a.nkv;
   const int item = a.blocks[3 * bi], row0 = a.blocks[3 * bi + 1], nrows = a.blocks[3 * bi + 2];
   const int32_t* bt = a.bt + a.item_bt[item];
   const int last_pos = a.pos[row0 + nrows - 1];
+  const int first_pos = a.pos[row0];
   const int n_pages = last_pos / kPage + 1;
   const int n_pairs = (n_pages + 1) / 2;
   const float qscale = a.scale * kLog2e;
@@ -281,83 +283,92 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(PrefillAttnArgs a) {
     for (int t = 0; t < NT; ++t) o[n][t] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  // cooperative staging of one page pair: 2 K pages + 2 V^T pages, 16 B chunks
-  constexpr int CH = PAGE / 8;  // 16-byte chunks per page
-  constexpr int PER = (4 * CH) / 256;
-  uint4 stage[PER];
-  auto fetch = [&](int pair) {
+  // Wave w brings tile w of every stage: the K (w < 2) or V^T (w >= 2) tile
+  // of page 2*pair + (w & 1).  The absent second page of an odd count is
+  // stood in for by the last page: finite values, all of its keys masked.
+  const size_t part = kv_offset(0, wave >> 1, a.nkv, h, 0, HD, 0);
+  const size_t pstride = static_cast<size_t>(2) * a.nkv * kPage * HD;
+  auto issue = [&](int pair) __attribute__((always_inline)) {
+    const int pi = min(2 * pair + (wave & 1), n_pages - 1);
+    const uint16_t* src = a.kv + static_cast<size_t>(bt[pi]) * pstride + part + 8 * lane;
+    const uint32_t dst = lds_address(&ring[pair % NS][wave][0]);
 #pragma unroll
-    for (int r = 0; r < PER; ++r) {
-      const int c = tid + 256 * r;
-      const int which = c / CH, off = c % CH;  // which: 0,1 = K pages, 2,3 = V pages
-      const int pi = 2 * pair + (which & 1);
-      if (pi < n_pages) {
-        const int page = bt[pi];
-        const uint16_t* src = a.kv + kv_offset(page, which >> 1, a.nkv, h, 0, HD, 0);
-        stage[r] = *reinterpret_cast<const uint4*>(src + 8 * off);
-      } else {
-        stage[r] = make_uint4(0, 0, 0, 0);
-      }
-    }
-  };
-  auto stash = [&](int buf) {
-#pragma unroll
-    for (int r = 0; r < PER; ++r) {
-      const int c = tid + 256 * r;
-      const int which = c / CH, off = c % CH;
-      uint16_t* dst = (which < 2 ? ks[buf][which] : vs[buf][which - 2]) + 8 * off;
-      *reinterpret_cast<uint4*>(dst) = stage[r];
-    }
+    for (int c = 0; c < LPW; ++c) lds_load16(src + 512 * c, dst + 1024 * c);
   };
 
-  fetch(0);
-  stash(0);
-  __syncthreads();
+  issue(0);
+  if (n_pairs > 1) issue(1);
+  if (n_pairs > 2) issue(2);
   for (int pair = 0; pair < n_pairs; ++pair) {
-    const int buf = pair & 1;
-    if (pair + 1 < n_pairs) fetch(pair + 1);
+    // this pair's tiles have landed once at most the later pairs' loads are
+    // outstanding; then every wave's part is in LDS after the barrier, and the
+    // stage read in the previous iteration is free for pair + 3
+    const int later = min(n_pairs - 1 - pair, 2);
+    if (later == 2) wait_vmcnt<2 * LPW>();
+    else if (later == 1) wait_vmcnt<LPW>();
+    else wait_vmcnt<0>();
+    lds_barrier();
+    if (pair + 3 < n_pairs) issue(pair + 3);
+    const uint4(*st)[PCH] = ring[pair % NS];
 
-    // K operand of both pages (A of S^T): key row col, dims 32i + 8grp .. +7
-    uint4 kf[2][KQ];
+    // K operand of both pages (A of S^T): key row col, dims 32i + 8grp .. +7;
+    // V^T operand over the pair: dims of tile t, keys 4grp .. 4grp+3 of each page
+    uint4 kf[2][KQ], vf[NT];
 #pragma unroll
     for (int pg = 0; pg < 2; ++pg)
 #pragma unroll
-      for (int i = 0; i < KQ; ++i)
-        kf[pg][i] = *reinterpret_cast<const uint4*>(&ks[buf][pg][512 * i + 8 * lane]);
+      for (int i = 0; i < KQ; ++i) kf[pg][i] = st[pg][64 * i + lane];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const int vo = 128 * (t >> 1) + 2 * lane + (t & 1);  // in 8-byte units
+      const uint2 va = reinterpret_cast<const uint2*>(st[2])[vo];
+      const uint2 vb = reinterpret_cast<const uint2*>(st[3])[vo];
+      vf[t] = make_uint4(va.x, va.y, vb.x, vb.y);
+    }
 
+    // keys of this pair visible to every query of the block: no mask needed
+    const bool all_visible = (2 * pair + 2) * kPage - 1 <= first_pos;
 #pragma unroll
     for (int n = 0; n < NQ; ++n) {
-      float sv[2][4];
+      float sv[2][4];  // raw scores q.k
 #pragma unroll
       for (int pg = 0; pg < 2; ++pg) {
-        f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+        f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int i = 0; i < KQ; ++i) s = mfma_k32(kf[pg][i], qf[n][i], s);
+        for (int i = 0; i < KQ; ++i) sc = mfma_k32(kf[pg][i], qf[n][i], sc);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int kpos = (2 * pair + pg) * kPage + 4 * grp + r;
-          sv[pg][r] = kpos <= qpos[n] ? s[r] * qscale : -INFINITY;
+          sv[pg][r] = all_visible || kpos <= qpos[n] ? sc[r] : -INFINITY;
         }
       }
       float mp = fmaxf(fmaxf(fmaxf(sv[0][0], sv[0][1]), fmaxf(sv[0][2], sv[0][3])),
                        fmaxf(fmaxf(sv[1][0], sv[1][1]), fmaxf(sv[1][2], sv[1][3])));
       mp = fmaxf(mp, __shfl_xor(mp, 16, kWave));
-      mp = fmaxf(mp, __shfl_xor(mp, 32, kWave));
-      const float mn = fmaxf(m[n], mp);
-      const float corr = exp2f(m[n] - mn);
-      m[n] = mn;
+      mp = fmaxf(mp, __shfl_xor(mp, 32, kWave)) * qscale;  // in log2 units
+      // The reference max m only moves when some column's max exceeds it by
+      // more than 8 (a factor 2^8): o and l carry the same scale, so their
+      // quotient is unchanged, and p = 2^(s - m) stays below 2^8.
+      if (__any(mp > m[n] + 8.f)) {
+        const float mn = fmaxf(m[n], mp);
+        const float corr = exp2f(m[n] - mn);
+        m[n] = mn;
+        l[n] *= corr;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) o[n][t] *= corr;
+      }
       float pv[2][4];
       float ps = 0.f;
 #pragma unroll
       for (int pg = 0; pg < 2; ++pg)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          pv[pg][r] = exp2f(sv[pg][r] - mn);
+          pv[pg][r] = exp2f(fmaf(sv[pg][r], qscale, -m[n]));
           ps += pv[pg][r];
         }
-      l[n] = l[n] * corr + ps;
+      l[n] += ps;
       // P^T operand over the page pair: k-slot 8grp+j is key 4grp+j of page
-      // j/4; the V^T operand below uses the same order.
+      // j/4, the order of the V^T operand
       uint4 hi, lo;
       split_bf16(pv[0][0], pv[0][1], hi.x, lo.x);
       split_bf16(pv[0][2], pv[0][3], hi.y, lo.y);
@@ -365,17 +376,10 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(PrefillAttnArgs a) {
       split_bf16(pv[1][2], pv[1][3], hi.w, lo.w);
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        const int vo = 512 * (t >> 1) + 8 * lane + (t & 1) * 4;
-        const uint2 va = *reinterpret_cast<const uint2*>(&vs[buf][0][vo]);
-        const uint2 vb = *reinterpret_cast<const uint2*>(&vs[buf][1][vo]);
-        const uint4 vf = make_uint4(va.x, va.y, vb.x, vb.y);
-        o[n][t] *= corr;
-        o[n][t] = mfma_k32(vf, hi, o[n][t]);
-        o[n][t] = mfma_k32(vf, lo, o[n][t]);
+        o[n][t] = mfma_k32(vf[t], hi, o[n][t]);
+        o[n][t] = mfma_k32(vf[t], lo, o[n][t]);
       }
     }
-    if (pair + 1 < n_pairs) stash(buf ^ 1);
-    __syncthreads();
   }
 
 #pragma unroll

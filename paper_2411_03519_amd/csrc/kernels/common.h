@@ -15,17 +15,16 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
 
-// float32 -> bfloat16 bits, round to nearest even; NaN stays a quiet NaN.
-__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return static_cast<uint16_t>(u >> 16);
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// float32 -> bfloat16 bits, round to nearest even (subnormals kept); a NaN
+// stays a NaN.  One v_cvt_pk_bf16_f32 for two values.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2{lo, hi}), bf16x2));
 }
 
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
-}
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) { return static_cast<uint16_t>(pack_bf16x2(f, 0.f)); }
 
 // The two bf16 values of a 32-bit word as floats (exact).
 __device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
@@ -80,6 +79,33 @@ __device__ __forceinline__ int vt_tile_offset(int d, int key) {
 // and a row tile's successive k tiles are contiguous.
 __host__ __device__ __forceinline__ int64_t packed_offset(int64_t n, int64_t k, int64_t Kp) {
   return ((((n >> 4) * (Kp >> 5) + (k >> 5)) * 64 + (n & 15) + 16 * ((k >> 3) & 3)) << 3) + (k & 7);
+}
+
+// --- direct loads into LDS ---------------------------------------------------
+// global_load_lds_dwordx4 writes each lane's 16 bytes at LDS base + 16 * lane
+// (base in M0, wave-uniform) and counts in vmcnt like any vector load.  The
+// loads and their waits are issued as inline assembly so that the compiler,
+// which cannot tell which LDS bytes they write, does not guard every later
+// LDS read with a wait for all of them; code using them waits explicitly
+// (wait_vmcnt) and synchronises the workgroup with lds_barrier.  Waits the
+// compiler inserts for its own loads can only wait longer, never shorter.
+
+template <int N_>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N_) : "memory");
+}
+
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// 16 bytes per lane from gptr into LDS bytes lds_base + 16 * lane; one wait
+// state separates the M0 write from the load that reads it
+__device__ __forceinline__ void lds_load16(const void* gptr, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(lds_base)
+               : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void*)p));
 }
 
 }  // namespace metro

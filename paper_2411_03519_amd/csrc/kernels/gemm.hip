@@ -216,33 +216,13 @@ __global__ __launch_bounds__(256) void reduce_parts_kernel(const float* __restri
 // order (the packed weight layout; activations are gathered into the same
 // form, 64 contiguous bytes of each of 16 rows per wave load), so every MFMA
 // operand read by 16 lanes is 256 contiguous bytes, free of bank conflicts.
-// The loads and their waits are issued as inline assembly: the compiler
-// would otherwise guard every LDS read with a wait for all of them.  The
-// stage consumed in step kt is refilled (with stage kt + 4) in step kt + 1,
-// after the barrier that every wave passes only once done reading it.
+// The stage consumed in step kt is refilled (with stage kt + 4) in step
+// kt + 1, after the barrier that every wave passes only once done reading it.
 // ---------------------------------------------------------------------------
 constexpr int TBM = 256, TBN = 256, TBK = 32;
 
 __device__ __forceinline__ f32x16 mfma32(uint4 a, uint4 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
-}
-
-template <int N_>
-__device__ __forceinline__ void wait_vmcnt() {
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N_) : "memory");
-}
-
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
-
-// 16 bytes per lane from gptr into LDS bytes lds_base + 16 * lane; lds_base is
-// wave-uniform.  One wait state separates the M0 write from the load that reads it.
-__device__ __forceinline__ void lds_load16(const void* gptr, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(lds_base)
-               : "memory", "m0");
-}
-
-__device__ __forceinline__ uint32_t lds_address(const void* p) {
-  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void*)p));
 }
 
 template <int EPI>
