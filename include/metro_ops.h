@@ -44,7 +44,7 @@ metro_status metro_op_pack_weight(const uint16_t* W_rowmajor, int32_t ld, int32_
  *      bf16(silu(gate_j) * up_j), j < N/2
  *      (SwiGLU, Shazeer 2020).
  * workspace: NULL, or device fp32 [8][M][N]; when given, a decode-sized GEMM
- * (M <= 256, epilogue 0 or 1) runs the k-split form the model uses (slices in
+ * (M <= 1024, epilogue 0 or 1) may run the k-split form the model uses (slices in
  * the workspace, then summed in slice order into the output).
  * Errors: E_INVAL for shapes outside these rules or a NULL operand. */
 metro_status metro_op_gemm(const uint16_t* X, int32_t ldx, const uint16_t* W, int32_t Kp, int32_t M, int32_t N,

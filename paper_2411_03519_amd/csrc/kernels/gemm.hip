@@ -219,57 +219,97 @@ __global__ __launch_bounds__(256) void reduce_parts_kernel(const float* __restri
 // The stage consumed in step kt is refilled (with stage kt + 4) in step
 // kt + 1, after the barrier that every wave passes only once done reading it.
 // ---------------------------------------------------------------------------
-constexpr int TBM = 256, TBN = 256, TBK = 32;
+// Tile shapes: WN x WM waves, each TN x TM tiles of 32 x 32, NS stages of
+// 32-wide k in the LDS ring.  Big: 256 x 256 blocks for long prefill chunks.
+// Mid: 128 x 128 blocks and a deeper ring for batches of a few hundred rows,
+// where there are few blocks and the weight stream must keep more in flight.
+template <int WN_, int WM_, int TN_, int TM_, int NS_>
+struct TileShape {
+  static constexpr int WN = WN_, WM = WM_, TN = TN_, TM = TM_, NS = NS_;
+  static constexpr int WAVES = WN * WM, NTH = WAVES * 64;
+  static constexpr int BN = WN * TN * 32, BM = WM * TM * 32;  // block tile
+  static constexpr int WT = BN / 16, XT = BM / 16;            // 16 x 32 tiles per stage
+  static constexpr int LPW = (WT + XT) / WAVES;               // direct loads per wave per stage
+  static_assert((WT + XT) % WAVES == 0 && WT % LPW == 0, "each wave loads tiles of one operand");
+};
+using BigTile = TileShape<4, 2, 2, 4, 4>;
+using MidTile = TileShape<4, 1, 1, 4, 8>;
 
 __device__ __forceinline__ f32x16 mfma32(uint4 a, uint4 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
 }
 
-template <int EPI>
-__global__ __launch_bounds__(512) void gemm_tiled_kernel(const uint16_t* __restrict__ X, int ldx,
-                                                         const uint16_t* __restrict__ W, int Kp, int M, int N,
-                                                         float* __restrict__ outf, uint16_t* __restrict__ outb,
-                                                         int ldo) {
-  constexpr int WM = 2, TN = 2, TM = 4;
-  // one array per stage and operand: 16 tiles of 16 x 32 (1 KiB each)
-  __shared__ uint4 w0[1024], w1[1024], w2[1024], w3[1024];
-  __shared__ uint4 x0[1024], x1[1024], x2[1024], x3[1024];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int wn = wave / WM, wm = wave % WM;  // the wave's 64 x 128 tile
+// wait until at most PER * min(later, MAXC) direct loads of this wave are outstanding
+template <int PER, int MAXC>
+__device__ __forceinline__ void wait_later_stages(int later) {
+  if constexpr (MAXC > 0) {
+    if (later >= MAXC) {
+      wait_vmcnt<PER * MAXC>();
+      return;
+    }
+    wait_later_stages<PER, MAXC - 1>(later);
+  } else {
+    wait_vmcnt<0>();
+  }
+}
+
+template <class S, int EPI>
+__global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __restrict__ X, int ldx,
+                                                            const uint16_t* __restrict__ W, int Kp, int M, int N,
+                                                            float* __restrict__ outf, uint16_t* __restrict__ outb,
+                                                            int ldo, float* __restrict__ part) {
+  constexpr int WM = S::WM, TN = S::TN, TM = S::TM, NS = S::NS, LPW = S::LPW;
+  __shared__ uint4 wring[NS][S::WT * 64];  // per stage: WT tiles of 16 x 32 (1 KiB each)
+  __shared__ uint4 xring[NS][S::XT * 64];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wn = wave / WM, wm = wave % WM;  // the wave's (TN*32) x (TM*32) tile
   const int lr = lane & 31, lh = lane >> 5;
+
+  // k range: slice blockIdx.y of gridDim.y (each a multiple of 128)
+  const int KS = gridDim.y, slice = blockIdx.y;
+  const int kspan = Kp / KS, k0 = slice * kspan;
+  const int nk = kspan / 32;
 
   // Grouped tile order: blocks in launch order sweep groups of kGroupM m-tiles,
   // m fastest within a group, so the ~256 blocks in flight cover a compact
   // patch of tiles and share their W and X tiles through the caches.
   constexpr int kGroupM = 16;
-  const int mt = (M + TBM - 1) / TBM, nt = (N + TBN - 1) / TBN;
+  const int mt = (M + S::BM - 1) / S::BM, nt = (N + S::BN - 1) / S::BN;
   const int b = blockIdx.x;
   const int group = b / (kGroupM * nt);
   const int first_m = group * kGroupM;
   const int gm = min(mt - first_m, kGroupM);
   const int in = b % (kGroupM * nt);
-  const int n0 = (in / gm) * TBN, m0 = (first_m + in % gm) * TBM;
+  const int n0 = (in / gm) * S::BN, m0 = (first_m + in % gm) * S::BM;
 
-  // Wave w loads tiles 2w, 2w+1 of each operand of every stage.  Rows past N
-  // or M re-read the last valid row: finite values whose products only reach
-  // outputs that are not stored.
-  const uint16_t* wsrc[2];
-  const uint16_t* xsrc[2];
+  // Wave w loads tiles w*LPW .. w*LPW + LPW - 1 of the list [W tiles, X
+  // tiles] of every stage.  Rows past N or M re-read the last valid row:
+  // finite values whose products only reach outputs that are not stored.
+  const bool loads_w = wave * LPW < S::WT;
+  const uint16_t* src[LPW];
+  uint32_t dst[LPW];
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int rt = min(n0 / 16 + 2 * wave + j, N / 16 - 1);
-    wsrc[j] = W + static_cast<size_t>(rt) * (Kp / 32) * 512 + lane * 8;
-    const int row = min(m0 + 16 * (2 * wave + j) + (lane & 15), M - 1);
-    xsrc[j] = X + static_cast<size_t>(row) * ldx + 8 * (lane >> 4);
-  }
-  const uint32_t wave_off = __builtin_amdgcn_readfirstlane(wave) * 2 * 1024;
-  auto issue = [&](const uint4* ws, const uint4* xs, int kt) __attribute__((always_inline)) {
-    const uint32_t wb = lds_address(ws) + wave_off, xb = lds_address(xs) + wave_off;
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      lds_load16(wsrc[j] + kt * 512, wb + j * 1024);
-      lds_load16(xsrc[j] + kt * TBK, xb + j * 1024);
+  for (int j = 0; j < LPW; ++j) {
+    const int t = wave * LPW + j;
+    if (loads_w) {
+      const int rt = min(n0 / 16 + t, N / 16 - 1);
+      src[j] = W + (static_cast<size_t>(rt) * (Kp / 32) + k0 / 32) * 512 + lane * 8;
+      dst[j] = lds_address(&wring[0][0]) + t * 1024;
+    } else {
+      const int tx = t - S::WT;
+      const int row = min(m0 + 16 * tx + (lane & 15), M - 1);
+      src[j] = X + static_cast<size_t>(row) * ldx + k0 + 8 * (lane >> 4);
+      dst[j] = lds_address(&xring[0][0]) + tx * 1024;
     }
+  }
+  const int src_step = loads_w ? 512 : 32;  // elements per 32-wide k tile
+  constexpr uint32_t wstage = S::WT * 1024, xstage = S::XT * 1024;
+  const uint32_t dst_step = loads_w ? wstage : xstage;
+  auto issue = [&](int kt) __attribute__((always_inline)) {
+    const uint32_t off = (kt % NS) * dst_step;
+#pragma unroll
+    for (int j = 0; j < LPW; ++j) lds_load16(src[j] + kt * src_step, dst[j] + off);
   };
 
   f32x16 acc[TN][TM];
@@ -280,10 +320,21 @@ __global__ __launch_bounds__(512) void gemm_tiled_kernel(const uint16_t* __restr
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  auto compute = [&](const uint4* ws, const uint4* xs) __attribute__((always_inline)) {
 #pragma unroll
-    for (int ks = 0; ks < TBK / 16; ++ks) {
-      const int q = 16 * (2 * ks + lh);  // chunk of the lane's 8 k values within the tile
+  for (int p = 0; p < NS - 1; ++p)
+    if (p < nk) issue(p);
+  for (int kt = 0; kt < nk; ++kt) {
+    // stage kt has landed once only the later stages' loads are outstanding;
+    // after the barrier every wave's part is in LDS, and the stage read in
+    // step kt-1 is free for stage kt + NS - 1
+    wait_later_stages<LPW, NS - 2>(nk - 1 - kt);
+    lds_barrier();
+    if (kt + NS - 1 < nk) issue(kt + NS - 1);
+    const uint4* ws = wring[kt % NS];
+    const uint4* xs = xring[kt % NS];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const int q = 16 * (2 * ks + lh);  // chunk of the lane's 8 k values within a tile
       uint4 af[TN], bf[TM];
 #pragma unroll
       for (int i = 0; i < TN; ++i) {
@@ -300,33 +351,13 @@ __global__ __launch_bounds__(512) void gemm_tiled_kernel(const uint16_t* __restr
 #pragma unroll
         for (int j = 0; j < TM; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
     }
-  };
-
-  const int nk = Kp / TBK;  // a multiple of 4 (Kp % 128 == 0)
-  // step kt: wait for stage kt (each wave has 4 loads per stage; those of
-  // kt+1 and kt+2 may stay in flight), barrier, refill the stage consumed in
-  // step kt-1 with kt+3, then compute stage kt
-  auto step = [&](int kt, const uint4* ws, const uint4* xs, const uint4* wr, const uint4* xr)
-                  __attribute__((always_inline)) {
-    if (kt + 2 < nk) wait_vmcnt<8>();
-    else if (kt + 1 < nk) wait_vmcnt<4>();
-    else wait_vmcnt<0>();
-    lds_barrier();
-    if (kt + 3 < nk) issue(wr, xr, kt + 3);
-    compute(ws, xs);
-  };
-  issue(w0, x0, 0);
-  issue(w1, x1, 1);
-  issue(w2, x2, 2);
-  for (int kt = 0; kt < nk; kt += 4) {
-    step(kt, w0, x0, w3, x3);
-    step(kt + 1, w1, x1, w0, x0);
-    step(kt + 2, w2, x2, w1, x1);
-    step(kt + 3, w3, x3, w2, x2);
   }
 
   // fully unrolled (acc must stay in registers); the scheduling barriers keep
-  // the read-modify-write epilogue from hoisting all of its loads at once
+  // the read-modify-write epilogue from hoisting all of its loads at once.
+  // With KS > 1 the slice sums go to part[slice][m][n].
+  float* const pout = KS > 1 ? part + static_cast<size_t>(slice) * M * N : outf;
+  const int pld = KS > 1 ? N : ldo;
 #pragma unroll
   for (int j = 0; j < TM; ++j) {
     const int m = m0 + wm * TM * 32 + j * 32 + lr;
@@ -348,7 +379,10 @@ __global__ __launch_bounds__(512) void gemm_tiled_kernel(const uint16_t* __restr
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const f32x4 v{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-          store_tile<EPI>(v, m, nb + 8 * q + 4 * lh, outf, ldo);
+          if (KS > 1)
+            store_tile<kEpiStoreF32>(v, m, nb + 8 * q + 4 * lh, pout, pld);
+          else
+            store_tile<EPI>(v, m, nb + 8 * q + 4 * lh, pout, pld);
           __builtin_amdgcn_sched_barrier(0);
         }
       }
@@ -364,26 +398,51 @@ __global__ __launch_bounds__(512) void gemm_tiled_kernel(const uint16_t* __restr
 constexpr int kSkinnyPF = METRO_SKINNY_PF;  // k blocks in flight per wave
 constexpr int kSkinnyWaves = 8;             // waves per workgroup (k split inside it)
 
-// Which kernel serves an M x N product (crossovers measured on MI355X with
-// K = 4096 .. 14336): the weight-streaming kernel, in 64-row chunks above 64
-// rows, keeps more workgroups busy than 256 x 256 tiles until the tiles are
-// both numerous (large N) and full enough (large M) to win.
-bool gemm_uses_skinny(int M, int N) {
-  if (M <= 64) return true;
-  if (N >= 65536) return false;  // LM head
-  if (N >= 16384) return M <= 128;
-  return M <= kSkinnyMaxRows;
+// Row tiles per wave of the decode kernel: 4 (64 rows) amortises the
+// activation reads best, but for short, narrow products (QKV-sized) 2 tiles
+// and twice the workgroups finish sooner (11.0 vs 12.9 us at N=6144, K=4096).
+static int skinny_tiles(int N, int Kp) {
+  if (N % 64) return 2;
+  return N <= 8192 && Kp <= 4096 ? 2 : 4;
 }
 
-int gemm_splits(int M, int N, int Kp, int epilogue) {
-  if (!gemm_uses_skinny(M, N) || M > kSplitMaxRows || epilogue == kEpiSwiGLU) return 1;
-  const int nt = N % 64 == 0 ? 4 : 2;
-  const int wgs = N / (16 * nt) * (M > 64 ? (M + 63) / 64 : 1);
+// Workgroups split K while fewer than `target` cover the product; slices stay
+// multiples of 128, and the slice sums (ks * M * N fp32) never exceed the
+// weight bytes (N * Kp bf16), i.e. 2 * ks * M <= Kp.
+static int gemm_k_splits(int blocks, int target, int M, int Kp) {
   int ks = 1;
-  // enough workgroups to cover the 256 CUs; each slice a multiple of 128
-  while (wgs * ks < 256 && ks < 8 && (Kp / (2 * ks)) % 128 == 0) ks *= 2;
+  while (blocks * ks < target && ks < 8 && (Kp / (2 * ks)) % 128 == 0 && 2 * (2 * ks) * M <= Kp) ks *= 2;
   return ks;
 }
+
+// Kernel choice, from probes over M = 80 .. 12800 at the Llama-3-8B shapes:
+// the decode kernel up to 64 rows; then 128 x 128 tiles (more blocks, deeper
+// ring) for narrow products and for wide ones up to 192 rows; 256 x 256 tiles
+// for the LM head and for long prefill chunks.
+GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, bool can_split) {
+  GemmPlan p{GemmKind::kBig, 4, 1};
+  const bool split = can_split && epilogue != kEpiSwiGLU && M <= kSplitMaxRows;
+  if (M <= 64) {
+    p.kind = GemmKind::kSkinny;
+    p.nt = skinny_tiles(N, Kp);
+    if (split) p.ks = gemm_k_splits(N / (16 * p.nt), p.nt == 2 ? 512 : 256, M, Kp);
+    return p;
+  }
+  if (N >= 65536)
+    p.kind = GemmKind::kBig;
+  else if (N >= 16384)
+    p.kind = M <= 192 ? GemmKind::kMid : GemmKind::kBig;
+  else
+    p.kind = M <= kMidMaxRows ? GemmKind::kMid : GemmKind::kBig;
+  if (split) {
+    const bool mid = p.kind == GemmKind::kMid;
+    const int bn = mid ? MidTile::BN : BigTile::BN, bm = mid ? MidTile::BM : BigTile::BM;
+    p.ks = gemm_k_splits(((N + bn - 1) / bn) * ((M + bm - 1) / bm), mid ? 512 : 256, M, Kp);
+  }
+  return p;
+}
+
+int gemm_splits(int M, int N, int Kp, int epilogue) { return plan_gemm(M, N, Kp, epilogue, true).ks; }
 
 template <int MT, int NT, int EPI>
 static void launch_skinny(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, float* outf,
@@ -404,17 +463,30 @@ static void launch_skinny_m(const uint16_t* X, int ldx, const uint16_t* W, int K
     launch_skinny<4, NT, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, ks, s);
 }
 
+template <class S, int EPI>
+static void launch_tiled(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, float* outf,
+                         uint16_t* outb, int ldo, float* part, int ks, hipStream_t s) {
+  const int blocks = ((N + S::BN - 1) / S::BN) * ((M + S::BM - 1) / S::BM);
+  launch_kernel((gemm_tiled_kernel<S, EPI>), dim3(blocks, ks), dim3(S::NTH), 0, s, X, ldx, W, Kp, M, N, outf, outb,
+                ldo, part);
+}
+
 template <int EPI>
-static hipError_t launch_epi(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, float* outf,
-                             uint16_t* outb, int ldo, float* part, int ks, hipStream_t s) {
-  if (gemm_uses_skinny(M, N)) {
-    if (N % 64 == 0)
-      launch_skinny_m<4, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, ks, s);
-    else
-      launch_skinny_m<2, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, ks, s);
-  } else {
-    const int tiles = ((N + TBN - 1) / TBN) * ((M + TBM - 1) / TBM);
-    launch_kernel((gemm_tiled_kernel<EPI>), dim3(tiles), dim3(512), 0, s, X, ldx, W, Kp, M, N, outf, outb, ldo);
+static hipError_t launch_epi(const GemmPlan& p, const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N,
+                             float* outf, uint16_t* outb, int ldo, float* part, hipStream_t s) {
+  switch (p.kind) {
+    case GemmKind::kSkinny:
+      if (p.nt == 4)
+        launch_skinny_m<4, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, p.ks, s);
+      else
+        launch_skinny_m<2, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, p.ks, s);
+      break;
+    case GemmKind::kMid:
+      launch_tiled<MidTile, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, p.ks, s);
+      break;
+    case GemmKind::kBig:
+      launch_tiled<BigTile, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, p.ks, s);
+      break;
   }
   return hipGetLastError();
 }
@@ -423,15 +495,15 @@ hipError_t launch_gemm(const uint16_t* X, int ldx, const uint16_t* W, int Kp, in
                        float* out_f32, uint16_t* out_bf16, int ldo, float* part, int* n_parts, hipStream_t s) {
   *n_parts = 0;
   if (M <= 0) return hipSuccess;
-  const int ks = part ? gemm_splits(M, N, Kp, epilogue) : 1;
-  if (ks > 1) *n_parts = ks;
+  const GemmPlan p = plan_gemm(M, N, Kp, epilogue, part != nullptr);
+  if (p.ks > 1) *n_parts = p.ks;
   switch (epilogue) {
     case kEpiStoreF32:
-      return launch_epi<kEpiStoreF32>(X, ldx, W, Kp, M, N, out_f32, out_bf16, ldo, part, ks, s);
+      return launch_epi<kEpiStoreF32>(p, X, ldx, W, Kp, M, N, out_f32, out_bf16, ldo, part, s);
     case kEpiAddF32:
-      return launch_epi<kEpiAddF32>(X, ldx, W, Kp, M, N, out_f32, out_bf16, ldo, part, ks, s);
+      return launch_epi<kEpiAddF32>(p, X, ldx, W, Kp, M, N, out_f32, out_bf16, ldo, part, s);
     case kEpiSwiGLU:
-      return launch_epi<kEpiSwiGLU>(X, ldx, W, Kp, M, N, out_f32, out_bf16, ldo, part, ks, s);
+      return launch_epi<kEpiSwiGLU>(p, X, ldx, W, Kp, M, N, out_f32, out_bf16, ldo, part, s);
     default:
       return hipErrorInvalidValue;
   }

@@ -88,12 +88,18 @@ enum GemmEpilogue {
 // ([8][M][N] fp32) a decode-sized GEMM (M <= kSplitMaxRows, fp32 epilogue) may split K
 // over workgroups: it then writes *n_parts > 0 slices part[s][m][n] instead of
 // applying the epilogue, and the consumer sums them in slice order.
-// Small batches run the weight-streaming decode GEMM (in chunks of 64 rows
-// above 64, at most kSkinnyMaxRows), large ones the tiled GEMM
-// (gemm_uses_skinny); k-split slices are only written for M <= kSplitMaxRows.
-constexpr int kSkinnyMaxRows = 1024;
-constexpr int kSplitMaxRows = 256;
-bool gemm_uses_skinny(int M, int N);
+// Kernel choice: up to 64 rows the weight-streaming decode GEMM; up to
+// kMidMaxRows the tiled GEMM with 128 x 128 blocks, above it 256 x 256 blocks.
+// Both may split K over workgroups (k-slice sums, only for M <= kSplitMaxRows).
+enum class GemmKind { kSkinny, kMid, kBig };
+struct GemmPlan {
+  GemmKind kind;
+  int nt;  // row tiles per wave (decode kernel)
+  int ks;  // k slices
+};
+constexpr int kMidMaxRows = 1000;
+constexpr int kSplitMaxRows = 1024;
+GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, bool can_split);
 hipError_t launch_gemm(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, int epilogue,
                        float* out_f32, uint16_t* out_bf16, int ldo, float* part, int* n_parts, hipStream_t s);
 int gemm_splits(int M, int N, int Kp, int epilogue);

@@ -82,7 +82,7 @@ struct metro_model {
   float* xr = nullptr;
   float* logits_ws = nullptr;
   int32_t* next_ws = nullptr;
-  float* parts = nullptr;    // k-slice sums of decode GEMMs, [8][kSplitMaxRows][max(qkv_n, d)]
+  float* parts = nullptr;    // k-slice sums of decode GEMMs, [8][min(kSplitMaxRows, rows)][max(qkv_n, d)]
   float* attn_part = nullptr;  // decode attention split states
   int32_t* desc_dev = nullptr;
   int64_t desc_cap = 0;  // int32 elements
@@ -407,7 +407,7 @@ metro_status metro_create_model(const metro_config* cfg, uint64_t init_seed, met
   {
     const size_t bytes = Tm * d * 4 + Tm * d * 2 + Tm * m->qkv_n * 4 + 2 * Tm * m->q_dim * 2 + Tm * m->Fp * 2 +
                          int64_t(c.max_batch) * d * 4 + int64_t(c.max_batch) * V * 4 + int64_t(c.max_batch) * 4 +
-                         8LL * metro::kSplitMaxRows * std::max(m->qkv_n, d) * 4 +
+                         8LL * std::min<int64_t>(metro::kSplitMaxRows, Tm) * std::max(m->qkv_n, d) * 4 +
                          decode_work_capacity(c) * nkv * m->group * (hd + 2) * 4 + m->desc_cap * 4 + 256 * 16;
     m->scratch_bytes = bytes;
     e = hipMalloc(&m->sbase, bytes);
@@ -422,7 +422,7 @@ metro_status metro_create_model(const metro_config* cfg, uint64_t init_seed, met
     m->xr = cv.take<float>(int64_t(c.max_batch) * d);
     m->logits_ws = cv.take<float>(int64_t(c.max_batch) * V);
     m->next_ws = cv.take<int32_t>(c.max_batch);
-    m->parts = cv.take<float>(8LL * metro::kSplitMaxRows * std::max(m->qkv_n, d));
+    m->parts = cv.take<float>(8LL * std::min<int64_t>(metro::kSplitMaxRows, Tm) * std::max(m->qkv_n, d));
     m->attn_part = cv.take<float>(decode_work_capacity(c) * nkv * m->group * (hd + 2));
     m->desc_dev = cv.take<int32_t>(m->desc_cap);
     // the SwiGLU output's padding columns must read as zero

@@ -14,17 +14,18 @@ oracle pass over prompt + fed tokens yields every compared row.
   chunks.
 - 8B widths, 2 layers, a ready batch of 800 agents (the largest batch of the
   agent trace) with lognormal(median 1500) contexts: tiled GEMMs and 800-row
-  attention in decode.  Two agents against the oracle, and 200 agents decoded
-  again in a batch of their own (forked sequences) must give bitwise the same
-  logits: at 200 and at 800 rows every GEMM takes the same kernel and k split
-  (gemm_uses_skinny), so each row's sums are formed in the same order.
+  attention in decode.  Two agents against the oracle; and 600 of the agents,
+  decoded again (forked sequences) in another batch of 800 where the other 200
+  rows are different agents, must give bitwise the same logits.  (The GEMM
+  kernel and its k split are chosen from the number of rows, plan_gemm, so
+  equal batch sizes form each row's sums in the same order.)
 - 8B widths, 2 layers, the prefix-heavy batch: a 1024-token prefix prefilled
   once and forked by page reference into 64 requests with suffixes of
   512..2048 tokens.  Every request's block table starts with the same 64
   prefix pages, and the shortest request is compared with the oracle.
   (Bitwise equality with an unshared run is not asked for here: its calls
   would have other token counts, and the GEMM kernel, so the summation order,
-  is chosen by the number of rows, gemm_uses_skinny.)
+  is chosen by the number of rows, plan_gemm.)
 - Llama-3-70B widths (d 8192, 64/8 heads: GQA group 8, FFN 28672), 2 layers,
   128 agents with contexts uniform in [1024, 3072], decode at B = 128.
 """
@@ -147,7 +148,9 @@ def test_8b_widths_ready_batch_800(metro):
     shape = synth.with_layers(synth.LLAMA3_8B, 2)
     V = shape["vocab"]
     B = 800
-    ctx = synth.trace_start_contexts(0)[:B]
+    ctx_all = synth.trace_start_contexts(0)
+    ctx = ctx_all[:B]
+    extra = ctx_all[B:]
     lens = np.array([len(c) for c in ctx])
     s1 = int(np.argmin(lens))
     s2 = min((n, j) for j, n in enumerate(lens) if n > 1024)[1]
@@ -155,20 +158,26 @@ def test_8b_widths_ready_batch_800(metro):
     say("B=800: drawing weights")
     w = synth.llama_weights(shape, 1, workers=16)
     wants = {s: oracle_with_floor(shape, w, ctx[s], feeds[s], f"B=800 agent {s}") for s in (s1, s2)}
-    subset = sorted(set(range(0, B, 4)) | {s1, s2})
-    say(f"B=800: gpu prefill of {lens.sum()} tokens, decode at B = {B} and at B = {len(subset)}")
-    m = metro.Model(shape, max_batch=B, max_tokens=32 * 512, max_context=4096 + 16, max_seqs=B + len(subset) + 8,
-                    kv_pool_bytes=16 << 30)
+    shared = [i for i in range(B) if i < 400 or i >= 600]
+    say(f"B=800: gpu prefill of {lens.sum()} + {sum(len(c) for c in extra)} tokens, decode of two batches of {B}")
+    m = metro.Model(shape, max_batch=B, max_tokens=32 * 512, max_context=4096 + 16, max_seqs=2 * B + 400,
+                    kv_pool_bytes=20 << 30)
     with m:
         m.load_weights(w)
         seqs = [m.seq_open() for _ in range(B)]
+        others = [m.seq_open() for _ in extra]
         pre = prefill_batched(m, seqs, ctx, 512, 32, [s1, s2])
-        forks = [m.seq_fork(seqs[i], int(lens[i])) for i in subset]
-        dec = decode_fed(m, seqs, feeds, subset)
-        dec_sub = decode_fed(m, forks, feeds[subset], list(range(len(subset))))
-    for j, i in enumerate(subset):
-        np.testing.assert_array_equal(dec_sub[j][0], dec[i][0], err_msg=f"agent {i}: batch of {len(subset)}")
-        np.testing.assert_array_equal(dec_sub[j][1], dec[i][1])
+        prefill_batched(m, others, extra, 512, 32, [])
+        forks = [m.seq_fork(seqs[i], int(lens[i])) for i in shared]
+        dec = decode_fed(m, seqs, feeds, shared)
+        # the same agents at the same rows, the rows 400..599 taken by other agents
+        batch2 = forks[:400] + others + forks[400:]
+        feeds2 = np.concatenate([feeds[:400], synth.feed_tokens(5, len(others), DECODE_STEPS, V), feeds[600:]])
+        rows2 = list(range(400)) + list(range(600, B))
+        dec2 = decode_fed(m, batch2, feeds2, rows2)
+    for i in shared:
+        np.testing.assert_array_equal(dec2[i][0], dec[i][0], err_msg=f"agent {i}: other batch of {B}")
+        np.testing.assert_array_equal(dec2[i][1], dec[i][1])
     for s in (s1, s2):
         got, toks = stitched(pre, dec, s)
         compare(f"B=800 agent {s} ({lens[s]} tokens)", got, toks, *wants[s])

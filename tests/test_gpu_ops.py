@@ -73,8 +73,9 @@ def test_pack_weight_rejects_bad_shapes(metro):
             metro.op_pack_weight(W, ld, N, K, Kp, out)
 
 
-# (M, K, N): decode kernel at M <= 64 and in 64-row chunks above (small N up
-# to 1024 rows), tiled kernel for large M or large N (gemm_uses_skinny)
+# (M, K, N): decode kernel at M <= 64; above it the tiled kernel with 128 x 128
+# blocks (narrow products up to 1000 rows, wide ones up to 192) or 256 x 256
+# blocks, with or without a k split (plan_gemm)
 GEMM_CASES = [(1, 256, 64), (7, 640, 96), (16, 256, 32), (25, 4096, 512), (33, 768, 160), (64, 384, 1376),
               (65, 256, 160), (200, 1152, 416), (129, 128, 96), (300, 4096, 256), (1100, 384, 160),
               (200, 256, 16384), (70, 128, 65536)]
