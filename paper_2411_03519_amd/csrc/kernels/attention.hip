@@ -20,7 +20,7 @@
 // P enters the bf16 matrix core as hi = bf16(p) plus lo = bf16(p - hi) (two
 // MFMAs), which keeps p to about 16 significant bits.
 //
-// Decode: one workgroup per (work item, kv head), a work item being up to 32
+// Decode: one workgroup per (work item, kv head), a work item being up to 128
 // pages of one row, so that long rows spread over several CUs; its waves take
 // the pages round-robin and merge through LDS in wave order.  Rows of several
 // work items leave their states in a workspace and a small kernel merges them
@@ -67,10 +67,10 @@ __device__ __forceinline__ void split_bf16(float p0, float p1, uint32_t& hi, uin
 // loop never waits on a memory lookup; kDecodeRing pages of K/V are kept in
 // flight in a register ring.  The waves' (max, sum, output) states are merged
 // through LDS in wave order.
-constexpr int kDecodeWaves = 4;
-constexpr int kDecodeRing = 2;
+constexpr int kDecodeWaves = 8;
+constexpr int kDecodeRing = 4;
 
-template <int HD, int G, int NW, int PD>
+template <int HD, int G, int NW, int PD, int PS = kDecodePagesPerSplit>
 __global__ __launch_bounds__(NW * 64) void attn_decode_kernel(AttnArgs a) {
   constexpr int KQ = HD / 32;  // score MFMAs per page
   constexpr int NT = HD / 16;  // output tiles (pairs share one 16-byte V load)
@@ -80,9 +80,9 @@ __global__ __launch_bounds__(NW * 64) void attn_decode_kernel(AttnArgs a) {
   const int row = a.work[2 * wi], split = a.work[2 * wi + 1];
   const int ctx = a.row_ctx[row];
   const int qrow = a.row_qrow[row];
-  const int p0 = split * kDecodePagesPerSplit;
+  const int p0 = split * PS;
   const int32_t* bt = a.bt + a.row_bt[row] + p0;
-  const int n_pages = min(ceil_div(ctx, kPage) - p0, kDecodePagesPerSplit);  // pages of this split
+  const int n_pages = min(ceil_div(ctx, kPage) - p0, PS);  // pages of this split
   const float qscale = a.scale * kLog2e;
 
   // Q^T operand: column col = head h*G + col (zero beyond the group); MFMA i

@@ -65,14 +65,10 @@ template <int MT, int NT, int EPI, int PF, int NW>
 __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const uint16_t* __restrict__ X, int ldx,
                                                               const uint16_t* __restrict__ W, int Kp, int M, int N,
                                                               float* __restrict__ outf, uint16_t* __restrict__ outb,
-                                                              int ldo, float* __restrict__ part, int mchunks) {
+                                                              int ldo, float* __restrict__ part) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r = lane & 15, g = lane >> 4;
-  // blockIdx.x = (W row block) * mchunks + (chunk of 16*MT activation rows):
-  // the chunks of one W block are dispatched together, so all but the first
-  // read that block from the caches
-  const int mbase = (blockIdx.x % mchunks) * 16 * MT;
-  const int n0 = (blockIdx.x / mchunks) * 16 * NT;
+  const int n0 = blockIdx.x * 16 * NT;
   const int KS = gridDim.y, slice = blockIdx.y;
   const int kslice = Kp / KS, k0 = slice * kslice;
 
@@ -91,7 +87,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const uint16_t* __
   bool xok[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
-    const int m = mbase + mt * 16 + r;
+    const int m = mt * 16 + r;
     xok[mt] = m < M;
     xrow[mt] = X + static_cast<size_t>(xok[mt] ? m : 0) * ldx + k0 + 8 * g;
   }
@@ -154,7 +150,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const uint16_t* __
         gs += red[w][2 * pr * MT + mt][lane];
         us += red[w][(2 * pr + 1) * MT + mt][lane];
       }
-      const int m = mbase + mt * 16 + m_lane;
+      const int m = mt * 16 + m_lane;
       if (m < M) store_swiglu(gs, us, m, (n0 / 32 + pr) * 16 + n_lane, outb, ldo);
     }
   } else {
@@ -163,7 +159,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const uint16_t* __
 #pragma unroll
       for (int w = 1; w < NW; ++w) sum += red[w][t][lane];
       const int nt = t / MT, mt = t % MT;
-      const int m = mbase + mt * 16 + m_lane;
+      const int m = mt * 16 + m_lane;
       if (m >= M) continue;
       if (KS > 1)
         store_tile<kEpiStoreF32>(sum, m, n0 + nt * 16 + n_lane, part + static_cast<size_t>(slice) * M * N, N);
@@ -230,9 +226,9 @@ struct TileShape {
   static constexpr int BN = WN * TN * 32, BM = WM * TM * 32;  // block tile
   static constexpr int WT = BN / 16, XT = BM / 16;            // 16 x 32 tiles per stage
   static constexpr int LPW = (WT + XT) / WAVES;               // direct loads per wave per stage
-  static_assert((WT + XT) % WAVES == 0 && WT % LPW == 0, "each wave loads tiles of one operand");
+  static_assert((WT + XT) % WAVES == 0, "the waves share the tiles of a stage evenly");
 };
-using BigTile = TileShape<4, 2, 2, 4, 4>;
+using BigTile = TileShape<4, 2, 2, 4, 5>;
 using MidTile = TileShape<4, 1, 1, 4, 8>;
 
 __device__ __forceinline__ f32x16 mfma32(uint4 a, uint4 b, f32x16 c) {
@@ -286,30 +282,32 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
   // Wave w loads tiles w*LPW .. w*LPW + LPW - 1 of the list [W tiles, X
   // tiles] of every stage.  Rows past N or M re-read the last valid row:
   // finite values whose products only reach outputs that are not stored.
-  const bool loads_w = wave * LPW < S::WT;
   const uint16_t* src[LPW];
   uint32_t dst[LPW];
+  int src_step[LPW];       // elements per 32-wide k tile
+  uint32_t dst_step[LPW];  // bytes per stage of the operand's ring
 #pragma unroll
   for (int j = 0; j < LPW; ++j) {
     const int t = wave * LPW + j;
-    if (loads_w) {
+    if (t < S::WT) {
       const int rt = min(n0 / 16 + t, N / 16 - 1);
       src[j] = W + (static_cast<size_t>(rt) * (Kp / 32) + k0 / 32) * 512 + lane * 8;
       dst[j] = lds_address(&wring[0][0]) + t * 1024;
+      src_step[j] = 512;
+      dst_step[j] = S::WT * 1024;
     } else {
       const int tx = t - S::WT;
       const int row = min(m0 + 16 * tx + (lane & 15), M - 1);
       src[j] = X + static_cast<size_t>(row) * ldx + k0 + 8 * (lane >> 4);
       dst[j] = lds_address(&xring[0][0]) + tx * 1024;
+      src_step[j] = 32;
+      dst_step[j] = S::XT * 1024;
     }
   }
-  const int src_step = loads_w ? 512 : 32;  // elements per 32-wide k tile
-  constexpr uint32_t wstage = S::WT * 1024, xstage = S::XT * 1024;
-  const uint32_t dst_step = loads_w ? wstage : xstage;
   auto issue = [&](int kt) __attribute__((always_inline)) {
-    const uint32_t off = (kt % NS) * dst_step;
+    const uint32_t stage = kt % NS;
 #pragma unroll
-    for (int j = 0; j < LPW; ++j) lds_load16(src[j] + kt * src_step, dst[j] + off);
+    for (int j = 0; j < LPW; ++j) lds_load16(src[j] + kt * src_step[j], dst[j] + stage * dst_step[j]);
   };
 
   f32x16 acc[TN][TM];
@@ -353,11 +351,44 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
     }
   }
 
-  // fully unrolled (acc must stay in registers); the scheduling barriers keep
-  // the read-modify-write epilogue from hoisting all of its loads at once.
-  // With KS > 1 the slice sums go to part[slice][m][n].
+  // Fully unrolled (acc must stay in registers).  With KS > 1 the slice sums
+  // go to part[slice][m][n].  The residual add first loads all 4 * TN float4
+  // of one 32-row group of activation rows, then adds and stores them (one
+  // round trip per group rather than per value); the scheduling barrier keeps
+  // the compiler from hoisting every group's loads at once.
   float* const pout = KS > 1 ? part + static_cast<size_t>(slice) * M * N : outf;
   const int pld = KS > 1 ? N : ldo;
+  if (EPI == kEpiAddF32 && KS == 1) {
+#pragma unroll
+    for (int j = 0; j < TM; ++j) {
+      const int m = m0 + wm * TM * 32 + j * 32 + lr;
+      if (m >= M) continue;
+      float4 r[TN][4];
+#pragma unroll
+      for (int i = 0; i < TN; ++i) {
+        const int nb = min(n0 + wn * TN * 32 + i * 32, N - 32);  // in bounds; stored only if < N
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          r[i][q] = *reinterpret_cast<const float4*>(outf + static_cast<size_t>(m) * ldo + nb + 8 * q + 4 * lh);
+      }
+#pragma unroll
+      for (int i = 0; i < TN; ++i) {
+        const int nb = n0 + wn * TN * 32 + i * 32;
+        if (nb >= N) continue;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float4 v = r[i][q];
+          v.x += acc[i][j][4 * q];
+          v.y += acc[i][j][4 * q + 1];
+          v.z += acc[i][j][4 * q + 2];
+          v.w += acc[i][j][4 * q + 3];
+          *reinterpret_cast<float4*>(outf + static_cast<size_t>(m) * ldo + nb + 8 * q + 4 * lh) = v;
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    return;
+  }
 #pragma unroll
   for (int j = 0; j < TM; ++j) {
     const int m = m0 + wm * TM * 32 + j * 32 + lr;
@@ -392,10 +423,7 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
 
 // ---------------------------------------------------------------------------
 
-#ifndef METRO_SKINNY_PF
-#define METRO_SKINNY_PF 1
-#endif
-constexpr int kSkinnyPF = METRO_SKINNY_PF;  // k blocks in flight per wave
+constexpr int kSkinnyPF = 1;                // k blocks in flight per wave
 constexpr int kSkinnyWaves = 8;             // waves per workgroup (k split inside it)
 
 // Row tiles per wave of the decode kernel: 4 (64 rows) amortises the
@@ -447,9 +475,8 @@ int gemm_splits(int M, int N, int Kp, int epilogue) { return plan_gemm(M, N, Kp,
 template <int MT, int NT, int EPI>
 static void launch_skinny(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, float* outf,
                           uint16_t* outb, int ldo, float* part, int ks, hipStream_t s) {
-  const int mchunks = (M + 16 * MT - 1) / (16 * MT);
-  launch_kernel((gemm_skinny_kernel<MT, NT, EPI, kSkinnyPF, kSkinnyWaves>), dim3(N / (16 * NT) * mchunks, ks),
-                dim3(kSkinnyWaves * 64), 0, s, X, ldx, W, Kp, M, N, outf, outb, ldo, part, mchunks);
+  launch_kernel((gemm_skinny_kernel<MT, NT, EPI, kSkinnyPF, kSkinnyWaves>), dim3(N / (16 * NT), ks),
+                dim3(kSkinnyWaves * 64), 0, s, X, ldx, W, Kp, M, N, outf, outb, ldo, part);
 }
 
 template <int NT, int EPI>

@@ -130,7 +130,7 @@ struct AttnArgs {
 // Decode attention: one workgroup per (work item, kv head), a work item being
 // up to kDecodePagesPerSplit pages of one row.  Rows of one split are final;
 // the others leave (max, sum, output) states for launch_attn_combine.
-constexpr int kDecodePagesPerSplit = 32;
+constexpr int kDecodePagesPerSplit = 128;
 hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s);
 hipError_t launch_attn_combine(const AttnArgs& a, hipStream_t s);
 

@@ -78,7 +78,10 @@ def test_pack_weight_rejects_bad_shapes(metro):
 # blocks, with or without a k split (plan_gemm)
 GEMM_CASES = [(1, 256, 64), (7, 640, 96), (16, 256, 32), (25, 4096, 512), (33, 768, 160), (64, 384, 1376),
               (65, 256, 160), (200, 1152, 416), (129, 128, 96), (300, 4096, 256), (1100, 384, 160),
-              (200, 256, 16384), (70, 128, 65536)]
+              (200, 256, 16384), (70, 128, 65536),
+              (129, 1024, 512),      # 128 x 128 tiles, 2 k slices with a workspace
+              (300, 4096, 16384),    # 256 x 256 tiles, 2 k slices with a workspace
+              (600, 2048, 288)]      # 128 x 128 tiles, ragged in both M and N
 
 
 @pytest.mark.parametrize("M,K,N", GEMM_CASES + [(25, 14336, 512), (3, 1024, 4096)])

@@ -288,14 +288,15 @@ def test_llama3_8b_widths_two_layers(metro):
 
 
 def test_long_contexts_split_decode_attention(metro):
-    """Contexts of 600 and 1100 tokens span several 32-page work items of the
-    decode attention (merged by the combine kernel); a short row rides along."""
+    """Contexts of 2049 to 4300 tokens span two and three 128-page work items of
+    the decode attention (merged by the combine kernel in split order); short
+    rows ride along."""
     w = synth.llama_weights(synth.TINY, 5, norm="random")
     ref = OracleModel(LlamaShape(**synth.TINY), w)
     rng = np.random.default_rng(25)
-    prompts = [rng.integers(0, 4096, n) for n in (600, 1100, 40, 513)]
+    prompts = [rng.integers(0, 4096, n) for n in (2049, 4300, 40, 513)]
     gens = [ref.generate(p, 4, chunk=512) for p in prompts]
-    with make_model(metro, synth.TINY, w, max_batch=8, max_tokens=2048, max_context=2048) as m:
+    with make_model(metro, synth.TINY, w, max_batch=8, max_tokens=2048, max_context=4400) as m:
         logits, toks = gpu_teacher_forced(m, prompts, [g[0][:-1] for g in gens], chunk=512)
     want = np.stack([g[1] for g in gens])
     assert_logits_close(logits, want, "long contexts")
