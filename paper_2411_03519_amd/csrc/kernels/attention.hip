@@ -31,7 +31,7 @@
 // Prefill (flash attention): one workgroup = (query block, kv head); the K and
 // V pages of the block's visible context go through LDS in pairs, by direct
 // loads into a 4-stage ring (three pairs in flight while one is consumed), and
-// are shared by the four waves; causal masking per element.
+// are shared by the eight waves (two per SIMD); causal masking per element.
 #include "common.h"
 #include "kernels.h"
 
@@ -233,14 +233,15 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
 
 // Query columns of one 16-wide MFMA tile: 16/G tokens x G heads.
 template <int HD, int G>
-__global__ __launch_bounds__(256) void attn_prefill_kernel(PrefillAttnArgs a) {
+__global__ __launch_bounds__(512) void attn_prefill_kernel(PrefillAttnArgs a) {
   constexpr int KQ = HD / 32;
   constexpr int NT = HD / 16;
-  constexpr int NQ = 4;               // query tiles per wave
+  constexpr int NW = 8;               // waves (two per SIMD)
+  constexpr int NQ = 2;               // query tiles per wave
   constexpr int TPT = 16 / G;         // tokens per tile
   constexpr int TPW = NQ * TPT;       // tokens per wave
   constexpr int PCH = kPage * HD / 8;  // 16-byte chunks of one K (or V^T) page tile
-  constexpr int LPW = PCH / 64;       // direct loads per wave per stage
+  constexpr int LPW = PCH / 128;      // direct loads per wave per stage (half a tile)
   constexpr int NS = 4;               // stages of the LDS ring
   // stage = one page pair: [K page 0, K page 1, V^T page 0, V^T page 1]
   __shared__ uint4 ring[NS][4][PCH];
@@ -283,15 +284,17 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(PrefillAttnArgs a) {
     for (int t = 0; t < NT; ++t) o[n][t] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  // Wave w brings tile w of every stage: the K (w < 2) or V^T (w >= 2) tile
-  // of page 2*pair + (w & 1).  The absent second page of an odd count is
-  // stood in for by the last page: finite values, all of its keys masked.
-  const size_t part = kv_offset(0, wave >> 1, a.nkv, h, 0, HD, 0);
+  // Waves 2t and 2t+1 bring the two halves of tile t of every stage: the K
+  // (t < 2) or V^T (t >= 2) tile of page 2*pair + (t & 1).  The absent second
+  // page of an odd count is stood in for by the last page: finite values, all
+  // of its keys masked.
+  const int tile = wave >> 1, half = wave & 1;
+  const size_t part = kv_offset(0, tile >> 1, a.nkv, h, 0, HD, 0) + half * (PCH / 2) * 8;
   const size_t pstride = static_cast<size_t>(2) * a.nkv * kPage * HD;
   auto issue = [&](int pair) __attribute__((always_inline)) {
-    const int pi = min(2 * pair + (wave & 1), n_pages - 1);
+    const int pi = min(2 * pair + (tile & 1), n_pages - 1);
     const uint16_t* src = a.kv + static_cast<size_t>(bt[pi]) * pstride + part + 8 * lane;
-    const uint32_t dst = lds_address(&ring[pair % NS][wave][0]);
+    const uint32_t dst = lds_address(&ring[pair % NS][tile][half * (PCH / 2)]);
 #pragma unroll
     for (int c = 0; c < LPW; ++c) lds_load16(src + 512 * c, dst + 1024 * c);
   };
@@ -344,8 +347,7 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(PrefillAttnArgs a) {
       }
       float mp = fmaxf(fmaxf(fmaxf(sv[0][0], sv[0][1]), fmaxf(sv[0][2], sv[0][3])),
                        fmaxf(fmaxf(sv[1][0], sv[1][1]), fmaxf(sv[1][2], sv[1][3])));
-      mp = fmaxf(mp, __shfl_xor(mp, 16, kWave));
-      mp = fmaxf(mp, __shfl_xor(mp, 32, kWave)) * qscale;  // in log2 units
+      mp = max_xor32(max_xor16(mp)) * qscale;  // in log2 units
       // The reference max m only moves when some column's max exceeds it by
       // more than 8 (a factor 2^8): o and l carry the same scale, so their
       // quotient is unchanged, and p = 2^(s - m) stays below 2^8.
@@ -384,9 +386,7 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(PrefillAttnArgs a) {
 
 #pragma unroll
   for (int n = 0; n < NQ; ++n) {
-    float L = l[n];
-    L += __shfl_xor(L, 16, kWave);
-    L += __shfl_xor(L, 32, kWave);
+    const float L = sum_xor32(sum_xor16(l[n]));
     if (!qok[n]) continue;
     const float inv = 1.0f / L;
     uint16_t* op = a.out + (static_cast<size_t>(qrow[n]) * a.nq + h * G + col % G) * HD;
@@ -433,10 +433,10 @@ template <int HD>
 static hipError_t launch_prefill_hd(const PrefillAttnArgs& a, hipStream_t s) {
   const dim3 grid(a.n_blocks * a.nkv);
   switch (a.nq / a.nkv) {
-    case 1: launch_kernel((attn_prefill_kernel<HD, 1>), grid, dim3(256), 0, s, a); break;
-    case 2: launch_kernel((attn_prefill_kernel<HD, 2>), grid, dim3(256), 0, s, a); break;
-    case 4: launch_kernel((attn_prefill_kernel<HD, 4>), grid, dim3(256), 0, s, a); break;
-    case 8: launch_kernel((attn_prefill_kernel<HD, 8>), grid, dim3(256), 0, s, a); break;
+    case 1: launch_kernel((attn_prefill_kernel<HD, 1>), grid, dim3(512), 0, s, a); break;
+    case 2: launch_kernel((attn_prefill_kernel<HD, 2>), grid, dim3(512), 0, s, a); break;
+    case 4: launch_kernel((attn_prefill_kernel<HD, 4>), grid, dim3(512), 0, s, a); break;
+    case 8: launch_kernel((attn_prefill_kernel<HD, 8>), grid, dim3(512), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
