@@ -39,9 +39,9 @@ metro_status metro_op_pack_weight(const uint16_t* W_rowmajor, int32_t ld, int32_
  * epilogue:
  *   0  out_f32[m*ldo + n]  = acc[m, n]
  *   1  out_f32[m*ldo + n] += acc[m, n]                       (residual add)
- *   2  W rows come in blocks of 32 = 16 gate rows then 16 up rows of the same
- *      features (16-row tiles alternate gate, up); out_bf16[m*ldo + j] =
- *      bf16(silu(gate_j) * up_j), j < N/2
+ *   2  W rows come in blocks of 16 = 8 gate rows then the 8 up rows of the
+ *      same features (block b: gate_j, j = 8b .. 8b+7, then up_j);
+ *      out_bf16[m*ldo + j] = bf16(silu(gate_j) * up_j), j < N/2
  *      (SwiGLU, Shazeer 2020).
  * workspace: NULL, or device fp32 [8][M][N]; when given, a decode-sized GEMM
  * (M <= 1024, epilogue 0 or 1) may run the k-split form the model uses (slices in

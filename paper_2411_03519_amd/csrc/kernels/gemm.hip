@@ -141,17 +141,23 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const uint16_t* __
   const int m_lane = r;  // activation row within a 16-row tile
   const int n_lane = 4 * g;
   if (EPI == kEpiSwiGLU) {
-    // tiles (2p, 2p+1) hold the gate and up features of (gate, up) block n0/32 + p
-    for (int u = wave; u < (NT / 2) * MT; u += NW) {
-      const int pr = u / MT, mt = u % MT;
-      f32x4 gs = red[0][2 * pr * MT + mt][lane], us = red[0][(2 * pr + 1) * MT + mt][lane];
+    // Tile nt holds the gate (rows 0..7) and up (rows 8..15) projections of
+    // features 8 (n0/16 + nt) .. +7: lane l < 32 has gate rows 4(l/16) .. +3
+    // and lane l + 32 the matching up rows, which a 32-lane swap brings together.
+    for (int t = wave; t < NT * MT; t += NW) {
+      f32x4 sum = red[0][t][lane];
 #pragma unroll
-      for (int w = 1; w < NW; ++w) {
-        gs += red[w][2 * pr * MT + mt][lane];
-        us += red[w][(2 * pr + 1) * MT + mt][lane];
+      for (int w = 1; w < NW; ++w) sum += red[w][t][lane];
+      f32x4 gt, up;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(sum[i]), __float_as_uint(sum[i]), false, false);
+        gt[i] = __uint_as_float(pr[0]);  // from lane l % 32
+        up[i] = __uint_as_float(pr[1]);  // from lane l % 32 + 32
       }
+      const int nt = t / MT, mt = t % MT;
       const int m = mt * 16 + m_lane;
-      if (m < M) store_swiglu(gs, us, m, (n0 / 32 + pr) * 16 + n_lane, outb, ldo);
+      if (lane < 32 && m < M) store_swiglu(gt, up, m, 8 * (n0 / 16 + nt) + n_lane, outb, ldo);
     }
   } else {
     for (int t = wave; t < NT * MT; t += NW) {
@@ -398,12 +404,14 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
       const int nb = n0 + wn * TN * 32 + i * 32;  // 32-row tile of W
       if (nb >= N) continue;
       if (EPI == kEpiSwiGLU) {
-        // rows 0..15 of the tile are gate features, rows 16..31 the matching up features
+        // the tile is two 16-row blocks of 8 gate rows then the 8 matching up
+        // rows: the lane's rows 8q + 4(l/32) + i of q = 0, 2 (gate) pair with
+        // those of q = 1, 3 (up) in the same lane
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
-          const f32x4 gt{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-          const f32x4 up{acc[i][j][4 * q + 8], acc[i][j][4 * q + 9], acc[i][j][4 * q + 10], acc[i][j][4 * q + 11]};
-          store_swiglu(gt, up, m, (nb / 32) * 16 + 8 * q + 4 * lh, outb, ldo);
+          const f32x4 gt{acc[i][j][8 * q], acc[i][j][8 * q + 1], acc[i][j][8 * q + 2], acc[i][j][8 * q + 3]};
+          const f32x4 up{acc[i][j][8 * q + 4], acc[i][j][8 * q + 5], acc[i][j][8 * q + 6], acc[i][j][8 * q + 7]};
+          store_swiglu(gt, up, m, 8 * (nb / 16 + q) + 4 * lh, outb, ldo);
           __builtin_amdgcn_sched_barrier(0);
         }
       } else {
@@ -428,8 +436,12 @@ constexpr int kSkinnyWaves = 8;             // waves per workgroup (k split insi
 
 // Row tiles per wave of the decode kernel: 4 (64 rows) amortises the
 // activation reads best, but for short, narrow products (QKV-sized) 2 tiles
-// and twice the workgroups finish sooner (11.0 vs 12.9 us at N=6144, K=4096).
-static int skinny_tiles(int N, int Kp) {
+// and twice the workgroups finish sooner (11.0 vs 12.9 us at N=6144, K=4096),
+// and the gate/up product, which cannot split K, takes 7 where that makes the
+// workgroups a multiple of the 256 CUs (448 -> 256 at the 8B shape: 46.3 ->
+// 42.5 us).
+static int skinny_tiles(int N, int Kp, int epilogue) {
+  if (epilogue == kEpiSwiGLU && (N / 16) % (7 * 256) == 0) return 7;
   if (N % 64) return 2;
   return N <= 8192 && Kp <= 4096 ? 2 : 4;
 }
@@ -452,7 +464,7 @@ GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, bool can_split) {
   const bool split = can_split && epilogue != kEpiSwiGLU && M <= kSplitMaxRows;
   if (M <= 64) {
     p.kind = GemmKind::kSkinny;
-    p.nt = skinny_tiles(N, Kp);
+    p.nt = skinny_tiles(N, Kp, epilogue);
     if (split) p.ks = gemm_k_splits(N / (16 * p.nt), p.nt == 2 ? 512 : 256, M, Kp);
     return p;
   }
@@ -475,8 +487,10 @@ int gemm_splits(int M, int N, int Kp, int epilogue) { return plan_gemm(M, N, Kp,
 template <int MT, int NT, int EPI>
 static void launch_skinny(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, float* outf,
                           uint16_t* outb, int ldo, float* part, int ks, hipStream_t s) {
-  launch_kernel((gemm_skinny_kernel<MT, NT, EPI, kSkinnyPF, kSkinnyWaves>), dim3(N / (16 * NT), ks),
-                dim3(kSkinnyWaves * 64), 0, s, X, ldx, W, Kp, M, N, outf, outb, ldo, part);
+  // 7 row tiles: 4 waves, so that the cross-wave reduction buffer fits in LDS
+  constexpr int NW = NT == 7 ? 4 : kSkinnyWaves;
+  launch_kernel((gemm_skinny_kernel<MT, NT, EPI, kSkinnyPF, NW>), dim3(N / (16 * NT), ks), dim3(NW * 64), 0, s, X,
+                ldx, W, Kp, M, N, outf, outb, ldo, part);
 }
 
 template <int NT, int EPI>
@@ -503,7 +517,9 @@ static hipError_t launch_epi(const GemmPlan& p, const uint16_t* X, int ldx, cons
                              float* outf, uint16_t* outb, int ldo, float* part, hipStream_t s) {
   switch (p.kind) {
     case GemmKind::kSkinny:
-      if (p.nt == 4)
+      if (p.nt == 7)
+        launch_skinny_m<7, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, p.ks, s);
+      else if (p.nt == 4)
         launch_skinny_m<4, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, p.ks, s);
       else
         launch_skinny_m<2, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, p.ks, s);

@@ -55,17 +55,17 @@ hipError_t launch_gather_rows(const float* x, int d, const int32_t* rows, int n,
 hipError_t launch_argmax(const float* logits, int vocab, int rows, int32_t* out, hipStream_t s);
 
 // Random initialisation of one logical weight tensor [rows, cols]: logical
-// row r goes to row map(r) = (r / 16) * row_block + row_shift + r % 16 of the
-// destination, which is row-major with row stride ld, or, with packed, in MFMA
-// operand order (packed_offset) with ld = Kp.  Values are 0.02 * N(0, 1) from
-// a SplitMix64-keyed Box-Muller draw, rounded to bf16.
-hipError_t launch_init_normal(uint16_t* dst, int64_t ld, int rows, int cols, int row_block, int row_shift,
-                              uint64_t key, bool packed, hipStream_t s);
+// row r goes to row map(r) = (r / row_group) * row_block + row_shift +
+// r % row_group of the destination, which is row-major with row stride ld,
+// or, with packed, in MFMA operand order (packed_offset) with ld = Kp.  Values
+// are 0.02 * N(0, 1) from a SplitMix64-keyed Box-Muller draw, rounded to bf16.
+hipError_t launch_init_normal(uint16_t* dst, int64_t ld, int rows, int cols, int row_group, int row_block,
+                              int row_shift, uint64_t key, bool packed, hipStream_t s);
 
 // Row-major bf16 [rows, cols] (row stride ld_src, device) -> rows map(r) (as
 // above) of a packed [*, Kp] weight; columns cols .. Kp-1 are written as zero.
 hipError_t launch_pack_weight(const uint16_t* src, int64_t ld_src, int rows, int cols, uint16_t* dst, int Kp,
-                              int row_block, int row_shift, hipStream_t s);
+                              int row_group, int row_block, int row_shift, hipStream_t s);
 hipError_t launch_fill_bf16(uint16_t* dst, int64_t n, uint16_t value, hipStream_t s);
 
 // Copy page src to page dst in every layer (page_elems bf16 per layer).
@@ -77,7 +77,8 @@ hipError_t launch_page_copy(uint16_t* pool, int64_t layer_stride, int64_t page_e
 enum GemmEpilogue {
   kEpiStoreF32 = 0,  // out_f32[m, n] = acc
   kEpiAddF32 = 1,    // out_f32[m, n] += acc   (residual stream)
-  kEpiSwiGLU = 2,    // W rows interleaved in blocks of 16 (gate, up):
+  kEpiSwiGLU = 2,    // W rows in blocks of 16 = 8 gate rows, then the 8 up
+                     // rows of the same features:
                      // out_bf16[m, j] = bf16(silu(gate_j) * up_j), N = 2 * F
 };
 

@@ -48,7 +48,7 @@ struct Layer {
   uint16_t* ffn_norm;
   uint16_t* wqkv;   // [(nq + 2 nkv) hd, d]: rows of wq, then wk, then wv
   uint16_t* wo;     // [d, nq hd]
-  uint16_t* wgu;    // [2F, d]: blocks of 16 gate rows then 16 up rows
+  uint16_t* wgu;    // [2F, d]: blocks of 16 rows = 8 gate rows, then the 8 up rows of the same features
   uint16_t* wdown;  // [d, Fp] (K padded with zeros to a multiple of 128)
 };
 
@@ -484,22 +484,22 @@ metro_status metro_create_model(const metro_config* cfg, uint64_t init_seed, met
     auto chk = [&](hipError_t x) {
       if (r == hipSuccess) r = x;
     };
-    chk(metro::launch_init_normal(m->embed, d, V, d, 16, 0, key(METRO_W_EMBED, -1), false, 0));
-    chk(metro::launch_init_normal(m->lm_head, d, V, d, 16, 0, key(METRO_W_LM_HEAD, -1), true, 0));
+    chk(metro::launch_init_normal(m->embed, d, V, d, 16, 16, 0, key(METRO_W_EMBED, -1), false, 0));
+    chk(metro::launch_init_normal(m->lm_head, d, V, d, 16, 16, 0, key(METRO_W_LM_HEAD, -1), true, 0));
     chk(metro::launch_fill_bf16(m->final_norm, d, one, 0));
     for (int l = 0; l < c.n_layers; ++l) {
       Layer& L = m->layers[l];
       chk(metro::launch_fill_bf16(L.attn_norm, d, one, 0));
       chk(metro::launch_fill_bf16(L.ffn_norm, d, one, 0));
-      chk(metro::launch_init_normal(L.wqkv, d, m->q_dim, d, 16, 0, key(METRO_W_WQ, l), true, 0));
-      chk(metro::launch_init_normal(L.wqkv, d, m->kv_dim, d, 16, m->q_dim, key(METRO_W_WK, l), true, 0));
-      chk(metro::launch_init_normal(L.wqkv, d, m->kv_dim, d, 16, m->q_dim + m->kv_dim, key(METRO_W_WV, l), true,
+      chk(metro::launch_init_normal(L.wqkv, d, m->q_dim, d, 16, 16, 0, key(METRO_W_WQ, l), true, 0));
+      chk(metro::launch_init_normal(L.wqkv, d, m->kv_dim, d, 16, 16, m->q_dim, key(METRO_W_WK, l), true, 0));
+      chk(metro::launch_init_normal(L.wqkv, d, m->kv_dim, d, 16, 16, m->q_dim + m->kv_dim, key(METRO_W_WV, l), true,
                                     0));
-      chk(metro::launch_init_normal(L.wo, m->q_dim, d, m->q_dim, 16, 0, key(METRO_W_WO, l), true, 0));
-      chk(metro::launch_init_normal(L.wgu, d, F, d, 32, 0, key(METRO_W_WGATE, l), true, 0));
-      chk(metro::launch_init_normal(L.wgu, d, F, d, 32, 16, key(METRO_W_WUP, l), true, 0));
+      chk(metro::launch_init_normal(L.wo, m->q_dim, d, m->q_dim, 16, 16, 0, key(METRO_W_WO, l), true, 0));
+      chk(metro::launch_init_normal(L.wgu, d, F, d, 8, 16, 0, key(METRO_W_WGATE, l), true, 0));
+      chk(metro::launch_init_normal(L.wgu, d, F, d, 8, 16, 8, key(METRO_W_WUP, l), true, 0));
       if (m->Fp != F) chk(metro::launch_fill_bf16(L.wdown, static_cast<int64_t>(d) * m->Fp, 0, 0));
-      chk(metro::launch_init_normal(L.wdown, m->Fp, d, F, 16, 0, key(METRO_W_WDOWN, l), true, 0));
+      chk(metro::launch_init_normal(L.wdown, m->Fp, d, F, 16, 16, 0, key(METRO_W_WDOWN, l), true, 0));
     }
     if (r == hipSuccess) r = hipDeviceSynchronize();
     if (r != hipSuccess) return bail(hip_fail(nullptr, r, "weight initialisation"));
@@ -526,9 +526,10 @@ metro_status metro_load_weight(metro_model* m, int32_t id, int32_t layer, const 
   if (id < METRO_W_EMBED || id > METRO_W_WDOWN) return fail(METRO_E_INVAL, "unknown weight id %d", id);
   if (!global && (layer < 0 || layer >= c.n_layers)) return fail(METRO_E_INVAL, "layer %d out of range", layer);
   HIP_TRY(m, hipSetDevice(m->device));
-  // destination: (base, rows, cols, dst row stride, row block, row shift)
+  // destination: (base, rows, cols, dst row stride); logical row r goes to
+  // row (r / grp) * blk + shift + r % grp
   uint16_t* base = nullptr;
-  int64_t rows = 0, cols = 0, ld = 0, blk = 16, shift = 0;
+  int64_t rows = 0, cols = 0, ld = 0, grp = 16, blk = 16, shift = 0;
   const Layer* L = global ? nullptr : &m->layers[layer];
   switch (id) {
     case METRO_W_EMBED: base = m->embed; rows = V; cols = d; break;
@@ -540,8 +541,8 @@ metro_status metro_load_weight(metro_model* m, int32_t id, int32_t layer, const 
     case METRO_W_WK: base = L->wqkv; rows = m->kv_dim; cols = d; shift = m->q_dim; break;
     case METRO_W_WV: base = L->wqkv; rows = m->kv_dim; cols = d; shift = m->q_dim + m->kv_dim; break;
     case METRO_W_WO: base = L->wo; rows = d; cols = m->q_dim; break;
-    case METRO_W_WGATE: base = L->wgu; rows = F; cols = d; blk = 32; break;
-    case METRO_W_WUP: base = L->wgu; rows = F; cols = d; blk = 32; shift = 16; break;
+    case METRO_W_WGATE: base = L->wgu; rows = F; cols = d; grp = 8; break;
+    case METRO_W_WUP: base = L->wgu; rows = F; cols = d; grp = 8; shift = 8; break;
     case METRO_W_WDOWN: base = L->wdown; rows = d; cols = F; ld = m->Fp; break;
   }
   if (ld == 0) ld = cols;
@@ -553,13 +554,14 @@ metro_status metro_load_weight(metro_model* m, int32_t id, int32_t layer, const 
     return METRO_OK;
   }
   // projections: row-major upload into a staging buffer, then rearranged into
-  // MFMA operand order, logical row r going to row (r / 16) * blk + shift + r % 16
+  // MFMA operand order at their rows
   uint16_t* stage = nullptr;
   HIP_TRY(m, hipMalloc(&stage, rows * cols * 2));
   hipError_t e = hipMemcpy(stage, src, rows * cols * 2, hipMemcpyHostToDevice);
   if (e == hipSuccess)
     e = metro::launch_pack_weight(stage, cols, static_cast<int>(rows), static_cast<int>(cols), base,
-                                  static_cast<int>(ld), static_cast<int>(blk), static_cast<int>(shift), nullptr);
+                                  static_cast<int>(ld), static_cast<int>(grp), static_cast<int>(blk),
+                                  static_cast<int>(shift), nullptr);
   if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
   (void)hipFree(stage);
   if (e != hipSuccess) return hip_fail(m, e, "weight upload");
@@ -849,7 +851,8 @@ metro_status metro_op_pack_weight(const uint16_t* W_rowmajor, int32_t ld, int32_
   g_err.clear();
   if (!W_rowmajor || !W_packed || N <= 0 || N % 16 || Kp <= 0 || Kp % 128 || K <= 0 || K > Kp || ld < K)
     return fail(METRO_E_INVAL, "pack_weight: bad shape (N %% 16, Kp %% 128, 0 < K <= Kp, ld >= K required)");
-  hipError_t e = metro::launch_pack_weight(W_rowmajor, ld, N, K, W_packed, Kp, 16, 0, static_cast<hipStream_t>(stream));
+  hipError_t e =
+      metro::launch_pack_weight(W_rowmajor, ld, N, K, W_packed, Kp, 16, 16, 0, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(nullptr, e, "launch_pack_weight");
   return METRO_OK;
 }

@@ -110,17 +110,17 @@ def test_gemm_f32_epilogues(metro, M, K, N, epi, split):
 
 
 @pytest.mark.parametrize("M,K,F", [(3, 256, 688), (25, 256, 48), (64, 512, 112), (96, 256, 688), (130, 384, 80),
-                                   (150, 128, 8192)])
+                                   (150, 128, 8192), (25, 128, 14336), (40, 128, 14336), (300, 128, 14336)])
 def test_gemm_swiglu_epilogue(metro, M, K, F):
     print(f"swiglu M={M} K={K} F={F}", flush=True)
     rng = np.random.default_rng(M + K + F)
     X = rand_bf16(rng, (M, K))
     Wg = rand_bf16(rng, (F, K), 0.1)
     Wu = rand_bf16(rng, (F, K), 0.1)
-    packed = np.zeros((2 * F, K), np.uint16)
-    for b in range(F // 16):
-        packed[32 * b:32 * b + 16] = Wg[16 * b:16 * b + 16]
-        packed[32 * b + 16:32 * b + 32] = Wu[16 * b:16 * b + 16]
+    packed = np.zeros((2 * F, K), np.uint16)  # blocks of 8 gate rows, then the 8 matching up rows
+    for b in range(F // 8):
+        packed[16 * b:16 * b + 8] = Wg[8 * b:8 * b + 8]
+        packed[16 * b + 8:16 * b + 16] = Wu[8 * b:8 * b + 8]
     ldo = (F + 127) // 128 * 128
     out = torch.zeros((M, ldo), dtype=torch.int16, device="cuda")
     metro.op_gemm(dev_u16(X), pack_dev(metro, packed, K, K), M, 2 * F, K, 2, out, ldo)
