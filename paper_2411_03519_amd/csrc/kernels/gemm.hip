@@ -131,6 +131,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const uint16_t* __
     }
   }
 
+  mfma_drain();
   __shared__ f32x4 red[NW][NT * MT][kWave];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt)
@@ -233,6 +234,7 @@ struct TileShape {
   static constexpr int WT = BN / 16, XT = BM / 16;            // 16 x 32 tiles per stage
   static constexpr int LPW = (WT + XT) / WAVES;               // direct loads per wave per stage
   static_assert((WT + XT) % WAVES == 0, "the waves share the tiles of a stage evenly");
+  static_assert(NS >= 3, "the pipeline keeps a stage in use, one landed and loads in flight");
 };
 using BigTile = TileShape<4, 2, 2, 4, 5>;
 using MidTile = TileShape<4, 1, 1, 4, 8>;
@@ -324,38 +326,62 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+  // operand fragments of one 16-wide k half (ks) of stage kt
+  auto read_frags = [&](int kt, int ks, uint4 (&af)[TN], uint4 (&bf)[TM]) __attribute__((always_inline)) {
+    const uint4* ws = wring[kt % NS];
+    const uint4* xs = xring[kt % NS];
+    const int q = 16 * (2 * ks + lh);  // chunk of the lane's 8 k values within a tile
+#pragma unroll
+    for (int i = 0; i < TN; ++i) {
+      const int row = wn * TN * 32 + i * 32 + lr;
+      af[i] = ws[(row >> 4) * 64 + (row & 15) + q];
+    }
+#pragma unroll
+    for (int j = 0; j < TM; ++j) {
+      const int row = wm * TM * 32 + j * 32 + lr;
+      bf[j] = xs[(row >> 4) * 64 + (row & 15) + q];
+    }
+  };
+  auto mfmas = [&](const uint4 (&af)[TN], const uint4 (&bf)[TM]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < TN; ++i)
+#pragma unroll
+      for (int j = 0; j < TM; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
+  };
+
+  // Software pipeline across the barrier: the fragments of the first k half
+  // of step kt + 1 are read while the second half of step kt multiplies, so
+  // no wave waits on LDS after a barrier.  The barrier of step kt sits
+  // between its two halves: past it, every wave's loads of stage kt + 1 have
+  // landed and every wave has consumed stage kt - 1, whose slot then takes
+  // stage kt + NS - 1.
 #pragma unroll
   for (int p = 0; p < NS - 1; ++p)
     if (p < nk) issue(p);
-  for (int kt = 0; kt < nk; ++kt) {
-    // stage kt has landed once only the later stages' loads are outstanding;
-    // after the barrier every wave's part is in LDS, and the stage read in
-    // step kt-1 is free for stage kt + NS - 1
-    wait_later_stages<LPW, NS - 2>(nk - 1 - kt);
+  wait_later_stages<LPW, NS - 2>(nk - 1);
+  lds_barrier();
+  uint4 a0[TN], b0[TM], a1[TN], b1[TM];
+  read_frags(0, 0, a0, b0);
+  // (the last step is peeled: a loop exit between the halves would merge
+  // control flow there and make the compiler's LDS waits cover the reads
+  // issued for the next step)
+  for (int kt = 0; kt + 1 < nk; ++kt) {
+    read_frags(kt, 1, a1, b1);
+    mfmas(a0, b0);
+    // stage kt + 1 has landed once only the loads of stages kt + 2 .. are
+    // outstanding
+    wait_later_stages<LPW, NS - 3>(nk - 2 - kt);
+    __builtin_amdgcn_sched_barrier(0);
     lds_barrier();
+    __builtin_amdgcn_sched_barrier(0);
     if (kt + NS - 1 < nk) issue(kt + NS - 1);
-    const uint4* ws = wring[kt % NS];
-    const uint4* xs = xring[kt % NS];
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const int q = 16 * (2 * ks + lh);  // chunk of the lane's 8 k values within a tile
-      uint4 af[TN], bf[TM];
-#pragma unroll
-      for (int i = 0; i < TN; ++i) {
-        const int row = wn * TN * 32 + i * 32 + lr;
-        af[i] = ws[(row >> 4) * 64 + (row & 15) + q];
-      }
-#pragma unroll
-      for (int j = 0; j < TM; ++j) {
-        const int row = wm * TM * 32 + j * 32 + lr;
-        bf[j] = xs[(row >> 4) * 64 + (row & 15) + q];
-      }
-#pragma unroll
-      for (int i = 0; i < TN; ++i)
-#pragma unroll
-        for (int j = 0; j < TM; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
-    }
+    read_frags(kt + 1, 0, a0, b0);
+    mfmas(a1, b1);
   }
+  read_frags(nk - 1, 1, a1, b1);
+  mfmas(a0, b0);
+  mfmas(a1, b1);
+  mfma_drain();
 
   // Fully unrolled (acc must stay in registers).  With KS > 1 the slice sums
   // go to part[slice][m][n].  The residual add first loads all 4 * TN float4
