@@ -45,7 +45,10 @@ metro_status metro_op_pack_weight(const uint16_t* W_rowmajor, int32_t ld, int32_
  *      (SwiGLU, Shazeer 2020).
  * workspace: NULL, or device fp32 [8][M][N]; when given, a decode-sized GEMM
  * (M <= 1024, epilogue 0 or 1) may run the k-split form the model uses (slices in
- * the workspace, then summed in slice order into the output).
+ * the workspace, then summed in slice order into the output), and a larger one
+ * (epilogue 0 or 1) may split the 256 x 256 tiles of its last, partly filled
+ * round of workgroups over k the same way.  Its contents on return are
+ * unspecified.
  * Errors: E_INVAL for shapes outside these rules or a NULL operand. */
 metro_status metro_op_gemm(const uint16_t* X, int32_t ldx, const uint16_t* W, int32_t Kp, int32_t M, int32_t N,
                            int32_t epilogue, float* out_f32, uint16_t* out_bf16, int32_t ldo, float* workspace,

@@ -257,11 +257,33 @@ __device__ __forceinline__ void wait_later_stages(int later) {
   }
 }
 
+// Grouped tile order: tiles in launch order sweep groups of kGroupM m-tiles,
+// m fastest within a group, so the ~256 blocks in flight cover a compact
+// patch of tiles and share their W and X tiles through the caches.
+template <class S>
+__host__ __device__ __forceinline__ void tile_origin(int t, int M, int N, int& m0, int& n0) {
+  constexpr int kGroupM = 16;
+  const int mt = (M + S::BM - 1) / S::BM, nt = (N + S::BN - 1) / S::BN;
+  const int group = t / (kGroupM * nt);
+  const int first_m = group * kGroupM;
+  const int gm = min(mt - first_m, kGroupM);
+  const int in = t % (kGroupM * nt);
+  n0 = (in / gm) * S::BN;
+  m0 = (first_m + in % gm) * S::BM;
+}
+
+// Work of one workgroup.  Without a tail split, workgroup (x, y) takes tile x
+// over k slice y of gridDim.y.  With one (tail_split = S > 1), workgroups
+// x < tail_first take tile x over all of K, and the last tiles, which would
+// leave most CUs idle in the final round, are cut into S k slices each:
+// workgroup tail_first + u takes slice u % S of tile tail_first + u / S and
+// stores its fp32 sums to part[u][BM][BN] for gemm_tail_fixup_kernel.
 template <class S, int EPI>
 __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __restrict__ X, int ldx,
                                                             const uint16_t* __restrict__ W, int Kp, int M, int N,
                                                             float* __restrict__ outf, uint16_t* __restrict__ outb,
-                                                            int ldo, float* __restrict__ part) {
+                                                            int ldo, float* __restrict__ part, int tail_first,
+                                                            int tail_split) {
   constexpr int WM = S::WM, TN = S::TN, TM = S::TM, NS = S::NS, LPW = S::LPW;
   __shared__ uint4 wring[NS][S::WT * 64];  // per stage: WT tiles of 16 x 32 (1 KiB each)
   __shared__ uint4 xring[NS][S::XT * 64];
@@ -270,22 +292,18 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
   const int wn = wave / WM, wm = wave % WM;  // the wave's (TN*32) x (TM*32) tile
   const int lr = lane & 31, lh = lane >> 5;
 
-  // k range: slice blockIdx.y of gridDim.y (each a multiple of 128)
-  const int KS = gridDim.y, slice = blockIdx.y;
+  // tile and k range (each slice a multiple of 128)
+  int tile = blockIdx.x, KS = gridDim.y, slice = blockIdx.y, unit = -1;
+  if (tail_split > 1 && tile >= tail_first) {
+    unit = tile - tail_first;
+    tile = tail_first + unit / tail_split;
+    KS = tail_split;
+    slice = unit % tail_split;
+  }
   const int kspan = Kp / KS, k0 = slice * kspan;
   const int nk = kspan / 32;
-
-  // Grouped tile order: blocks in launch order sweep groups of kGroupM m-tiles,
-  // m fastest within a group, so the ~256 blocks in flight cover a compact
-  // patch of tiles and share their W and X tiles through the caches.
-  constexpr int kGroupM = 16;
-  const int mt = (M + S::BM - 1) / S::BM, nt = (N + S::BN - 1) / S::BN;
-  const int b = blockIdx.x;
-  const int group = b / (kGroupM * nt);
-  const int first_m = group * kGroupM;
-  const int gm = min(mt - first_m, kGroupM);
-  const int in = b % (kGroupM * nt);
-  const int n0 = (in / gm) * S::BN, m0 = (first_m + in % gm) * S::BM;
+  int m0, n0;
+  tile_origin<S>(tile, M, N, m0, n0);
 
   // Wave w loads tiles w*LPW .. w*LPW + LPW - 1 of the list [W tiles, X
   // tiles] of every stage.  Rows past N or M re-read the last valid row:
@@ -383,14 +401,19 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
   mfmas(a1, b1);
   mfma_drain();
 
-  // Fully unrolled (acc must stay in registers).  With KS > 1 the slice sums
-  // go to part[slice][m][n].  The residual add first loads all 4 * TN float4
-  // of one 32-row group of activation rows, then adds and stores them (one
-  // round trip per group rather than per value); the scheduling barrier keeps
-  // the compiler from hoisting every group's loads at once.
-  float* const pout = KS > 1 ? part + static_cast<size_t>(slice) * M * N : outf;
-  const int pld = KS > 1 ? N : ldo;
-  if (EPI == kEpiAddF32 && KS == 1) {
+  // Fully unrolled (acc must stay in registers).  Slice sums are stored raw:
+  // to part[slice][m][n] with KS > 1, to part[unit][m - m0][n - n0] for a
+  // tail unit.  The residual add first loads all 4 * TN float4 of one 32-row
+  // group of activation rows, then adds and stores them (one round trip per
+  // group rather than per value); the scheduling barrier keeps the compiler
+  // from hoisting every group's loads at once.
+  const bool raw = KS > 1;
+  float* const pout = unit >= 0 ? part + static_cast<size_t>(unit) * S::BM * S::BN
+                      : raw     ? part + static_cast<size_t>(slice) * M * N
+                                : outf;
+  const int pld = unit >= 0 ? S::BN : raw ? N : ldo;
+  const int om = unit >= 0 ? m0 : 0, on = unit >= 0 ? n0 : 0;  // origin of pout
+  if (EPI == kEpiAddF32 && !raw) {
 #pragma unroll
     for (int j = 0; j < TM; ++j) {
       const int m = m0 + wm * TM * 32 + j * 32 + lr;
@@ -444,8 +467,8 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const f32x4 v{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-          if (KS > 1)
-            store_tile<kEpiStoreF32>(v, m, nb + 8 * q + 4 * lh, pout, pld);
+          if (raw)
+            store_tile<kEpiStoreF32>(v, m - om, nb + 8 * q + 4 * lh - on, pout, pld);
           else
             store_tile<EPI>(v, m, nb + 8 * q + 4 * lh, pout, pld);
           __builtin_amdgcn_sched_barrier(0);
@@ -453,6 +476,33 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
       }
     }
   }
+}
+
+// Tail tiles of a product split by gemm_tiled_kernel: out (=|+=) the sum of
+// each tile's `split` slice sums, added in slice order.  Workgroup (t, y)
+// covers rows 4y .. 4y+3 of tail tile t, a thread 4 consecutive columns.
+template <class S, int EPI>
+__global__ __launch_bounds__(256) void gemm_tail_fixup_kernel(const float* __restrict__ part, int tail_first,
+                                                              int split, int M, int N, float* __restrict__ out,
+                                                              int ldo) {
+  constexpr int kCols = S::BN / 4;  // threads per tile row
+  static_assert(256 % kCols == 0 && S::BM % (256 / kCols) == 0, "rows of a tile split evenly");
+  const int i = blockIdx.y * (256 / kCols) + threadIdx.x / kCols;
+  const int j = 4 * (threadIdx.x % kCols);
+  int m0, n0;
+  tile_origin<S>(tail_first + blockIdx.x, M, N, m0, n0);
+  const int m = m0 + i, n = n0 + j;
+  if (m >= M || n >= N) return;
+  const float* p = part + static_cast<size_t>(blockIdx.x) * split * S::BM * S::BN + i * S::BN + j;
+  float4 a = *reinterpret_cast<const float4*>(p);
+  for (int sl = 1; sl < split; ++sl) {
+    const float4 v = *reinterpret_cast<const float4*>(p + static_cast<size_t>(sl) * S::BM * S::BN);
+    a.x += v.x;
+    a.y += v.y;
+    a.z += v.z;
+    a.w += v.w;
+  }
+  store_tile<EPI>(f32x4{a.x, a.y, a.z, a.w}, m, n, out, ldo);
 }
 
 // ---------------------------------------------------------------------------
@@ -481,12 +531,26 @@ static int gemm_k_splits(int blocks, int target, int M, int Kp) {
   return ks;
 }
 
+// Compute units of the current device (256 on MI355X), cached per device.
+static int device_cus() {
+  static int cache[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
 // Kernel choice, from probes over M = 80 .. 12800 at the Llama-3-8B shapes:
 // the decode kernel up to 64 rows; then 128 x 128 tiles (more blocks, deeper
 // ring) for narrow products and for wide ones up to 192 rows; 256 x 256 tiles
 // for the LM head and for long prefill chunks.
-GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, bool can_split) {
-  GemmPlan p{GemmKind::kBig, 4, 1};
+GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, int64_t part_cap) {
+  GemmPlan p{GemmKind::kBig, 4, 1, 1, 0};
+  const bool can_split = part_cap > 0;
   const bool split = can_split && epilogue != kEpiSwiGLU && M <= kSplitMaxRows;
   if (M <= 64) {
     p.kind = GemmKind::kSkinny;
@@ -505,10 +569,22 @@ GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, bool can_split) {
     const int bn = mid ? MidTile::BN : BigTile::BN, bm = mid ? MidTile::BM : BigTile::BM;
     p.ks = gemm_k_splits(((N + bn - 1) / bn) * ((M + bm - 1) / bm), mid ? 512 : 256, M, Kp);
   }
+  // Last round of 256 x 256 tiles: with r tiles left for C CUs, cut each into
+  // S k slices (S a power of two, r * S <= C, slices multiples of 128), so
+  // that round takes 1/S of a tile's time; the fixup kernel adds the slices.
+  if (p.kind == GemmKind::kBig && p.ks == 1 && can_split && epilogue != kEpiSwiGLU) {
+    const int tiles = ((N + BigTile::BN - 1) / BigTile::BN) * ((M + BigTile::BM - 1) / BigTile::BM);
+    const int cus = device_cus(), r = tiles % cus;
+    int sp = 1;
+    while (r > 0 && sp < 8 && r * (2 * sp) <= cus && (Kp / (2 * sp)) % 128 == 0) sp *= 2;
+    if (sp > 1 && static_cast<int64_t>(r) * sp * BigTile::BM * BigTile::BN <= part_cap) {
+      p.tail_split = sp;
+      p.tail_first = tiles - r;
+    }
+  }
   return p;
 }
 
-int gemm_splits(int M, int N, int Kp, int epilogue) { return plan_gemm(M, N, Kp, epilogue, true).ks; }
 
 template <int MT, int NT, int EPI>
 static void launch_skinny(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, float* outf,
@@ -532,10 +608,17 @@ static void launch_skinny_m(const uint16_t* X, int ldx, const uint16_t* W, int K
 
 template <class S, int EPI>
 static void launch_tiled(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, float* outf,
-                         uint16_t* outb, int ldo, float* part, int ks, hipStream_t s) {
-  const int blocks = ((N + S::BN - 1) / S::BN) * ((M + S::BM - 1) / S::BM);
+                         uint16_t* outb, int ldo, float* part, int ks, hipStream_t s, int tail_split = 1,
+                         int tail_first = 0) {
+  const int tiles = ((N + S::BN - 1) / S::BN) * ((M + S::BM - 1) / S::BM);
+  const int blocks = tail_split > 1 ? tail_first + (tiles - tail_first) * tail_split : tiles;
   launch_kernel((gemm_tiled_kernel<S, EPI>), dim3(blocks, ks), dim3(S::NTH), 0, s, X, ldx, W, Kp, M, N, outf, outb,
-                ldo, part);
+                ldo, part, tail_first, tail_split);
+  if (tail_split > 1) {
+    if constexpr (EPI != kEpiSwiGLU)
+      launch_kernel((gemm_tail_fixup_kernel<S, EPI>), dim3(tiles - tail_first, S::BM / (1024 / S::BN)), dim3(256),
+                    0, s, part, tail_first, tail_split, M, N, outf, ldo);
+  }
 }
 
 template <int EPI>
@@ -554,17 +637,18 @@ static hipError_t launch_epi(const GemmPlan& p, const uint16_t* X, int ldx, cons
       launch_tiled<MidTile, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, p.ks, s);
       break;
     case GemmKind::kBig:
-      launch_tiled<BigTile, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, p.ks, s);
+      launch_tiled<BigTile, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, p.ks, s, p.tail_split, p.tail_first);
       break;
   }
   return hipGetLastError();
 }
 
 hipError_t launch_gemm(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, int epilogue,
-                       float* out_f32, uint16_t* out_bf16, int ldo, float* part, int* n_parts, hipStream_t s) {
+                       float* out_f32, uint16_t* out_bf16, int ldo, float* part, int64_t part_cap, int* n_parts,
+                       hipStream_t s) {
   *n_parts = 0;
   if (M <= 0) return hipSuccess;
-  const GemmPlan p = plan_gemm(M, N, Kp, epilogue, part != nullptr);
+  const GemmPlan p = plan_gemm(M, N, Kp, epilogue, part != nullptr ? part_cap : 0);
   if (p.ks > 1) *n_parts = p.ks;
   switch (epilogue) {
     case kEpiStoreF32:

@@ -85,25 +85,30 @@ enum GemmEpilogue {
 // Y = X[M, Kp] (bf16, row stride ldx) x W[N, Kp]^T (bf16 in MFMA operand
 // order, packed_offset; Kp % 128 == 0, N % 32 == 0), fp32 accumulation, then
 // the epilogue.
-// ldo is the row stride of the output in elements.  With a workspace `part`
-// ([8][M][N] fp32) a decode-sized GEMM (M <= kSplitMaxRows, fp32 epilogue) may split K
-// over workgroups: it then writes *n_parts > 0 slices part[s][m][n] instead of
-// applying the epilogue, and the consumer sums them in slice order.
+// ldo is the row stride of the output in elements.  `part` is an fp32
+// workspace of part_cap floats (or null).  With it a decode-sized GEMM
+// (M <= kSplitMaxRows, fp32 epilogue) may split K over workgroups: it then
+// writes *n_parts > 0 slices part[s][m][n] ([ks][M][N], ks <= 8) instead of
+// applying the epilogue, and the consumer sums them in slice order.  A larger
+// one with 256 x 256 tiles and an fp32 epilogue may split only the tiles of
+// its last, partly filled round (up to CUs * 256 * 256 floats of part), and
+// completes them itself (*n_parts stays 0).
 // Kernel choice: up to 64 rows the weight-streaming decode GEMM; up to
 // kMidMaxRows the tiled GEMM with 128 x 128 blocks, above it 256 x 256 blocks.
-// Both may split K over workgroups (k-slice sums, only for M <= kSplitMaxRows).
 enum class GemmKind { kSkinny, kMid, kBig };
 struct GemmPlan {
   GemmKind kind;
-  int nt;  // row tiles per wave (decode kernel)
-  int ks;  // k slices
+  int nt;          // row tiles per wave (decode kernel)
+  int ks;          // k slices of every tile
+  int tail_split;  // k slices of each tile from tail_first on (1: none)
+  int tail_first;
 };
 constexpr int kMidMaxRows = 1000;
 constexpr int kSplitMaxRows = 1024;
-GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, bool can_split);
+GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, int64_t part_cap);
 hipError_t launch_gemm(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, int epilogue,
-                       float* out_f32, uint16_t* out_bf16, int ldo, float* part, int* n_parts, hipStream_t s);
-int gemm_splits(int M, int N, int Kp, int epilogue);
+                       float* out_f32, uint16_t* out_bf16, int ldo, float* part, int64_t part_cap, int* n_parts,
+                       hipStream_t s);
 // Apply the fp32 epilogue to KS slices: out (=|+=) sum_s part[s].
 hipError_t launch_reduce_parts(const float* part, int KS, int M, int N, int epilogue, float* out, int ldo,
                                hipStream_t s);

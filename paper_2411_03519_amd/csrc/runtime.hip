@@ -83,6 +83,7 @@ struct metro_model {
   float* logits_ws = nullptr;
   int32_t* next_ws = nullptr;
   float* parts = nullptr;    // k-slice sums of decode GEMMs, [8][min(kSplitMaxRows, rows)][max(qkv_n, d)]
+  int64_t parts_cap = 0;     // floats in parts
   float* attn_part = nullptr;  // decode attention split states
   int32_t* desc_dev = nullptr;
   int64_t desc_cap = 0;  // int32 elements
@@ -254,7 +255,7 @@ metro_status launch_layers(metro_model* m, int T, const int32_t* tok_dev, const 
            metro::launch_rmsnorm(m->x, d, L.attn_norm, c.rms_eps, m->h, d, T, d, m->parts, xp, s));
     LAUNCH(m, METRO_K_GEMM_QKV, s,
            metro::launch_gemm(m->h, d, L.wqkv, d, T, m->qkv_n, metro::kEpiStoreF32, m->qkv, nullptr, m->qkv_n,
-                              m->parts, &qp, s));
+                              m->parts, m->parts_cap, &qp, s));
     LAUNCH(m, METRO_K_ROPE_KV, s,
            metro::launch_rope_kv(qp ? m->parts : m->qkv, qp, T, c.n_heads, c.n_kv_heads, c.head_dim, pos, slot,
                                  m->rope, m->q, kv_l, s));
@@ -270,16 +271,16 @@ metro_status launch_layers(metro_model* m, int T, const int32_t* tok_dev, const 
     }
     LAUNCH(m, METRO_K_GEMM_O, s,
            metro::launch_gemm(m->o, m->q_dim, L.wo, m->q_dim, T, d, metro::kEpiAddF32, m->x, nullptr, d, m->parts,
-                              &xp, s));
+                              m->parts_cap, &xp, s));
     LAUNCH(m, METRO_K_RMSNORM, s,
            metro::launch_rmsnorm(m->x, d, L.ffn_norm, c.rms_eps, m->h, d, T, d, m->parts, xp, s));
     int gp = 0;
     LAUNCH(m, METRO_K_GEMM_GATE_UP, s,
            metro::launch_gemm(m->h, d, L.wgu, d, T, 2 * c.ffn_dim, metro::kEpiSwiGLU, nullptr, m->a, m->Fp, nullptr,
-                              &gp, s));
+                              0, &gp, s));
     LAUNCH(m, METRO_K_GEMM_DOWN, s,
-           metro::launch_gemm(m->a, m->Fp, L.wdown, m->Fp, T, d, metro::kEpiAddF32, m->x, nullptr, d, m->parts, &xp,
-                              s));
+           metro::launch_gemm(m->a, m->Fp, L.wdown, m->Fp, T, d, metro::kEpiAddF32, m->x, nullptr, d, m->parts,
+                              m->parts_cap, &xp, s));
   }
   *x_parts = xp;
   return METRO_OK;
@@ -298,7 +299,7 @@ metro_status launch_head(metro_model* m, float* xrows, int R, int x_parts, float
                                x_parts, s));
   LAUNCH(m, METRO_K_LM_HEAD, s,
          metro::launch_gemm(m->h, c.d_model, m->lm_head, c.d_model, R, c.vocab, metro::kEpiStoreF32, lg, nullptr,
-                            c.vocab, nullptr, &lp, s));
+                            c.vocab, nullptr, 0, &lp, s));
   if (next_tok || !logits) LAUNCH(m, METRO_K_ARGMAX, s, metro::launch_argmax(lg, c.vocab, R, nt, s));
   return METRO_OK;
 }
@@ -422,7 +423,8 @@ metro_status metro_create_model(const metro_config* cfg, uint64_t init_seed, met
     m->xr = cv.take<float>(int64_t(c.max_batch) * d);
     m->logits_ws = cv.take<float>(int64_t(c.max_batch) * V);
     m->next_ws = cv.take<int32_t>(c.max_batch);
-    m->parts = cv.take<float>(8LL * std::min<int64_t>(metro::kSplitMaxRows, Tm) * std::max(m->qkv_n, d));
+    m->parts_cap = 8LL * std::min<int64_t>(metro::kSplitMaxRows, Tm) * std::max(m->qkv_n, d);
+    m->parts = cv.take<float>(m->parts_cap);
     m->attn_part = cv.take<float>(decode_work_capacity(c) * nkv * m->group * (hd + 2));
     m->desc_dev = cv.take<int32_t>(m->desc_cap);
     // the SwiGLU output's padding columns must read as zero
@@ -867,7 +869,8 @@ metro_status metro_op_gemm(const uint16_t* X, int32_t ldx, const uint16_t* W, in
   if ((epilogue == metro::kEpiSwiGLU ? ldo < N / 2 : ldo < N) || ldo % 4)
     return fail(METRO_E_INVAL, "gemm: bad ldo");
   int parts = 0;
-  hipError_t e = metro::launch_gemm(X, ldx, W, Kp, M, N, epilogue, out_f32, out_bf16, ldo, workspace, &parts,
+  hipError_t e = metro::launch_gemm(X, ldx, W, Kp, M, N, epilogue, out_f32, out_bf16, ldo, workspace,
+                                    8LL * M * N, &parts,
                                     static_cast<hipStream_t>(stream));
   if (e == hipSuccess && parts > 0)
     e = metro::launch_reduce_parts(workspace, parts, M, N, epilogue, out_f32, ldo, static_cast<hipStream_t>(stream));

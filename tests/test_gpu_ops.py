@@ -75,13 +75,16 @@ def test_pack_weight_rejects_bad_shapes(metro):
 
 # (M, K, N): decode kernel at M <= 64; above it the tiled kernel with 128 x 128
 # blocks (narrow products up to 1000 rows, wide ones up to 192) or 256 x 256
-# blocks, with or without a k split (plan_gemm)
+# blocks, with or without a k split (plan_gemm); the last two split only the
+# tiles of the last round of workgroups (on 256 CUs) when given a workspace
 GEMM_CASES = [(1, 256, 64), (7, 640, 96), (16, 256, 32), (25, 4096, 512), (33, 768, 160), (64, 384, 1376),
               (65, 256, 160), (200, 1152, 416), (129, 128, 96), (300, 4096, 256), (1100, 384, 160),
               (200, 256, 16384), (70, 128, 65536),
               (129, 1024, 512),      # 128 x 128 tiles, 2 k slices with a workspace
               (300, 4096, 16384),    # 256 x 256 tiles, 2 k slices with a workspace
-              (600, 2048, 288)]      # 128 x 128 tiles, ragged in both M and N
+              (600, 2048, 288),      # 128 x 128 tiles, ragged in both M and N
+              (1300, 2048, 4096),    # 256 x 256 tiles, 96 in one partial round: with a workspace 2 k slices each
+              (4300, 1024, 4000)]    # 272 ragged 256 x 256 tiles: the 16 past the first round in 8 k slices
 
 
 @pytest.mark.parametrize("M,K,N", GEMM_CASES + [(25, 14336, 512), (3, 1024, 4096)])
