@@ -366,6 +366,10 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
 #pragma unroll
       for (int j = 0; j < TM; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
   };
+  auto mfmas_row = [&](int i, const uint4 (&af)[TN], const uint4 (&bf)[TM]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < TM; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
+  };
 
   // Software pipeline across the barrier: the fragments of the first k half
   // of step kt + 1 are read while the second half of step kt multiplies, so
@@ -392,9 +396,14 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
     __builtin_amdgcn_sched_barrier(0);
     lds_barrier();
     __builtin_amdgcn_sched_barrier(0);
+    // the first row of MFMAs goes ahead of the load issue, so the matrix pipe
+    // is fed while the wave computes addresses
+    mfmas_row(0, a1, b1);
+    __builtin_amdgcn_sched_barrier(0);
     if (kt + NS - 1 < nk) issue(kt + NS - 1);
     read_frags(kt + 1, 0, a0, b0);
-    mfmas(a1, b1);
+#pragma unroll
+    for (int i = 1; i < TN; ++i) mfmas_row(i, a1, b1);
   }
   read_frags(nk - 1, 1, a1, b1);
   mfmas(a0, b0);
