@@ -133,7 +133,8 @@ __global__ __launch_bounds__(64) void rope_kv_kernel(const float* __restrict__ q
   if (j >= half) return;
   const int sl = slot[t];
   const int page = sl / kPage, off = sl % kPage;
-  const float a = val(j), b = val(j + half);
+  // columns of a head come in the rotate-half interleave of its W rows
+  const float a = val(rope_pair_row(j, half)), b = val(rope_pair_row(j + half, half));
   if (head < nq + nkv) {
     const float2 c = rope[static_cast<size_t>(pos[t]) * half + j];
     const uint16_t ra = f32_to_bf16(a * c.x - b * c.y);
@@ -246,9 +247,7 @@ __device__ __forceinline__ uint64_t splitmix64(uint64_t z) {
 }
 
 __global__ __launch_bounds__(256) void init_normal_kernel(uint16_t* __restrict__ dst, int64_t ld, int rows,
-                                                          int cols, int row_group, int row_block, int row_shift,
-                                                          uint64_t key,
-                                                          bool packed) {
+                                                          int cols, RowMap map, uint64_t key, bool packed) {
   const int64_t n = static_cast<int64_t>(rows) * cols;
   for (int64_t e = blockIdx.x * 256ll + threadIdx.x; e < n; e += static_cast<int64_t>(gridDim.x) * 256) {
     const int r = static_cast<int>(e / cols), c = static_cast<int>(e % cols);
@@ -256,30 +255,28 @@ __global__ __launch_bounds__(256) void init_normal_kernel(uint16_t* __restrict__
     const float u1 = (static_cast<float>(h >> 40) + 1.0f) * (1.0f / 16777216.0f);  // (0, 1]
     const float u2 = static_cast<float>((h >> 16) & 0xffffffull) * (1.0f / 16777216.0f);  // [0, 1)
     const float z = sqrtf(-2.0f * logf(u1)) * cosf(6.283185307179586f * u2);
-    const int64_t pr = static_cast<int64_t>(r / row_group) * row_block + row_shift + (r % row_group);
+    const int64_t pr = map_row(map, r);
     dst[packed ? packed_offset(pr, c, ld) : pr * ld + c] = f32_to_bf16(0.02f * z);
   }
 }
 
-hipError_t launch_init_normal(uint16_t* dst, int64_t ld, int rows, int cols, int row_group, int row_block,
-                              int row_shift, uint64_t key, bool packed, hipStream_t s) {
+hipError_t launch_init_normal(uint16_t* dst, int64_t ld, int rows, int cols, RowMap map, uint64_t key, bool packed,
+                              hipStream_t s) {
   const int64_t n = static_cast<int64_t>(rows) * cols;
   const int64_t blocks = (n + 255) / 256;
   const int grid = static_cast<int>(blocks < 65536 ? blocks : 65536);
-  launch_kernel(init_normal_kernel, dim3(grid), dim3(256), 0, s, dst, ld, rows, cols, row_group, row_block,
-                row_shift, key, packed);
+  launch_kernel(init_normal_kernel, dim3(grid), dim3(256), 0, s, dst, ld, rows, cols, map, key, packed);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
 // Row-major bf16 weight -> MFMA operand order (packed_offset): one thread per
 // 8-element chunk (row r, k .. k+7) of the destination's Kp columns, logical
-// row r going to row (r/row_group)*row_block + row_shift + r%row_group; k >= cols
-// is zero.
+// row r going to row map_row(map, r); k >= cols is zero.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void pack_weight_kernel(const uint16_t* __restrict__ src, int64_t ld_src,
                                                           int rows, int cols, uint16_t* __restrict__ dst, int Kp,
-                                                          int row_group, int row_block, int row_shift) {
+                                                          RowMap map) {
   const int kc = Kp / 8;
   const int64_t n = static_cast<int64_t>(rows) * kc;
   for (int64_t e = blockIdx.x * 256ll + threadIdx.x; e < n; e += static_cast<int64_t>(gridDim.x) * 256) {
@@ -287,7 +284,7 @@ __global__ __launch_bounds__(256) void pack_weight_kernel(const uint16_t* __rest
     uint16_t v[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) v[j] = k + j < cols ? src[r * ld_src + k + j] : 0;
-    const int64_t pr = static_cast<int64_t>(r / row_group) * row_block + row_shift + (r % row_group);
+    const int64_t pr = map_row(map, r);
     uint4 o;
     o.x = v[0] | (static_cast<uint32_t>(v[1]) << 16);
     o.y = v[2] | (static_cast<uint32_t>(v[3]) << 16);
@@ -298,12 +295,12 @@ __global__ __launch_bounds__(256) void pack_weight_kernel(const uint16_t* __rest
 }
 
 hipError_t launch_pack_weight(const uint16_t* src, int64_t ld_src, int rows, int cols, uint16_t* dst, int Kp,
-                              int row_group, int row_block, int row_shift, hipStream_t s) {
+                              RowMap map, hipStream_t s) {
   const int64_t n = static_cast<int64_t>(rows) * (Kp / 8);
   if (n <= 0) return hipSuccess;
   const int64_t blocks = (n + 255) / 256;
   launch_kernel(pack_weight_kernel, dim3(static_cast<int>(blocks < 65536 ? blocks : 65536)), dim3(256), 0, s, src,
-                ld_src, rows, cols, dst, Kp, row_group, row_block, row_shift);
+                ld_src, rows, cols, dst, Kp, map);
   return hipGetLastError();
 }
 

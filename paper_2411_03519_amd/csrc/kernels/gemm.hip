@@ -12,6 +12,7 @@
 // 16 x 32 tile of W is 1 KiB, lane l's 16 bytes at offset 16l, so a wave
 // loading an A operand from HBM issues one contiguous 1 KiB read.
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -61,11 +62,47 @@ __device__ __forceinline__ void store_swiglu(f32x4 gt, f32x4 up, int m, int j, u
 // KS > 1 the slice sums go to part[slice][m][n] and the consumer kernel adds
 // the slices (in slice order) where it reads the result.
 // ---------------------------------------------------------------------------
+// q / k / v of one row for dims d0 .. d0+3 (a) and d0+half .. (b) of a head
+// whose features start at column f0 of the QKV product
+__device__ __forceinline__ void store_rope_kv(f32x4 a, f32x4 b, int m, int head, int d0, const RopeKV& rk) {
+  const int hd = rk.hd, half = hd / 2;
+  const int sl = rk.slot[m], page = sl / kPage, off = sl % kPage;
+  if (head < rk.nq + rk.nkv) {
+    const float2* c = rk.rope + static_cast<size_t>(rk.pos[m]) * half + d0;
+    f32x4 ra, rb;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float2 cs = c[i];
+      ra[i] = a[i] * cs.x - b[i] * cs.y;
+      rb[i] = a[i] * cs.y + b[i] * cs.x;
+    }
+    if (head < rk.nq) {
+      uint16_t* dst = rk.q + (static_cast<size_t>(m) * rk.nq + head) * hd;
+      *reinterpret_cast<uint2*>(dst + d0) = make_uint2(pack_bf16x2(ra[0], ra[1]), pack_bf16x2(ra[2], ra[3]));
+      *reinterpret_cast<uint2*>(dst + d0 + half) = make_uint2(pack_bf16x2(rb[0], rb[1]), pack_bf16x2(rb[2], rb[3]));
+    } else {
+      uint16_t* kt = rk.kv + kv_offset(page, 0, rk.nkv, head - rk.nq, 0, hd, 0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        kt[k_tile_offset(off, d0 + i)] = f32_to_bf16(ra[i]);
+        kt[k_tile_offset(off, d0 + i + half)] = f32_to_bf16(rb[i]);
+      }
+    }
+  } else {
+    uint16_t* vt = rk.kv + kv_offset(page, 1, rk.nkv, head - rk.nq - rk.nkv, 0, hd, 0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      vt[vt_tile_offset(d0 + i, off)] = f32_to_bf16(a[i]);
+      vt[vt_tile_offset(d0 + i + half, off)] = f32_to_bf16(b[i]);
+    }
+  }
+}
+
 template <int MT, int NT, int EPI, int PF, int NW>
 __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const uint16_t* __restrict__ X, int ldx,
                                                               const uint16_t* __restrict__ W, int Kp, int M, int N,
                                                               float* __restrict__ outf, uint16_t* __restrict__ outb,
-                                                              int ldo, float* __restrict__ part) {
+                                                              int ldo, float* __restrict__ part, RopeKV rk) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r = lane & 15, g = lane >> 4;
   const int n0 = blockIdx.x * 16 * NT;
@@ -159,6 +196,26 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const uint16_t* __
       const int nt = t / MT, mt = t % MT;
       const int m = mt * 16 + m_lane;
       if (lane < 32 && m < M) store_swiglu(gt, up, m, 8 * (n0 / 16 + nt) + n_lane, outb, ldo);
+    }
+  } else if (EPI == kEpiRopeKV) {
+    // Tile nt holds dims 8j .. 8j+7 (rows 0..7) and the matching dims of the
+    // head's second half (rows 8..15) of one head, j = its 16-row tile within
+    // the head: as for SwiGLU, a 32-lane swap brings each pair together.
+    for (int t = wave; t < NT * MT; t += NW) {
+      f32x4 sum = red[0][t][lane];
+#pragma unroll
+      for (int w = 1; w < NW; ++w) sum += red[w][t][lane];
+      f32x4 a, b;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const auto pr = __builtin_amdgcn_permlane32_swap(__float_as_uint(sum[i]), __float_as_uint(sum[i]), false, false);
+        a[i] = __uint_as_float(pr[0]);  // dim d (lane l % 32)
+        b[i] = __uint_as_float(pr[1]);  // dim d + hd/2 (lane l % 32 + 32)
+      }
+      const int nt = t / MT, mt = t % MT;
+      const int m = mt * 16 + m_lane;
+      const int f0 = n0 + nt * 16;
+      if (lane < 32 && m < M) store_rope_kv(a, b, m, f0 / rk.hd, 8 * ((f0 % rk.hd) / 16) + n_lane, rk);
     }
   } else {
     for (int t = wave; t < NT * MT; t += NW) {
@@ -601,7 +658,7 @@ static void launch_skinny(const uint16_t* X, int ldx, const uint16_t* W, int Kp,
   // 7 row tiles: 4 waves, so that the cross-wave reduction buffer fits in LDS
   constexpr int NW = NT == 7 ? 4 : kSkinnyWaves;
   launch_kernel((gemm_skinny_kernel<MT, NT, EPI, kSkinnyPF, NW>), dim3(N / (16 * NT), ks), dim3(NW * 64), 0, s, X,
-                ldx, W, Kp, M, N, outf, outb, ldo, part);
+                ldx, W, Kp, M, N, outf, outb, ldo, part, RopeKV{});
 }
 
 template <int NT, int EPI>
@@ -669,6 +726,28 @@ hipError_t launch_gemm(const uint16_t* X, int ldx, const uint16_t* W, int Kp, in
     default:
       return hipErrorInvalidValue;
   }
+}
+
+// 2 row tiles per wave, 4 waves, K whole: 14.4 us at M=25, N=6144, K=4096
+// (with 4 k slices the product alone takes 13.1 us, but the slice sums then
+// cost a RoPE kernel of 5.2 us)
+hipError_t launch_gemm_rope_kv(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, const RopeKV& rk,
+                               hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (M > kRopeKVMaxRows || N != (rk.nq + 2 * rk.nkv) * rk.hd || rk.hd % 32 || N % 32) return hipErrorInvalidValue;
+  constexpr int NT = 2, NW = 4;
+  auto go = [&](auto mt) {
+    constexpr int MT = decltype(mt)::value;
+    launch_kernel((gemm_skinny_kernel<MT, NT, kEpiRopeKV, kSkinnyPF, NW>), dim3(N / (16 * NT), 1), dim3(NW * 64), 0,
+                  s, X, ldx, W, Kp, M, N, nullptr, nullptr, 0, nullptr, rk);
+  };
+  if (M <= 16)
+    go(std::integral_constant<int, 1>{});
+  else if (M <= 32)
+    go(std::integral_constant<int, 2>{});
+  else
+    go(std::integral_constant<int, 4>{});
+  return hipGetLastError();
 }
 
 hipError_t launch_reduce_parts(const float* part, int KS, int M, int N, int epilogue, float* out, int ldo,

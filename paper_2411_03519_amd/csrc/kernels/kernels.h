@@ -54,18 +54,44 @@ hipError_t launch_gather_rows(const float* x, int d, const int32_t* rows, int n,
 // non-NaN value.
 hipError_t launch_argmax(const float* logits, int vocab, int rows, int32_t* out, hipStream_t s);
 
-// Random initialisation of one logical weight tensor [rows, cols]: logical
-// row r goes to row map(r) = (r / row_group) * row_block + row_shift +
-// r % row_group of the destination, which is row-major with row stride ld,
-// or, with packed, in MFMA operand order (packed_offset) with ld = Kp.  Values
-// are 0.02 * N(0, 1) from a SplitMix64-keyed Box-Muller draw, rounded to bf16.
-hipError_t launch_init_normal(uint16_t* dst, int64_t ld, int rows, int cols, int row_group, int row_block,
-                              int row_shift, uint64_t key, bool packed, hipStream_t s);
+// Row placement of a weight matrix in its packed buffer: source row r goes to
+// row map_row(m, r).  With half > 0 each head of 2*half rows is first
+// interleaved for the rotate-half RoPE: blocks of 8 rows of the head's first
+// half, each followed by the 8 matching rows of its second half, so that dims
+// d and d + half meet in lanes l and l + 32 of a 16-row MFMA tile (half % 8
+// == 0).  Then rows go in groups of `group` to blocks of `block` rows, offset
+// by `shift` (gate/up: groups of 8 into blocks of 16, the up rows shifted by 8).
+struct RowMap {
+  int group, block, shift, half;
+};
+constexpr RowMap kRowsInOrder{16, 16, 0, 0};
 
-// Row-major bf16 [rows, cols] (row stride ld_src, device) -> rows map(r) (as
-// above) of a packed [*, Kp] weight; columns cols .. Kp-1 are written as zero.
+// row of dim d (0 <= d < 2*half) of a head in the rotate-half interleave
+__host__ __device__ __forceinline__ int rope_pair_row(int d, int half) {
+  const int e = d < half ? d : d - half;
+  return (e / 8) * 16 + (d < half ? 0 : 8) + e % 8;
+}
+
+__host__ __device__ __forceinline__ int64_t map_row(const RowMap& m, int64_t r) {
+  if (m.half > 0) {
+    const int64_t hd = 2 * m.half, d = r % hd;
+    r = r - d + rope_pair_row(static_cast<int>(d), m.half);
+  }
+  return (r / m.group) * m.block + m.shift + r % m.group;
+}
+
+// Random initialisation of one logical weight tensor [rows, cols]: logical
+// row r goes to row map_row(map, r) of the destination, which is row-major
+// with row stride ld, or, with packed, in MFMA operand order (packed_offset)
+// with ld = Kp.  Values are 0.02 * N(0, 1) from a SplitMix64-keyed Box-Muller
+// draw, rounded to bf16.
+hipError_t launch_init_normal(uint16_t* dst, int64_t ld, int rows, int cols, RowMap map, uint64_t key, bool packed,
+                              hipStream_t s);
+
+// Row-major bf16 [rows, cols] (row stride ld_src, device) -> rows map_row(map, r)
+// of a packed [*, Kp] weight; columns cols .. Kp-1 are written as zero.
 hipError_t launch_pack_weight(const uint16_t* src, int64_t ld_src, int rows, int cols, uint16_t* dst, int Kp,
-                              int row_group, int row_block, int row_shift, hipStream_t s);
+                              RowMap map, hipStream_t s);
 hipError_t launch_fill_bf16(uint16_t* dst, int64_t n, uint16_t value, hipStream_t s);
 
 // Copy page src to page dst in every layer (page_elems bf16 per layer).
@@ -80,6 +106,19 @@ enum GemmEpilogue {
   kEpiSwiGLU = 2,    // W rows in blocks of 16 = 8 gate rows, then the 8 up
                      // rows of the same features:
                      // out_bf16[m, j] = bf16(silu(gate_j) * up_j), N = 2 * F
+  kEpiRopeKV = 3,    // QKV projection with W rows in the rotate-half
+                     // interleave of RowMap: RoPE on q and k, q to its
+                     // buffer, k and v to the row's KV cache slot
+};
+
+// Where the QKV epilogue puts its results (launch_gemm_rope_kv).
+struct RopeKV {
+  const int32_t* pos;   // [M] position of each row
+  const int32_t* slot;  // [M] KV cache slot of each row (page * 16 + offset)
+  const float2* rope;   // [max_context][hd / 2] (cos, sin)
+  uint16_t* q;          // [M, nq, hd] bf16, rotated
+  uint16_t* kv;         // this layer's slab of the KV pool
+  int nq, nkv, hd;
 };
 
 // Y = X[M, Kp] (bf16, row stride ldx) x W[N, Kp]^T (bf16 in MFMA operand
@@ -109,6 +148,12 @@ GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, int64_t part_cap);
 hipError_t launch_gemm(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, int epilogue,
                        float* out_f32, uint16_t* out_bf16, int ldo, float* part, int64_t part_cap, int* n_parts,
                        hipStream_t s);
+// QKV projection of at most kRopeKVMaxRows rows (N = (nq + 2 nkv) * hd) with
+// RoPE and the KV cache write in its epilogue, in place of launch_gemm +
+// launch_rope_kv; K is not split, so no slice sums are left.
+constexpr int kRopeKVMaxRows = 64;
+hipError_t launch_gemm_rope_kv(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, const RopeKV& rk,
+                               hipStream_t s);
 // Apply the fp32 epilogue to KS slices: out (=|+=) sum_s part[s].
 hipError_t launch_reduce_parts(const float* part, int KS, int M, int N, int epilogue, float* out, int ldo,
                                hipStream_t s);

@@ -253,12 +253,17 @@ metro_status launch_layers(metro_model* m, int T, const int32_t* tok_dev, const 
     uint16_t* kv_l = m->kv + static_cast<size_t>(l) * m->layer_stride;
     LAUNCH(m, METRO_K_RMSNORM, s,
            metro::launch_rmsnorm(m->x, d, L.attn_norm, c.rms_eps, m->h, d, T, d, m->parts, xp, s));
-    LAUNCH(m, METRO_K_GEMM_QKV, s,
-           metro::launch_gemm(m->h, d, L.wqkv, d, T, m->qkv_n, metro::kEpiStoreF32, m->qkv, nullptr, m->qkv_n,
-                              m->parts, m->parts_cap, &qp, s));
-    LAUNCH(m, METRO_K_ROPE_KV, s,
-           metro::launch_rope_kv(qp ? m->parts : m->qkv, qp, T, c.n_heads, c.n_kv_heads, c.head_dim, pos, slot,
-                                 m->rope, m->q, kv_l, s));
+    if (T <= metro::kRopeKVMaxRows) {
+      const metro::RopeKV rk{pos, slot, m->rope, m->q, kv_l, c.n_heads, c.n_kv_heads, c.head_dim};
+      LAUNCH(m, METRO_K_GEMM_QKV, s, metro::launch_gemm_rope_kv(m->h, d, L.wqkv, d, T, m->qkv_n, rk, s));
+    } else {
+      LAUNCH(m, METRO_K_GEMM_QKV, s,
+             metro::launch_gemm(m->h, d, L.wqkv, d, T, m->qkv_n, metro::kEpiStoreF32, m->qkv, nullptr, m->qkv_n,
+                                m->parts, m->parts_cap, &qp, s));
+      LAUNCH(m, METRO_K_ROPE_KV, s,
+             metro::launch_rope_kv(qp ? m->parts : m->qkv, qp, T, c.n_heads, c.n_kv_heads, c.head_dim, pos, slot,
+                                   m->rope, m->q, kv_l, s));
+    }
     if (dec) {
       metro::AttnArgs a = *dec;
       a.kv = kv_l;
@@ -486,22 +491,24 @@ metro_status metro_create_model(const metro_config* cfg, uint64_t init_seed, met
     auto chk = [&](hipError_t x) {
       if (r == hipSuccess) r = x;
     };
-    chk(metro::launch_init_normal(m->embed, d, V, d, 16, 16, 0, key(METRO_W_EMBED, -1), false, 0));
-    chk(metro::launch_init_normal(m->lm_head, d, V, d, 16, 16, 0, key(METRO_W_LM_HEAD, -1), true, 0));
+    const metro::RowMap in_order = metro::kRowsInOrder;
+    const int half = hd / 2;  // QKV rows: rotate-half interleave per head
+    chk(metro::launch_init_normal(m->embed, d, V, d, in_order, key(METRO_W_EMBED, -1), false, 0));
+    chk(metro::launch_init_normal(m->lm_head, d, V, d, in_order, key(METRO_W_LM_HEAD, -1), true, 0));
     chk(metro::launch_fill_bf16(m->final_norm, d, one, 0));
     for (int l = 0; l < c.n_layers; ++l) {
       Layer& L = m->layers[l];
       chk(metro::launch_fill_bf16(L.attn_norm, d, one, 0));
       chk(metro::launch_fill_bf16(L.ffn_norm, d, one, 0));
-      chk(metro::launch_init_normal(L.wqkv, d, m->q_dim, d, 16, 16, 0, key(METRO_W_WQ, l), true, 0));
-      chk(metro::launch_init_normal(L.wqkv, d, m->kv_dim, d, 16, 16, m->q_dim, key(METRO_W_WK, l), true, 0));
-      chk(metro::launch_init_normal(L.wqkv, d, m->kv_dim, d, 16, 16, m->q_dim + m->kv_dim, key(METRO_W_WV, l), true,
-                                    0));
-      chk(metro::launch_init_normal(L.wo, m->q_dim, d, m->q_dim, 16, 16, 0, key(METRO_W_WO, l), true, 0));
-      chk(metro::launch_init_normal(L.wgu, d, F, d, 8, 16, 0, key(METRO_W_WGATE, l), true, 0));
-      chk(metro::launch_init_normal(L.wgu, d, F, d, 8, 16, 8, key(METRO_W_WUP, l), true, 0));
+      chk(metro::launch_init_normal(L.wqkv, d, m->q_dim, d, {16, 16, 0, half}, key(METRO_W_WQ, l), true, 0));
+      chk(metro::launch_init_normal(L.wqkv, d, m->kv_dim, d, {16, 16, m->q_dim, half}, key(METRO_W_WK, l), true, 0));
+      chk(metro::launch_init_normal(L.wqkv, d, m->kv_dim, d, {16, 16, m->q_dim + m->kv_dim, half},
+                                    key(METRO_W_WV, l), true, 0));
+      chk(metro::launch_init_normal(L.wo, m->q_dim, d, m->q_dim, in_order, key(METRO_W_WO, l), true, 0));
+      chk(metro::launch_init_normal(L.wgu, d, F, d, {8, 16, 0, 0}, key(METRO_W_WGATE, l), true, 0));
+      chk(metro::launch_init_normal(L.wgu, d, F, d, {8, 16, 8, 0}, key(METRO_W_WUP, l), true, 0));
       if (m->Fp != F) chk(metro::launch_fill_bf16(L.wdown, static_cast<int64_t>(d) * m->Fp, 0, 0));
-      chk(metro::launch_init_normal(L.wdown, m->Fp, d, F, 16, 16, 0, key(METRO_W_WDOWN, l), true, 0));
+      chk(metro::launch_init_normal(L.wdown, m->Fp, d, F, in_order, key(METRO_W_WDOWN, l), true, 0));
     }
     if (r == hipSuccess) r = hipDeviceSynchronize();
     if (r != hipSuccess) return bail(hip_fail(nullptr, r, "weight initialisation"));
@@ -529,9 +536,9 @@ metro_status metro_load_weight(metro_model* m, int32_t id, int32_t layer, const 
   if (!global && (layer < 0 || layer >= c.n_layers)) return fail(METRO_E_INVAL, "layer %d out of range", layer);
   HIP_TRY(m, hipSetDevice(m->device));
   // destination: (base, rows, cols, dst row stride); logical row r goes to
-  // row (r / grp) * blk + shift + r % grp
+  // row map_row({grp, 16, shift, half}, r)
   uint16_t* base = nullptr;
-  int64_t rows = 0, cols = 0, ld = 0, grp = 16, blk = 16, shift = 0;
+  int64_t rows = 0, cols = 0, ld = 0, grp = 16, shift = 0, half = 0;
   const Layer* L = global ? nullptr : &m->layers[layer];
   switch (id) {
     case METRO_W_EMBED: base = m->embed; rows = V; cols = d; break;
@@ -539,9 +546,15 @@ metro_status metro_load_weight(metro_model* m, int32_t id, int32_t layer, const 
     case METRO_W_FINAL_NORM: base = m->final_norm; rows = 1; cols = d; break;
     case METRO_W_ATTN_NORM: base = L->attn_norm; rows = 1; cols = d; break;
     case METRO_W_FFN_NORM: base = L->ffn_norm; rows = 1; cols = d; break;
-    case METRO_W_WQ: base = L->wqkv; rows = m->q_dim; cols = d; break;
-    case METRO_W_WK: base = L->wqkv; rows = m->kv_dim; cols = d; shift = m->q_dim; break;
-    case METRO_W_WV: base = L->wqkv; rows = m->kv_dim; cols = d; shift = m->q_dim + m->kv_dim; break;
+    case METRO_W_WQ: base = L->wqkv; rows = m->q_dim; cols = d; half = c.head_dim / 2; break;
+    case METRO_W_WK: base = L->wqkv; rows = m->kv_dim; cols = d; shift = m->q_dim; half = c.head_dim / 2; break;
+    case METRO_W_WV:
+      base = L->wqkv;
+      rows = m->kv_dim;
+      cols = d;
+      shift = m->q_dim + m->kv_dim;
+      half = c.head_dim / 2;
+      break;
     case METRO_W_WO: base = L->wo; rows = d; cols = m->q_dim; break;
     case METRO_W_WGATE: base = L->wgu; rows = F; cols = d; grp = 8; break;
     case METRO_W_WUP: base = L->wgu; rows = F; cols = d; grp = 8; shift = 8; break;
@@ -562,8 +575,9 @@ metro_status metro_load_weight(metro_model* m, int32_t id, int32_t layer, const 
   hipError_t e = hipMemcpy(stage, src, rows * cols * 2, hipMemcpyHostToDevice);
   if (e == hipSuccess)
     e = metro::launch_pack_weight(stage, cols, static_cast<int>(rows), static_cast<int>(cols), base,
-                                  static_cast<int>(ld), static_cast<int>(grp), static_cast<int>(blk),
-                                  static_cast<int>(shift), nullptr);
+                                  static_cast<int>(ld),
+                                  {static_cast<int>(grp), 16, static_cast<int>(shift), static_cast<int>(half)},
+                                  nullptr);
   if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
   (void)hipFree(stage);
   if (e != hipSuccess) return hip_fail(m, e, "weight upload");
@@ -854,7 +868,8 @@ metro_status metro_op_pack_weight(const uint16_t* W_rowmajor, int32_t ld, int32_
   if (!W_rowmajor || !W_packed || N <= 0 || N % 16 || Kp <= 0 || Kp % 128 || K <= 0 || K > Kp || ld < K)
     return fail(METRO_E_INVAL, "pack_weight: bad shape (N %% 16, Kp %% 128, 0 < K <= Kp, ld >= K required)");
   hipError_t e =
-      metro::launch_pack_weight(W_rowmajor, ld, N, K, W_packed, Kp, 16, 16, 0, static_cast<hipStream_t>(stream));
+      metro::launch_pack_weight(W_rowmajor, ld, N, K, W_packed, Kp, metro::kRowsInOrder,
+                                static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(nullptr, e, "launch_pack_weight");
   return METRO_OK;
 }
