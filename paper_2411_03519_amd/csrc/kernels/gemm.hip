@@ -282,7 +282,9 @@ __global__ __launch_bounds__(256) void reduce_parts_kernel(const float* __restri
 // Tile shapes: WN x WM waves, each TN x TM tiles of 32 x 32, NS stages of
 // 32-wide k in the LDS ring.  Big: 256 x 256 blocks for long prefill chunks.
 // Mid: 128 x 128 blocks and a deeper ring for batches of a few hundred rows,
-// where there are few blocks and the weight stream must keep more in flight.
+// where there are few blocks and the weight stream must keep more in flight;
+// 8 waves of 32 x 64 (two per SIMD) ran 20-40% faster there than 4 waves of
+// 32 x 128 (one per SIMD), whose MFMA pipe idles at every barrier and LDS wait.
 template <int WN_, int WM_, int TN_, int TM_, int NS_>
 struct TileShape {
   static constexpr int WN = WN_, WM = WM_, TN = TN_, TM = TM_, NS = NS_;
@@ -294,7 +296,7 @@ struct TileShape {
   static_assert(NS >= 3, "the pipeline keeps a stage in use, one landed and loads in flight");
 };
 using BigTile = TileShape<4, 2, 2, 4, 5>;
-using MidTile = TileShape<4, 1, 1, 4, 8>;
+using MidTile = TileShape<4, 2, 1, 2, 8>;
 
 __device__ __forceinline__ f32x16 mfma32(uint4 a, uint4 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
@@ -589,11 +591,13 @@ static int skinny_tiles(int N, int Kp, int epilogue) {
 }
 
 // Workgroups split K while fewer than `target` cover the product; slices stay
-// multiples of 128, and the slice sums (ks * M * N fp32) never exceed the
-// weight bytes (N * Kp bf16), i.e. 2 * ks * M <= Kp.
+// multiples of 128, and the slice sums (ks * M * N fp32, written and read
+// again) stay within a quarter of the weight bytes (N * Kp bf16), i.e.
+// 8 * ks * M <= Kp: probes at M = 128..512 over the 8B and 70B shapes found
+// the best split there (8B QKV at M=256: 8 slices 49.8 us, 2 slices 35.5 us).
 static int gemm_k_splits(int blocks, int target, int M, int Kp) {
   int ks = 1;
-  while (blocks * ks < target && ks < 8 && (Kp / (2 * ks)) % 128 == 0 && 2 * (2 * ks) * M <= Kp) ks *= 2;
+  while (blocks * ks < target && ks < 8 && (Kp / (2 * ks)) % 128 == 0 && 8 * (2 * ks) * M <= Kp) ks *= 2;
   return ks;
 }
 
@@ -610,10 +614,12 @@ static int device_cus() {
   return cache[dev];
 }
 
-// Kernel choice, from probes over M = 80 .. 12800 at the Llama-3-8B shapes:
-// the decode kernel up to 64 rows; then 128 x 128 tiles (more blocks, deeper
-// ring) for narrow products and for wide ones up to 192 rows; 256 x 256 tiles
-// for the LM head and for long prefill chunks.
+// Kernel choice, from probes over M = 80 .. 12800 at the Llama-3-8B and 70B
+// shapes: the decode kernel up to 64 rows; then 128 x 128 tiles (more blocks,
+// deeper ring) for narrow products, and for wide ones up to 192 rows while
+// their tiles fit one round of the CUs (70B gate/up at M=128: 448 such tiles,
+// 271 us; 224 of 256 x 256, 231 us); 256 x 256 tiles for the LM head and for
+// long prefill chunks.
 GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, int64_t part_cap) {
   GemmPlan p{GemmKind::kBig, 4, 1, 1, 0};
   const bool can_split = part_cap > 0;
@@ -624,10 +630,11 @@ GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, int64_t part_cap) {
     if (split) p.ks = gemm_k_splits(N / (16 * p.nt), p.nt == 2 ? 512 : 256, M, Kp);
     return p;
   }
+  const int mid_tiles = ((N + MidTile::BN - 1) / MidTile::BN) * ((M + MidTile::BM - 1) / MidTile::BM);
   if (N >= 65536)
     p.kind = GemmKind::kBig;
-  else if (N >= 16384)
-    p.kind = M <= 192 ? GemmKind::kMid : GemmKind::kBig;
+  else if (N >= 16384)  // wide products: 128 x 128 tiles only while they fit one round of the CUs
+    p.kind = M <= 192 && mid_tiles <= device_cus() ? GemmKind::kMid : GemmKind::kBig;
   else
     p.kind = M <= kMidMaxRows ? GemmKind::kMid : GemmKind::kBig;
   if (split) {
