@@ -23,6 +23,7 @@ BUILD = os.path.join(ROOT, "_build")
 
 SOURCES = [
     "csrc/kv_pool.cpp",
+    "csrc/scheduler.cpp",
     "csrc/runtime.hip",
     "csrc/kernels/elementwise.hip",
     "csrc/kernels/gemm.hip",

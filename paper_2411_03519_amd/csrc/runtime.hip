@@ -15,6 +15,7 @@
 
 #include "../../include/metro.h"
 #include "../../include/metro_ops.h"
+#include "errors.h"
 #include "kernels/kernels.h"
 #include "kv_pool.h"
 
@@ -53,6 +54,22 @@ struct Layer {
 };
 
 }  // namespace
+
+namespace metro {
+
+metro_status report(metro_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+void clear_error() { g_err.clear(); }
+
+}  // namespace metro
 
 struct metro_model {
   metro_config cfg{};

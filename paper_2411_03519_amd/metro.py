@@ -1,4 +1,4 @@
-"""ctypes binding of libmetro.so (include/metro.h, include/metro_ops.h).
+"""ctypes binding of libmetro.so (include/metro.h, include/metro_ops.h, include/metro_sched.h).
 
 Argument marshalling only: every step of the forward pass runs in the HIP
 library.  PyTorch serves as the source of device buffers (``tensor.data_ptr()``)
@@ -70,6 +70,11 @@ _SIGS = {
     "metro_op_gemm": (_i32, [_vp, _i32, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp]),
     "metro_op_rmsnorm": (_i32, [_vp, _vp, ctypes.c_float, _vp, _i32, _i32, _vp]),
     "metro_op_argmax": (_i32, [_vp, _i32, _i32, _vp, _vp]),
+    "metro_sched_create": (_i32, [_vp, _vp, ctypes.POINTER(_vp)]),
+    "metro_sched_destroy": (None, [_vp]),
+    "metro_sched_next": (_i32, [_vp, ctypes.POINTER(_i32), ctypes.POINTER(_i32), _vp, _i32, ctypes.POINTER(_i32)]),
+    "metro_sched_ack": (_i32, [_vp, _i32, _vp]),
+    "metro_sched_state": (_i32, [_vp, _vp, _vp, _vp, ctypes.POINTER(_i32), ctypes.POINTER(_i32)]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _f = getattr(lib, _name)
@@ -247,3 +252,62 @@ def op_rmsnorm(x, g, eps: float, h, rows: int, d: int, stream=None):
 
 def op_argmax(logits, rows: int, vocab: int, out, stream=None):
     check(lib.metro_op_argmax(_ptr(logits), rows, vocab, _ptr(out), _stream(stream)))
+
+
+# ----------------------------------------------------------------------------
+# Out-of-order agent scheduler (include/metro_sched.h); host only, no device
+# ----------------------------------------------------------------------------
+
+DIST_CHEBYSHEV, DIST_EUCLIDEAN = 0, 1
+
+
+class SchedConfig(ctypes.Structure):
+    _fields_ = [("n_agents", ctypes.c_int32), ("radius_p", ctypes.c_float), ("max_vel", ctypes.c_float),
+                ("metric", ctypes.c_int32), ("target_step", ctypes.c_int32), ("sync", ctypes.c_int32)]
+
+
+class Scheduler:
+    """metro_sched_*: ``next()`` -> (cluster, step, members) or None;
+    ``ack(cluster, positions)`` with each member's new (x, y)."""
+
+    def __init__(self, positions, radius_p: float, max_vel: float, metric: int = DIST_CHEBYSHEV,
+                 target_step: int = 10, sync: bool = False):
+        self._h = ctypes.c_void_p()
+        xy = np.ascontiguousarray(np.asarray(positions, dtype=np.int32).reshape(-1, 2))
+        self.n = xy.shape[0]
+        cfg = SchedConfig(self.n, radius_p, max_vel, metric, target_step, 1 if sync else 0)
+        h = ctypes.c_void_p()
+        check(lib.metro_sched_create(ctypes.byref(cfg), xy.ctypes.data, ctypes.byref(h)))
+        self._h = h
+        self._buf = np.zeros(self.n, dtype=np.int32)
+
+    def close(self):
+        if self._h:
+            lib.metro_sched_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        self.close()
+
+    def next(self, cap: int | None = None):
+        cid, step, n = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+        cap = self.n if cap is None else cap
+        buf = self._buf if cap <= self.n else np.zeros(cap, dtype=np.int32)
+        check(lib.metro_sched_next(self._h, ctypes.byref(cid), ctypes.byref(step), buf.ctypes.data, cap,
+                                    ctypes.byref(n)))
+        if n.value == 0:
+            return None
+        return cid.value, step.value, [int(a) for a in buf[:n.value]]
+
+    def ack(self, cluster: int, positions):
+        xy = np.ascontiguousarray(np.asarray(positions, dtype=np.int32).reshape(-1, 2))
+        check(lib.metro_sched_ack(self._h, cluster, xy.ctypes.data))
+
+    def state(self):
+        steps = np.zeros(self.n, np.int32)
+        xy = np.zeros((self.n, 2), np.int32)
+        st = np.zeros(self.n, np.int32)
+        running, done = ctypes.c_int32(), ctypes.c_int32()
+        check(lib.metro_sched_state(self._h, steps.ctypes.data, xy.ctypes.data, st.ctypes.data,
+                                     ctypes.byref(running), ctypes.byref(done)))
+        return {"steps": steps, "xy": xy, "state": st, "running": running.value, "done": bool(done.value)}

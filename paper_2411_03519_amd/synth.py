@@ -208,3 +208,97 @@ def agent_trace(seed: int = 0, n_agents: int = 1000, grid=(100, 140), radius: in
         pos[idx] = np.clip(pos[idx] + mv, 0, [H - 1, W - 1])
         budget[idx] = new_budget(len(idx))
     return batches
+
+
+# ----------------------------------------------------------------------------
+# Synthetic world for the out-of-order scheduler (inputs only: positions,
+# moves and per-step work, drawn from a counter-based generator so that they
+# do not depend on the order in which a scheduler runs the agents)
+# ----------------------------------------------------------------------------
+
+_M64 = (1 << 64) - 1
+
+
+def splitmix64(z: int) -> int:
+    """SplitMix64 (Steele, Lea & Flood, OOPSLA 2014): one 64-bit output for counter z."""
+    z = (z + 0x9E3779B97F4A7C15) & _M64
+    z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & _M64
+    z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & _M64
+    return z ^ (z >> 31)
+
+
+def agent_draw(seed: int, agent: int, step: int, k: int) -> int:
+    """The k-th 64-bit draw of (agent, step)."""
+    return splitmix64((((seed * 1_000_003 + agent) * 1_000_033 + step) * 16 + k) & _M64)
+
+
+class SimWorld:
+    """Agents on a W x H grid (the paper's world is 100 x 140, §4.2).
+
+    Each agent's step ends with a move to one of the 8 neighbouring cells or
+    staying (4 neighbours for the Euclidean metric, so a move is at most 1),
+    clamped at the border, and costs some LLM work: none with probability
+    p_idle, else ``max(1, round(exp(N(0, sigma))))`` units (a token budget, or
+    ticks of an abstract clock)."""
+
+    def __init__(self, seed: int, n_agents: int, grid=(100, 140), p_idle: float = 0.2, sigma: float = 1.5,
+                 diagonal: bool = True):
+        self.seed, self.n = seed, n_agents
+        self.H, self.W = grid
+        self.p_idle, self.sigma, self.diagonal = p_idle, sigma, diagonal
+        rng = np.random.Generator(np.random.PCG64([seed, 3]))
+        self.start = np.stack([rng.integers(0, self.H, n_agents), rng.integers(0, self.W, n_agents)], axis=1)
+
+    def move(self, agent: int, step: int, pos) -> tuple:
+        h = agent_draw(self.seed, agent, step, 0)
+        if self.diagonal:
+            dx, dy = h % 3 - 1, (h >> 8) % 3 - 1
+        else:
+            dx, dy = ((0, 0), (1, 0), (-1, 0), (0, 1), (0, -1))[h % 5]
+        return (min(max(int(pos[0]) + dx, 0), self.H - 1), min(max(int(pos[1]) + dy, 0), self.W - 1))
+
+    def work(self, agent: int, step: int) -> int:
+        h1, h2, h3 = (agent_draw(self.seed, agent, step, k) for k in (1, 2, 3))
+        if (h1 >> 11) * 2.0 ** -53 < self.p_idle:
+            return 0
+        # Box-Muller on two 53-bit uniforms
+        u1 = ((h2 >> 11) + 1) * 2.0 ** -53
+        u2 = (h3 >> 11) * 2.0 ** -53
+        z = math.sqrt(-2.0 * math.log(u1)) * math.cos(2.0 * math.pi * u2)
+        return max(1, int(round(math.exp(self.sigma * z))))
+
+
+def run_event_sim(sched, world: SimWorld, workers: int | None = None, on_ack=None):
+    """Drive a scheduler (``next()`` -> (cluster, step, members) or None,
+    ``ack(cluster, positions)``) on an abstract clock: a cluster takes as long
+    as its slowest member's work; at most ``workers`` clusters run at once (None:
+    no limit); completions at the same time are acknowledged lowest step first,
+    then in hand-out order (the priority ack queue of §3.5).
+
+    Returns (log, makespan); the log lists ("run" | "ack", time, step, members)."""
+    import heapq
+
+    pos = [tuple(int(v) for v in p) for p in world.start]
+    log, events, t = [], [], 0
+    while True:
+        while workers is None or len(events) < workers:
+            got = sched.next()
+            if got is None:
+                break
+            cid, step, members = got
+            dur = max(world.work(a, step) for a in members)
+            heapq.heappush(events, (t + dur, step, cid, tuple(members)))
+            log.append(("run", t, step, tuple(members)))
+        if not events:
+            break
+        t = events[0][0]
+        while events and events[0][0] == t:
+            _, step, cid, members = heapq.heappop(events)
+            new = [world.move(a, step, pos[a]) for a in members]
+            for a, p in zip(members, new):
+                pos[a] = p
+            sched.ack(cid, new)
+            log.append(("ack", t, step, members))
+            if on_ack is not None:
+                on_ack(sched)
+    return log, t

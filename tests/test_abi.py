@@ -8,7 +8,7 @@ import pytest
 
 def declared_functions(repo_root):
     names = set()
-    for h in ("metro.h", "metro_ops.h"):
+    for h in ("metro.h", "metro_ops.h", "metro_sched.h"):
         text = open(os.path.join(repo_root, "include", h)).read()
         text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
         names |= set(re.findall(r"\b(metro_[a-z_0-9]+)\s*\(", text))
@@ -18,7 +18,7 @@ def declared_functions(repo_root):
 def test_headers_declare_the_entry_points(repo_root):
     names = declared_functions(repo_root)
     for must in ("metro_create_model", "metro_prefill_chunk", "metro_decode_step", "metro_seq_fork",
-                 "metro_op_gemm"):
+                 "metro_op_gemm", "metro_sched_next", "metro_sched_ack"):
         assert must in names
 
 
