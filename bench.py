@@ -311,6 +311,165 @@ def bench_trace(args, torch, metro, synth):
             "roofline": roof, "fixed_batch": fixed}
 
 
+def sched_calls(world, seed, step, agent, vocab):
+    """The LLM call of one agent step: None for an idle step, else (prompt
+    token ids, tokens to generate); prompts lognormal(median 640, sigma 0.5)
+    clipped to [128, 2048] (the paper's calls average 642.6 tokens in and 21.9
+    out, §4.2), 8 output tokens per unit of the step's work, 8..128."""
+    work = world.work(agent, step)
+    if work == 0:
+        return None
+    rng = np.random.Generator(np.random.PCG64([seed, 11, agent, step]))
+    plen = int(np.clip(np.rint(np.exp(rng.normal(np.log(640.0), 0.5))), 128, 2048))
+    return rng.integers(0, vocab, size=plen, dtype=np.int64), int(np.clip(8 * work, 8, 128))
+
+
+def run_sched_loop(model, sched, world, seed, shape, torch, max_batch, chunk=512, group=16):
+    """Closed loop of scheduler and engine: hand-out clusters run one LLM call
+    per agent step (idle steps none); each engine iteration prefills the calls
+    that arrived (chunked, ``group`` calls per prefill call) and then decodes one
+    token for every running call; a cluster is acknowledged, with its agents'
+    moves, when its last call finishes.  Returns wall seconds and counters."""
+    V = shape["vocab"]
+    pos = [tuple(int(v) for v in p) for p in world.start]
+    last = torch.zeros(max_batch + 8, dtype=torch.int32, device="cuda")
+    free_slots = list(range(max_batch + 8))
+    clusters = {}       # cluster -> [step, members, calls still running]
+    arriving, running = [], []   # calls: dict(seq, slot, left, cluster)
+    stats = {"prefill_tokens": 0, "decode_tokens": 0, "iterations": 0, "batch_sum": 0, "agent_steps": 0,
+             "calls": 0, "max_running": 0}
+    logits = None
+    nxt = torch.empty(max_batch, dtype=torch.int32, device="cuda")
+
+    def finish(cid):
+        step, members, _ = clusters.pop(cid)
+        new = [world.move(a, step, pos[a]) for a in members]
+        for a, p in zip(members, new):
+            pos[a] = p
+        sched.ack(cid, new)
+        stats["agent_steps"] += len(members)
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while True:
+        # hand out every ready cluster (idle clusters finish at once and may free others)
+        while True:
+            got = sched.next()
+            if got is None:
+                break
+            cid, step, members = got
+            calls = [(a, sched_calls(world, seed, step, a, V)) for a in members]
+            calls = [(a, c) for a, c in calls if c is not None]
+            clusters[cid] = [step, members, len(calls)]
+            if not calls:
+                finish(cid)
+                continue
+            for a, (prompt, n_out) in calls:
+                arriving.append({"seq": model.seq_open(), "slot": free_slots.pop(), "prompt": prompt,
+                                 "left": n_out, "cluster": cid})
+                stats["calls"] += 1
+        if not arriving and not running:
+            break
+        # prefill the calls that arrived; their first token comes from the prefill
+        for g0 in range(0, len(arriving), group):
+            batch = arriving[g0:g0 + group]
+            off = 0
+            while True:
+                items = [c for c in batch if off < len(c["prompt"])]
+                if not items:
+                    break
+                nt = torch.empty(len(items), dtype=torch.int32, device="cuda")
+                model.prefill_chunk([c["seq"] for c in items], [c["prompt"][off:off + chunk] for c in items], None, nt)
+                done = [j for j, c in enumerate(items) if off + chunk >= len(c["prompt"])]
+                if done:
+                    slots = torch.tensor([items[j]["slot"] for j in done], dtype=torch.int64, device="cuda")
+                    last[slots] = nt[torch.tensor(done, dtype=torch.int64, device="cuda")]
+                off += chunk
+            for c in batch:
+                stats["prefill_tokens"] += len(c["prompt"])
+                c["left"] -= 1
+                stats["decode_tokens"] += 1
+            running.extend(batch)
+        arriving = []
+        # one decode token for every running call that still has tokens to make
+        live = [c for c in running if c["left"] > 0]
+        if live:
+            for b0 in range(0, len(live), max_batch):
+                part = live[b0:b0 + max_batch]
+                idx = torch.tensor([c["slot"] for c in part], dtype=torch.int64, device="cuda")
+                model.decode_step([c["seq"] for c in part], last[idx], logits, nxt[:len(part)])
+                last[idx] = nxt[:len(part)]
+                for c in part:
+                    c["left"] -= 1
+                stats["decode_tokens"] += len(part)
+                stats["iterations"] += 1
+                stats["batch_sum"] += len(part)
+            stats["max_running"] = max(stats["max_running"], len(live))
+        # retire finished calls; acknowledge finished clusters
+        still = []
+        for c in running:
+            if c["left"] > 0:
+                still.append(c)
+                continue
+            model.seq_close(c["seq"])
+            free_slots.append(c["slot"])
+            cl = clusters[c["cluster"]]
+            cl[2] -= 1
+            if cl[2] == 0:
+                finish(c["cluster"])
+        running = still
+    torch.cuda.synchronize()
+    stats["seconds"] = time.perf_counter() - t0
+    return stats
+
+
+def bench_sched(args, torch, metro, synth):
+    """The out-of-order scheduler (Algorithm 3) in closed loop with the engine,
+    against the parallel-sync baseline (Algorithm 1) on the same seeded world
+    and calls (100 x 140 grid, radius_p 4, max_vel 1): 25 agents for 16 steps
+    (the paper's village size) and 200 agents for 4 steps."""
+    shape = synth.LLAMA3_8B
+    cases = [(25, 16), (200, 4)]
+    max_batch = max(n for n, _ in cases)
+    pages = max_batch * ((2048 + 128 + 15) // 16 + 1) + 64
+    model = metro.Model(shape, max_batch=max_batch, max_tokens=16 * 512, max_context=2048 + 128 + 16,
+                        max_seqs=max_batch + 16, kv_pool_bytes=pages * 16 * kv_token_bytes(shape), seed=args.seed)
+    warm = synth.SimWorld(args.seed + 1, 8)
+    run_sched_loop(model, metro.Scheduler(warm.start, 4.0, 1.0, target_step=1), warm, args.seed, shape, torch,
+                   max_batch)
+    out = {}
+    for n_agents, steps in cases:
+        world = synth.SimWorld(args.seed, n_agents, grid=(100, 140))
+        res = {}
+        for mode in ("parallel_sync", "out_of_order"):
+            sched = metro.Scheduler(world.start, 4.0, 1.0, metro.DIST_CHEBYSHEV, steps, sync=mode == "parallel_sync")
+            st = run_sched_loop(model, sched, world, args.seed, shape, torch, max_batch)
+            st["seconds"] = round(st["seconds"], 3)
+            st["tokens_per_s"] = round((st["prefill_tokens"] + st["decode_tokens"]) / st["seconds"], 1)
+            st["mean_decode_batch"] = round(st["batch_sum"] / max(1, st["iterations"]), 1)
+            res[mode] = st
+            log(f"sched {n_agents} agents x {steps} steps, {mode}: {st}")
+        res["speedup_vs_parallel_sync"] = round(res["parallel_sync"]["seconds"] / res["out_of_order"]["seconds"], 3)
+        out[f"{n_agents}x{steps}"] = res
+    model.close()
+    head = out["200x4"]["out_of_order"]
+    flops = 2.0 * shape["n_layers"] * layer_params(shape) * (head["prefill_tokens"] + head["decode_tokens"])
+    roof = {"bound": "mfma", "achieved": round(flops / head["seconds"] / 1e12, 1), "peak": BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(flops / head["seconds"] / 1e12 / BF16_PEAK_TFLOPS, 4), "traffic": None,
+            "kernel": "whole closed loop, linear-layer flops of every prefill and decode token over wall time"}
+    return {"metric": "simulation tokens/s (prefill + decode, wall clock) under the out-of-order scheduler",
+            "value": head["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1, "steps": 1, "warmup": 1,
+            "ms_per_step": round(head["seconds"] * 1e3, 1), "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "bf16",
+            "data": "synthetic: seeded world (SplitMix64 moves and work), prompt ids and random N(0,0.02) weights",
+            "config": {"workload": "Llama-3-8B-shaped decoder serving agents on a 100x140 grid: one LLM call per "
+                                   "busy agent step (prompts lognormal median 640, 8-128 output tokens), radius_p "
+                                   "4, max_vel 1, Chebyshev distance; 200 agents x 4 steps (value) and 25 x 16",
+                       "cases": [f"{n}x{s}" for n, s in cases]},
+            "speedup_vs_parallel_sync": out["200x4"]["speedup_vs_parallel_sync"],
+            "cases": out, "roofline": roof}
+
+
 def bench_prefix(args, torch, metro, synth):
     """Prefix-heavy requests: a 1024-token prefix prefilled once and forked by
     page reference into 64 requests, their suffixes (512..2048 tokens)
@@ -452,9 +611,10 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--agents", type=int, default=25)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--workload", choices=["agents", "trace", "prefix", "70b"], default="agents",
+    ap.add_argument("--workload", choices=["agents", "trace", "prefix", "70b", "sched"], default="agents",
                     help="agents (default): 25 agents, the benchmarked workload; trace: decode driven by the "
-                         "seeded agent trace; prefix: prefix-heavy requests; 70b: Llama-3-70B shape at B=128")
+                         "seeded agent trace; prefix: prefix-heavy requests; 70b: Llama-3-70B shape at B=128; "
+                         "sched: the out-of-order scheduler in closed loop with the engine vs parallel-sync")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device copy three times (counter calibration) and exit")
     args = ap.parse_args()
@@ -475,7 +635,7 @@ def main():
         calibrate_copy(torch)
         return
     if args.workload != "agents":
-        fn = {"trace": bench_trace, "prefix": bench_prefix, "70b": bench_70b}[args.workload]
+        fn = {"trace": bench_trace, "prefix": bench_prefix, "70b": bench_70b, "sched": bench_sched}[args.workload]
         print(json.dumps(fn(args, torch, metro, synth)), flush=True)
         return
     shape = synth.LLAMA3_8B

@@ -282,9 +282,9 @@ class Scheduler:
         self._buf = np.zeros(self.n, dtype=np.int32)
 
     def close(self):
-        if self._h:
+        if self._h and lib is not None:   # lib is gone during interpreter shutdown
             lib.metro_sched_destroy(self._h)
-            self._h = ctypes.c_void_p()
+        self._h = ctypes.c_void_p()
 
     def __del__(self):
         self.close()
