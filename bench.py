@@ -324,12 +324,16 @@ def sched_calls(world, seed, step, agent, vocab):
     return rng.integers(0, vocab, size=plen, dtype=np.int64), int(np.clip(8 * work, 8, 128))
 
 
-def run_sched_loop(model, sched, world, seed, shape, torch, max_batch, chunk=512, group=16):
+def run_sched_loop(model, sched, world, seed, shape, torch, max_batch, chunk=512, group=16, mixed=False,
+                   max_tokens=16 * 512):
     """Closed loop of scheduler and engine: hand-out clusters run one LLM call
     per agent step (idle steps none); each engine iteration prefills the calls
     that arrived (chunked, ``group`` calls per prefill call) and then decodes one
     token for every running call; a cluster is acknowledged, with its agents'
-    moves, when its last call finishes.  Returns wall seconds and counters."""
+    moves, when its last call finishes.  With ``mixed`` an iteration that has
+    arrivals runs one forward for both: every running call's next token as a
+    one-token item plus the arrivals' prompt chunks (up to ``max_tokens``), so
+    the weights are read once for both.  Returns wall seconds and counters."""
     V = shape["vocab"]
     pos = [tuple(int(v) for v in p) for p in world.start]
     last = torch.zeros(max_batch + 8, dtype=torch.int32, device="cuda")
@@ -370,6 +374,45 @@ def run_sched_loop(model, sched, world, seed, shape, torch, max_batch, chunk=512
                 stats["calls"] += 1
         if not arriving and not running:
             break
+        mixed_done = False
+        if mixed and arriving:
+            # one forward: every running call's next token as a one-token item,
+            # then the arrivals' prompt chunks while the token budget lasts;
+            # further forwards for what is left of the prompts
+            mixed_done = True
+            live = [c for c in running if c["left"] > 0][:max_batch]
+            host_last = last.cpu().numpy()
+            items = [(c, host_last[c["slot"]:c["slot"] + 1].astype(np.int64), True) for c in live]
+            pend = [(c, 0) for c in arriving]
+            while items or pend:
+                budget = max_tokens - len(items)
+                rest = []
+                for c, off in pend:
+                    take = min(chunk, len(c["prompt"]) - off)
+                    if len(items) < max_batch and take <= budget:
+                        items.append((c, c["prompt"][off:off + take], off + take >= len(c["prompt"])))
+                        budget -= take
+                        if off + take < len(c["prompt"]):
+                            rest.append((c, off + take))
+                    else:
+                        rest.append((c, off))
+                nt = torch.empty(len(items), dtype=torch.int32, device="cuda")
+                model.prefill_chunk([c["seq"] for c, _, _ in items], [t for _, t, _ in items], None, nt)
+                upd = [j for j, (_, _, fin) in enumerate(items) if fin]
+                if upd:
+                    slots = torch.tensor([items[j][0]["slot"] for j in upd], dtype=torch.int64, device="cuda")
+                    last[slots] = nt[torch.tensor(upd, dtype=torch.int64, device="cuda")]
+                for c, _, fin in items:
+                    if fin:   # a decode token, or the first token of a finished prompt
+                        c["left"] -= 1
+                        stats["decode_tokens"] += 1
+                stats["iterations"] += 1
+                stats["batch_sum"] += len(items)
+                items, pend = [], rest
+            for c in arriving:
+                stats["prefill_tokens"] += len(c["prompt"])
+            running.extend(arriving)
+            arriving = []
         # prefill the calls that arrived; their first token comes from the prefill
         for g0 in range(0, len(arriving), group):
             batch = arriving[g0:g0 + group]
@@ -392,7 +435,7 @@ def run_sched_loop(model, sched, world, seed, shape, torch, max_batch, chunk=512
             running.extend(batch)
         arriving = []
         # one decode token for every running call that still has tokens to make
-        live = [c for c in running if c["left"] > 0]
+        live = [] if mixed_done else [c for c in running if c["left"] > 0]
         if live:
             for b0 in range(0, len(live), max_batch):
                 part = live[b0:b0 + max_batch]
@@ -441,18 +484,21 @@ def bench_sched(args, torch, metro, synth):
     for n_agents, steps in cases:
         world = synth.SimWorld(args.seed, n_agents, grid=(100, 140))
         res = {}
-        for mode in ("parallel_sync", "out_of_order"):
-            sched = metro.Scheduler(world.start, 4.0, 1.0, metro.DIST_CHEBYSHEV, steps, sync=mode == "parallel_sync")
-            st = run_sched_loop(model, sched, world, args.seed, shape, torch, max_batch)
-            st["seconds"] = round(st["seconds"], 3)
-            st["tokens_per_s"] = round((st["prefill_tokens"] + st["decode_tokens"]) / st["seconds"], 1)
-            st["mean_decode_batch"] = round(st["batch_sum"] / max(1, st["iterations"]), 1)
-            res[mode] = st
-            log(f"sched {n_agents} agents x {steps} steps, {mode}: {st}")
-        res["speedup_vs_parallel_sync"] = round(res["parallel_sync"]["seconds"] / res["out_of_order"]["seconds"], 3)
+        for policy in ("separate", "mixed"):
+            for mode in ("parallel_sync", "out_of_order"):
+                sched = metro.Scheduler(world.start, 4.0, 1.0, metro.DIST_CHEBYSHEV, steps,
+                                        sync=mode == "parallel_sync")
+                st = run_sched_loop(model, sched, world, args.seed, shape, torch, max_batch, mixed=policy == "mixed")
+                st["seconds"] = round(st["seconds"], 3)
+                st["tokens_per_s"] = round((st["prefill_tokens"] + st["decode_tokens"]) / st["seconds"], 1)
+                st["mean_batch"] = round(st["batch_sum"] / max(1, st["iterations"]), 1)
+                res[f"{mode}/{policy}"] = st
+                log(f"sched {n_agents} agents x {steps} steps, {mode}, {policy} forwards: {st}")
+            res[f"speedup_vs_parallel_sync/{policy}"] = round(
+                res[f"parallel_sync/{policy}"]["seconds"] / res[f"out_of_order/{policy}"]["seconds"], 3)
         out[f"{n_agents}x{steps}"] = res
     model.close()
-    head = out["200x4"]["out_of_order"]
+    head = out["200x4"]["out_of_order/mixed"]
     flops = 2.0 * shape["n_layers"] * layer_params(shape) * (head["prefill_tokens"] + head["decode_tokens"])
     roof = {"bound": "mfma", "achieved": round(flops / head["seconds"] / 1e12, 1), "peak": BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s", "frac": round(flops / head["seconds"] / 1e12 / BF16_PEAK_TFLOPS, 4), "traffic": None,
@@ -464,9 +510,10 @@ def bench_sched(args, torch, metro, synth):
             "data": "synthetic: seeded world (SplitMix64 moves and work), prompt ids and random N(0,0.02) weights",
             "config": {"workload": "Llama-3-8B-shaped decoder serving agents on a 100x140 grid: one LLM call per "
                                    "busy agent step (prompts lognormal median 640, 8-128 output tokens), radius_p "
-                                   "4, max_vel 1, Chebyshev distance; 200 agents x 4 steps (value) and 25 x 16",
+                                   "4, max_vel 1, Chebyshev distance; 200 agents x 4 steps (value: mixed "
+                                   "prefill/decode forwards) and 25 x 16; separate and mixed forwards",
                        "cases": [f"{n}x{s}" for n, s in cases]},
-            "speedup_vs_parallel_sync": out["200x4"]["speedup_vs_parallel_sync"],
+            "speedup_vs_parallel_sync": out["200x4"]["speedup_vs_parallel_sync/mixed"],
             "cases": out, "roofline": roof}
 
 
