@@ -134,6 +134,33 @@ def test_tiny_chunked_prefill(metro, tiny_case, chunk):
     check_tokens(toks, want)
 
 
+def test_mixed_prefill_and_decode_items(metro, tiny_case):
+    """One prefill call may carry one-token continuations of sequences that
+    already hold context (decode steps through the prefill path) beside whole
+    prompts and first chunks: the mixed batching the scheduler loop uses."""
+    prompts, n_new, cases = tiny_case
+    w, gens = cases["random"]
+    print("tiny mixed prefill/decode items", flush=True)
+    with make_model(metro, synth.TINY, w) as m:
+        V = m.vocab
+        s = [m.seq_open() for _ in range(4)]
+        lg = torch.empty(4, V, device="cuda")
+        nt = torch.empty(4, dtype=torch.int32, device="cuda")
+        m.prefill_chunk(s[:2], prompts[:2], lg[:2], nt[:2])
+        first = lg[:2].cpu().numpy()
+        cut = len(prompts[3]) // 2
+        # decode tokens of seqs 0 and 1, the whole prompt 2, the first half of prompt 3
+        m.prefill_chunk(s, [gens[0][0][:1], gens[1][0][:1], prompts[2], prompts[3][:cut]], lg, nt)
+        mixed = lg.cpu().numpy()
+        # seq 0's next token beside the rest of prompt 3
+        m.prefill_chunk([s[0], s[3]], [gens[0][0][1:2], prompts[3][cut:]], lg[:2], nt[:2])
+        last = lg[:2].cpu().numpy()
+    assert_logits_close(np.stack([first[0], mixed[0], last[0]])[None], gens[0][1][None, :3], "mixed seq 0")
+    assert_logits_close(np.stack([first[1], mixed[1]])[None], gens[1][1][None, :2], "mixed seq 1")
+    assert_logits_close(mixed[2][None, None], gens[2][1][None, :1], "mixed seq 2")
+    assert_logits_close(last[1][None, None], gens[3][1][None, :1], "mixed seq 3")
+
+
 def test_decode_rows_independent_of_batch_composition(metro):
     w = synth.llama_weights(synth.TINY, 1)
     rng = np.random.default_rng(21)
