@@ -325,7 +325,7 @@ def sched_calls(world, seed, step, agent, vocab):
 
 
 def run_sched_loop(model, sched, world, seed, shape, torch, max_batch, chunk=512, group=16, mixed=False,
-                   max_tokens=16 * 512):
+                   max_tokens=16 * 512, hold_tokens=0, hold_iters=0):
     """Closed loop of scheduler and engine: hand-out clusters run one LLM call
     per agent step (idle steps none); each engine iteration prefills the calls
     that arrived (chunked, ``group`` calls per prefill call) and then decodes one
@@ -333,7 +333,10 @@ def run_sched_loop(model, sched, world, seed, shape, torch, max_batch, chunk=512
     moves, when its last call finishes.  With ``mixed`` an iteration that has
     arrivals runs one forward for both: every running call's next token as a
     one-token item plus the arrivals' prompt chunks (up to ``max_tokens``), so
-    the weights are read once for both.  Returns wall seconds and counters."""
+    the weights are read once for both.  Arrived calls wait (at most
+    ``hold_iters`` iterations) until their prompts add up to ``hold_tokens``,
+    unless nothing else runs, so that prompts are prefilled in larger batches.
+    Returns wall seconds and counters."""
     V = shape["vocab"]
     pos = [tuple(int(v) for v in p) for p in world.start]
     last = torch.zeros(max_batch + 8, dtype=torch.int32, device="cuda")
@@ -374,6 +377,17 @@ def run_sched_loop(model, sched, world, seed, shape, torch, max_batch, chunk=512
                 stats["calls"] += 1
         if not arriving and not running:
             break
+        # hold back the arrivals until enough prompt tokens wait (or too long)
+        if arriving and hold_tokens > 0 and any(c["left"] > 0 for c in running):
+            waited = stats["iterations"] - min(c.get("since", stats["iterations"]) for c in arriving)
+            if sum(len(c["prompt"]) for c in arriving) < hold_tokens and waited < hold_iters:
+                for c in arriving:
+                    c.setdefault("since", stats["iterations"])
+                held, arriving = arriving, []
+            else:
+                held = []
+        else:
+            held = []
         mixed_done = False
         if mixed and arriving:
             # one forward: every running call's next token as a one-token item,
@@ -448,6 +462,7 @@ def run_sched_loop(model, sched, world, seed, shape, torch, max_batch, chunk=512
                 stats["iterations"] += 1
                 stats["batch_sum"] += len(part)
             stats["max_running"] = max(stats["max_running"], len(live))
+        arriving = held
         # retire finished calls; acknowledge finished clusters
         still = []
         for c in running:
@@ -484,11 +499,13 @@ def bench_sched(args, torch, metro, synth):
     for n_agents, steps in cases:
         world = synth.SimWorld(args.seed, n_agents, grid=(100, 140))
         res = {}
-        for policy in ("separate", "mixed"):
+        policies = {"separate": {}, "mixed": {"mixed": True},
+                    "mixed+hold": {"mixed": True, "hold_tokens": 8192, "hold_iters": 8}}
+        for policy, kw in policies.items():
             for mode in ("parallel_sync", "out_of_order"):
                 sched = metro.Scheduler(world.start, 4.0, 1.0, metro.DIST_CHEBYSHEV, steps,
                                         sync=mode == "parallel_sync")
-                st = run_sched_loop(model, sched, world, args.seed, shape, torch, max_batch, mixed=policy == "mixed")
+                st = run_sched_loop(model, sched, world, args.seed, shape, torch, max_batch, **kw)
                 st["seconds"] = round(st["seconds"], 3)
                 st["tokens_per_s"] = round((st["prefill_tokens"] + st["decode_tokens"]) / st["seconds"], 1)
                 st["mean_batch"] = round(st["batch_sum"] / max(1, st["iterations"]), 1)
