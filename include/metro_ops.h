@@ -55,7 +55,7 @@ metro_status metro_op_gemm(const uint16_t* X, int32_t ldx, const uint16_t* W, in
                            void* stream);
 
 /* RMSNorm (Zhang & Sennrich 2019): h[r, :] = bf16(x[r, :] / sqrt(mean(x[r, :]^2)
- * + eps) * g), x fp32 [rows, d], g bf16 [d], h bf16 [rows, d], d % 4 == 0. */
+ * + eps) * g), x fp32 [rows, d], g bf16 [d], h bf16 [rows, d], d % 4 == 0, d <= 8192. */
 metro_status metro_op_rmsnorm(float* x, const uint16_t* g, float eps, uint16_t* h, int32_t rows, int32_t d,
                               void* stream);
 

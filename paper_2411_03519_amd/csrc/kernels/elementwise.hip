@@ -1,6 +1,8 @@
 // Row-wise and elementwise kernels of the forward pass (gfx950, wave64):
 // embedding gather, RMSNorm, RoPE + paged KV write, row gather, greedy argmax,
 // plus weight initialisation and page copy used by the runtime.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -39,38 +41,58 @@ hipError_t launch_embed(const int32_t* tok, const uint16_t* embed, int vocab, in
 }
 
 // ---------------------------------------------------------------------------
-// RMSNorm: h = bf16(x * rsqrt(mean(x^2) + eps) * g).  One block per row.
+// RMSNorm: h = bf16(x * rsqrt(mean(x^2) + eps) * g).  One block per row; each
+// thread owns VPT float4 of the row and first issues all its loads (x, g and
+// the n_parts k-slice sums of the GEMM that produced the residual), so the
+// row costs one memory round trip; the slices are added in slice order and
+// the updated residual is written back.
 // ---------------------------------------------------------------------------
-template <int NTH>
+constexpr int kMaxParts = 8;
+
+template <int NTH, int VPT>
 __global__ __launch_bounds__(NTH) void rmsnorm_kernel(float* __restrict__ x, int ldx, const uint16_t* __restrict__ g,
                                                       float eps, uint16_t* __restrict__ h, int ldh, int d,
                                                       const float* __restrict__ parts, int n_parts, int rows) {
-  const int r = blockIdx.x;
+  const int r = blockIdx.x, n4 = d / 4;
   float4* xr = reinterpret_cast<float4*>(x + static_cast<size_t>(r) * ldx);
-  if (n_parts > 0) {
-    const size_t stride = static_cast<size_t>(rows) * d / 4;
-    const float4* pr = reinterpret_cast<const float4*>(parts + static_cast<size_t>(r) * d);
-    for (int i = threadIdx.x; i < d / 4; i += NTH) {
-      float4 s = pr[i];
-      for (int k = 1; k < n_parts; ++k) {
-        const float4 v = pr[k * stride + i];
-        s.x += v.x;
-        s.y += v.y;
-        s.z += v.z;
-        s.w += v.w;
-      }
-      float4 v = xr[i];
-      v.x += s.x;
-      v.y += s.y;
-      v.z += s.z;
-      v.w += s.w;
-      xr[i] = v;
+  const uint2* gr = reinterpret_cast<const uint2*>(g);
+  const float4* pr = reinterpret_cast<const float4*>(parts + static_cast<size_t>(r) * d);
+  const size_t stride = static_cast<size_t>(rows) * d / 4;
+  float4 v[VPT], pv[VPT][kMaxParts];
+  uint2 gw[VPT];
+#pragma unroll
+  for (int j = 0; j < VPT; ++j) {
+    const int i = threadIdx.x + j * NTH;
+    if (i < n4) {
+      v[j] = xr[i];
+      gw[j] = gr[i];
+#pragma unroll
+      for (int k = 0; k < kMaxParts; ++k)
+        if (k < n_parts) pv[j][k] = pr[k * stride + i];
     }
   }
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d / 4; i += NTH) {
-    float4 v = xr[i];
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+#pragma unroll
+  for (int j = 0; j < VPT; ++j) {
+    const int i = threadIdx.x + j * NTH;
+    if (i >= n4) continue;
+    if (n_parts > 0) {
+      float4 sum = pv[j][0];
+#pragma unroll
+      for (int k = 1; k < kMaxParts; ++k)
+        if (k < n_parts) {
+          sum.x += pv[j][k].x;
+          sum.y += pv[j][k].y;
+          sum.z += pv[j][k].z;
+          sum.w += pv[j][k].w;
+        }
+      v[j].x += sum.x;
+      v[j].y += sum.y;
+      v[j].z += sum.z;
+      v[j].w += sum.w;
+      xr[i] = v[j];
+    }
+    ss += v[j].x * v[j].x + v[j].y * v[j].y + v[j].z * v[j].z + v[j].w * v[j].w;
   }
   ss = wave_sum(ss);
   constexpr int NWV = NTH / 64;
@@ -81,14 +103,14 @@ __global__ __launch_bounds__(NTH) void rmsnorm_kernel(float* __restrict__ x, int
 #pragma unroll
   for (int w = 0; w < NWV; ++w) tot += red[w];
   const float inv = rsqrtf(tot / static_cast<float>(d) + eps);
-  const uint2* gr = reinterpret_cast<const uint2*>(g);
   uint2* hr = reinterpret_cast<uint2*>(h + static_cast<size_t>(r) * ldh);
-  for (int i = threadIdx.x; i < d / 4; i += NTH) {
-    float4 v = xr[i];
-    uint2 gw = gr[i];
+#pragma unroll
+  for (int j = 0; j < VPT; ++j) {
+    const int i = threadIdx.x + j * NTH;
+    if (i >= n4) continue;
     uint2 o;
-    o.x = pack_bf16x2(v.x * inv * lo_bf16(gw.x), v.y * inv * hi_bf16(gw.x));
-    o.y = pack_bf16x2(v.z * inv * lo_bf16(gw.y), v.w * inv * hi_bf16(gw.y));
+    o.x = pack_bf16x2(v[j].x * inv * lo_bf16(gw[j].x), v[j].y * inv * hi_bf16(gw[j].x));
+    o.y = pack_bf16x2(v[j].z * inv * lo_bf16(gw[j].y), v[j].w * inv * hi_bf16(gw[j].y));
     hr[i] = o;
   }
 }
@@ -96,13 +118,21 @@ __global__ __launch_bounds__(NTH) void rmsnorm_kernel(float* __restrict__ x, int
 hipError_t launch_rmsnorm(float* x, int ldx, const uint16_t* g, float eps, uint16_t* h, int ldh, int rows, int d,
                           const float* parts, int n_parts, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  // one float4 per thread where the row allows
-  if (d >= 4096)
-    launch_kernel(rmsnorm_kernel<1024>, dim3(rows), dim3(1024), 0, s, x, ldx, g, eps, h, ldh, d, parts, n_parts,
-                       rows);
+  if (n_parts > kMaxParts || d % 4) return hipErrorInvalidValue;
+  const int n4 = d / 4;
+  auto go = [&](auto nth, auto vpt) {
+    constexpr int NTH = decltype(nth)::value, VPT = decltype(vpt)::value;
+    launch_kernel((rmsnorm_kernel<NTH, VPT>), dim3(rows), dim3(NTH), 0, s, x, ldx, g, eps, h, ldh, d, parts, n_parts,
+                  rows);
+  };
+  if (n4 <= 256)
+    go(std::integral_constant<int, 256>{}, std::integral_constant<int, 1>{});
+  else if (n4 <= 1024)
+    go(std::integral_constant<int, 1024>{}, std::integral_constant<int, 1>{});
+  else if (n4 <= 2048)
+    go(std::integral_constant<int, 1024>{}, std::integral_constant<int, 2>{});
   else
-    launch_kernel(rmsnorm_kernel<256>, dim3(rows), dim3(256), 0, s, x, ldx, g, eps, h, ldh, d, parts, n_parts,
-                       rows);
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

@@ -32,9 +32,11 @@ inline void launch_kernel(F kernel, dim3 grid, dim3 block, uint32_t shmem, hipSt
 hipError_t launch_embed(const int32_t* tok, const uint16_t* embed, int vocab, int d, float* x, int T,
                         hipStream_t s);
 
-// h[r, :] = bf16(x[r, :] * rsqrt(mean(x[r, :]^2) + eps) * g); d % 4 == 0.
-// With n_parts > 0 the row first takes the pending GEMM slices:
-// x[r, :] += sum_s parts[s][r][:] (slice stride rows*d), written back to x.
+// h[r, :] = bf16(x[r, :] * rsqrt(mean(x[r, :]^2) + eps) * g); d % 4 == 0,
+// d <= kRmsNormMaxDim.  With 0 < n_parts <= 8 the row first takes the pending
+// GEMM slices: x[r, :] += sum_s parts[s][r][:] (slice stride rows*d), written
+// back to x.  hipErrorInvalidValue outside these limits.
+constexpr int kRmsNormMaxDim = 8192;
 hipError_t launch_rmsnorm(float* x, int ldx, const uint16_t* g, float eps, uint16_t* h, int ldh, int rows, int d,
                           const float* parts, int n_parts, hipStream_t s);
 

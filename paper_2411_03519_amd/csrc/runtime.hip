@@ -180,6 +180,7 @@ metro_status check_config(const metro_config* c) {
       c->vocab <= 0 || c->max_batch <= 0 || c->max_tokens <= 0 || c->max_context <= 0 || c->max_seqs <= 0)
     return fail(METRO_E_INVAL, "config: every count must be positive");
   if (c->d_model % 128) return fail(METRO_E_INVAL, "config: d_model %% 128 != 0");
+  if (c->d_model > metro::kRmsNormMaxDim) return fail(METRO_E_INVAL, "config: d_model > %d", metro::kRmsNormMaxDim);
   if (c->head_dim != 64 && c->head_dim != 128) return fail(METRO_E_INVAL, "config: head_dim must be 64 or 128");
   if (c->n_heads % c->n_kv_heads) return fail(METRO_E_INVAL, "config: n_heads %% n_kv_heads != 0");
   const int g = c->n_heads / c->n_kv_heads;
@@ -913,7 +914,8 @@ metro_status metro_op_gemm(const uint16_t* X, int32_t ldx, const uint16_t* W, in
 metro_status metro_op_rmsnorm(float* x, const uint16_t* g, float eps, uint16_t* h, int32_t rows, int32_t d,
                               void* stream) {
   g_err.clear();
-  if (!x || !g || !h || rows < 0 || d <= 0 || d % 4) return fail(METRO_E_INVAL, "rmsnorm: bad arguments");
+  if (!x || !g || !h || rows < 0 || d <= 0 || d % 4 || d > metro::kRmsNormMaxDim)
+    return fail(METRO_E_INVAL, "rmsnorm: bad arguments");
   hipError_t e = metro::launch_rmsnorm(x, d, g, eps, h, d, rows, d, nullptr, 0, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(nullptr, e, "launch_rmsnorm");
   return METRO_OK;
