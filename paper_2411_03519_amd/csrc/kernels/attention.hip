@@ -235,17 +235,28 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
 // ===========================================================================
 
 // Query columns of one 16-wide MFMA tile: 16/G tokens x G heads.
-template <int HD, int G>
-__global__ __launch_bounds__(512) void attn_prefill_kernel(PrefillAttnArgs a) {
+// Waves x query tiles per wave (16 tiles = 256 query columns per block): at
+// head dim 128, 16 waves (four per SIMD) of one tile each, since 8 waves of
+// two tiles (208 VGPRs) left only two waves per SIMD to hide the latency of
+// each tile's chain of score MFMAs, softmax and output MFMAs; at head dim 64
+// a page tile is too small to split over 16 waves, so 8 waves of two tiles.
+template <int HD>
+struct PrefillShape {
+  static constexpr int NW = HD >= 128 ? 16 : 8, NQ = 16 / NW;
+};
+constexpr int kPrefillTilesPerBlock = 16;
+
+template <int HD, int G, int NW, int NQ>
+__global__ __launch_bounds__(NW * 64) void attn_prefill_kernel(PrefillAttnArgs a) {
   constexpr int KQ = HD / 32;
   constexpr int NT = HD / 16;
-  constexpr int NW = 8;               // waves (two per SIMD)
-  constexpr int NQ = 2;               // query tiles per wave
   constexpr int TPT = 16 / G;         // tokens per tile
   constexpr int TPW = NQ * TPT;       // tokens per wave
   constexpr int PCH = kPage * HD / 8;  // 16-byte chunks of one K (or V^T) page tile
-  constexpr int LPW = PCH / 128;      // direct loads per wave per stage (half a tile)
+  constexpr int WPT = NW / 4;         // waves bringing each of the 4 tiles of a stage
+  constexpr int LPW = PCH / WPT / 64;  // direct loads per wave per stage
   constexpr int NS = 4;               // stages of the LDS ring
+  static_assert(NW % 4 == 0 && PCH % (WPT * 64) == 0, "the waves share each tile evenly");
   // stage = one page pair: [K page 0, K page 1, V^T page 0, V^T page 1]
   __shared__ uint4 ring[NS][4][PCH];
 
@@ -287,17 +298,17 @@ __global__ __launch_bounds__(512) void attn_prefill_kernel(PrefillAttnArgs a) {
     for (int t = 0; t < NT; ++t) o[n][t] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  // Waves 2t and 2t+1 bring the two halves of tile t of every stage: the K
-  // (t < 2) or V^T (t >= 2) tile of page 2*pair + (t & 1).  The absent second
-  // page of an odd count is stood in for by the last page: finite values, all
-  // of its keys masked.
-  const int tile = wave >> 1, half = wave & 1;
-  const size_t part = kv_offset(0, tile >> 1, a.nkv, h, 0, HD, 0) + half * (PCH / 2) * 8;
+  // Waves WPT*t .. WPT*t + WPT-1 bring the parts of tile t of every stage:
+  // the K (t < 2) or V^T (t >= 2) tile of page 2*pair + (t & 1).  The absent
+  // second page of an odd count is stood in for by the last page: finite
+  // values, all of its keys masked.
+  const int tile = wave / WPT, piece = wave % WPT;
+  const size_t part = kv_offset(0, tile >> 1, a.nkv, h, 0, HD, 0) + piece * (PCH / WPT) * 8;
   const size_t pstride = static_cast<size_t>(2) * a.nkv * kPage * HD;
   auto issue = [&](int pair) __attribute__((always_inline)) {
     const int pi = min(2 * pair + (tile & 1), n_pages - 1);
     const uint16_t* src = a.kv + static_cast<size_t>(bt[pi]) * pstride + part + 8 * lane;
-    const uint32_t dst = lds_address(&ring[pair % NS][tile][half * (PCH / 2)]);
+    const uint32_t dst = lds_address(&ring[pair % NS][tile][piece * (PCH / WPT)]);
 #pragma unroll
     for (int c = 0; c < LPW; ++c) lds_load16(src + 512 * c, dst + 1024 * c);
   };
@@ -318,18 +329,24 @@ __global__ __launch_bounds__(512) void attn_prefill_kernel(PrefillAttnArgs a) {
     const uint4(*st)[PCH] = ring[pair % NS];
 
     // K operand of both pages (A of S^T): key row col, dims 32i + 8grp .. +7;
-    // V^T operand over the pair: dims of tile t, keys 4grp .. 4grp+3 of each page
-    uint4 kf[2][KQ], vf[NT];
+    // V^T operand over the pair: dims of tile t, keys 4grp .. 4grp+3 of each
+    // page (held for all query tiles when the wave has several, else read
+    // from LDS as each output tile needs it)
+    uint4 kf[2][KQ];
 #pragma unroll
     for (int pg = 0; pg < 2; ++pg)
 #pragma unroll
       for (int i = 0; i < KQ; ++i) kf[pg][i] = st[pg][64 * i + lane];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
+    auto vt_operand = [&](int t) __attribute__((always_inline)) {
       const int vo = 128 * (t >> 1) + 2 * lane + (t & 1);  // in 8-byte units
       const uint2 va = reinterpret_cast<const uint2*>(st[2])[vo];
       const uint2 vb = reinterpret_cast<const uint2*>(st[3])[vo];
-      vf[t] = make_uint4(va.x, va.y, vb.x, vb.y);
+      return make_uint4(va.x, va.y, vb.x, vb.y);
+    };
+    uint4 vf[NQ > 1 ? NT : 1];
+    if constexpr (NQ > 1) {
+#pragma unroll
+      for (int t = 0; t < NT; ++t) vf[t] = vt_operand(t);
     }
 
     // keys of this pair visible to every query of the block: no mask needed
@@ -381,8 +398,9 @@ __global__ __launch_bounds__(512) void attn_prefill_kernel(PrefillAttnArgs a) {
       split_bf16(pv[1][2], pv[1][3], hi.w, lo.w);
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        o[n][t] = mfma_k32(vf[t], hi, o[n][t]);
-        o[n][t] = mfma_k32(vf[t], lo, o[n][t]);
+        const uint4 v = NQ > 1 ? vf[NQ > 1 ? t : 0] : vt_operand(t);
+        o[n][t] = mfma_k32(v, hi, o[n][t]);
+        o[n][t] = mfma_k32(v, lo, o[n][t]);
       }
     }
   }
@@ -434,12 +452,12 @@ hipError_t launch_attn_decode(const AttnArgs& a, hipStream_t s) {
 
 template <int HD>
 static hipError_t launch_prefill_hd(const PrefillAttnArgs& a, hipStream_t s) {
-  const dim3 grid(a.n_blocks * a.nkv);
+  const dim3 grid(a.n_blocks * a.nkv), block(PrefillShape<HD>::NW * 64);
   switch (a.nq / a.nkv) {
-    case 1: launch_kernel((attn_prefill_kernel<HD, 1>), grid, dim3(512), 0, s, a); break;
-    case 2: launch_kernel((attn_prefill_kernel<HD, 2>), grid, dim3(512), 0, s, a); break;
-    case 4: launch_kernel((attn_prefill_kernel<HD, 4>), grid, dim3(512), 0, s, a); break;
-    case 8: launch_kernel((attn_prefill_kernel<HD, 8>), grid, dim3(512), 0, s, a); break;
+    case 1: launch_kernel((attn_prefill_kernel<HD, 1, PrefillShape<HD>::NW, PrefillShape<HD>::NQ>), grid, block, 0, s, a); break;
+    case 2: launch_kernel((attn_prefill_kernel<HD, 2, PrefillShape<HD>::NW, PrefillShape<HD>::NQ>), grid, block, 0, s, a); break;
+    case 4: launch_kernel((attn_prefill_kernel<HD, 4, PrefillShape<HD>::NW, PrefillShape<HD>::NQ>), grid, block, 0, s, a); break;
+    case 8: launch_kernel((attn_prefill_kernel<HD, 8, PrefillShape<HD>::NW, PrefillShape<HD>::NQ>), grid, block, 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -452,6 +470,6 @@ hipError_t launch_attn_prefill(const PrefillAttnArgs& a, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
-int prefill_tokens_per_block(int group) { return 256 / group; }
+int prefill_tokens_per_block(int group) { return kPrefillTilesPerBlock * 16 / group; }
 
 }  // namespace metro
