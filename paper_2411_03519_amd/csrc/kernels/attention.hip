@@ -64,14 +64,17 @@ __device__ __forceinline__ void split_bf16(float p0, float p1, uint32_t& hi, uin
 // One workgroup of kDecodeWaves waves per (row, kv head); wave w takes pages
 // w, w + kDecodeWaves, ...  The wave's page ids are read once into one VGPR
 // (lane j holds the id of the wave's j-th page, 64 pages per pass) so the page
-// loop never waits on a memory lookup; kDecodeRing pages of K/V are kept in
-// flight in a register ring.  The waves' (max, sum, output) states are merged
-// through LDS in wave order.  Two pages in flight per wave (132 VGPRs) beat
-// four (196) in probes over 25 and 200 rows of ~1300-token contexts (27.4
-// vs 29.6 us at 25 rows, 5.8 TB/s at 200 rows), and smaller splits than
-// 128 pages only moved time into the combine kernel.
-constexpr int kDecodeWaves = 8;
-constexpr int kDecodeRing = 2;
+// loop never waits on a memory lookup; PD pages of K/V are kept in flight in
+// a register ring.  The waves' (max, sum, output) states are merged through
+// LDS in wave order.  Probes over 25 and 200 rows of ~1300-token contexts
+// (8 kv heads, scattered pages): 16 waves with two pages in flight (128
+// VGPRs) took 26.9 us at 25 rows against 28.1 for 8 waves x 2 and 27.9 for
+// 16 x 1; at 200 rows 16 x 1 (102 VGPRs) took 212 us against 218 for 8 x 2
+// and 220 for 16 x 2 -- a deeper ring pays while the grid is too small to
+// fill the CUs twice over, more resident waves pay once it is not.  Smaller
+// splits than 128 pages only moved time into the combine kernel.
+constexpr int kDecodeWaves = 16;
+constexpr int kDecodeRing2MaxBlocks = 512;  // workgroups up to which PD = 2
 
 template <int HD, int G, int NW, int PD, int PS = kDecodePagesPerSplit>
 __global__ __launch_bounds__(NW * 64) void attn_decode_kernel(AttnArgs a) {
@@ -423,18 +426,27 @@ __global__ __launch_bounds__(NW * 64) void attn_prefill_kernel(PrefillAttnArgs a
 
 // ===========================================================================
 
+template <int HD, int G, int NW>
+static hipError_t launch_decode_g(bool ring2, dim3 grid, dim3 block, const AttnArgs& a, hipStream_t s) {
+  if (ring2)
+    launch_kernel((attn_decode_kernel<HD, G, NW, 2>), grid, block, 0, s, a);
+  else
+    launch_kernel((attn_decode_kernel<HD, G, NW, 1>), grid, block, 0, s, a);
+  return hipGetLastError();
+}
+
 template <int HD>
 static hipError_t launch_decode_hd(const AttnArgs& a, hipStream_t s) {
-  constexpr int NW = kDecodeWaves, PD = kDecodeRing;
+  constexpr int NW = kDecodeWaves;
   const dim3 grid(a.n_work * a.nkv), block(NW * 64);
+  const bool ring2 = static_cast<int64_t>(a.n_work) * a.nkv <= kDecodeRing2MaxBlocks;
   switch (a.nq / a.nkv) {
-    case 1: launch_kernel((attn_decode_kernel<HD, 1, NW, PD>), grid, block, 0, s, a); break;
-    case 2: launch_kernel((attn_decode_kernel<HD, 2, NW, PD>), grid, block, 0, s, a); break;
-    case 4: launch_kernel((attn_decode_kernel<HD, 4, NW, PD>), grid, block, 0, s, a); break;
-    case 8: launch_kernel((attn_decode_kernel<HD, 8, NW, PD>), grid, block, 0, s, a); break;
+    case 1: return launch_decode_g<HD, 1, NW>(ring2, grid, block, a, s);
+    case 2: return launch_decode_g<HD, 2, NW>(ring2, grid, block, a, s);
+    case 4: return launch_decode_g<HD, 4, NW>(ring2, grid, block, a, s);
+    case 8: return launch_decode_g<HD, 8, NW>(ring2, grid, block, a, s);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 hipError_t launch_attn_combine(const AttnArgs& a, hipStream_t s) {
