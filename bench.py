@@ -534,6 +534,97 @@ def bench_sched(args, torch, metro, synth):
             "cases": out, "roofline": roof}
 
 
+def run_call_round(model, calls, outs, torch, use_cache, chunk=512):
+    """One round of agent calls as one batch: each call opens its sequence
+    (through the prefix cache when on), the uncached rest of every prompt is
+    prefilled in 512-token chunks, then decode steps run until each call has
+    its output length (finished calls leave the batch).  Returns (cached
+    prompt tokens, computed prompt tokens, decode tokens)."""
+    n = len(calls)
+    seqs, ks = [], []
+    for p in calls:
+        if use_cache:
+            sq, k = model.seq_open_cached(p)
+        else:
+            sq, k = model.seq_open(), 0
+        seqs.append(sq)
+        ks.append(k)
+    tok = torch.zeros(n, dtype=torch.int32, device="cuda")
+    prefill_all(model, seqs, [p[k:] for p, k in zip(calls, ks)], chunk, n, torch, tok)
+    left = np.asarray(outs, np.int64) - 1
+    active = [i for i in range(n) if left[i] > 0]
+    n_dec = 0
+    while active:
+        idx = torch.tensor(active, dtype=torch.int64, device="cuda")
+        nt = torch.empty(len(active), dtype=torch.int32, device="cuda")
+        model.decode_step([seqs[i] for i in active], tok[idx].contiguous(), None, nt)
+        tok[idx] = nt
+        n_dec += len(active)
+        left[active] -= 1
+        active = [i for i in active if left[i] > 0]
+    for sq in seqs:
+        model.seq_close(sq)
+    return sum(ks), sum(len(p) - k for p, k in zip(calls, ks)), n_dec
+
+
+def bench_apc(args, torch, metro, synth):
+    """Automatic prefix caching on successive agent calls: 25 agents, 8 rounds
+    of one call each (prompts: a 256-token preamble shared by all, a 192-token
+    persona per agent, a fresh observation lognormal median 160; outputs
+    lognormal median 18 -- about 640 prompt and 22 output tokens per call),
+    each round run as one batch, with the prefix cache off and on."""
+    shape = synth.LLAMA3_8B
+    n, rounds = 25, 8
+    prompts, outs = synth.agent_call_prompts(args.seed, n, rounds, shape["vocab"])
+    warm_p, warm_o = synth.agent_call_prompts(args.seed + 1, n, 1, shape["vocab"])
+    max_ctx = max(len(p) for r in prompts + warm_p for p in r) + 80
+    pages = 16384
+    model = metro.Model(shape, max_batch=n, max_tokens=n * 512, max_context=max_ctx, max_seqs=n + 8,
+                        kv_pool_bytes=pages * 16 * kv_token_bytes(shape), seed=args.seed)
+    run_call_round(model, warm_p[0], warm_o[0], torch, False)
+    res = {}
+    for mode in ("off", "on"):
+        model.prefix_cache(0)
+        if mode == "on":
+            model.prefix_cache(pages)
+        times, cached, computed, dec = [], 0, 0, 0
+        for r in range(rounds):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            c, p, d = run_call_round(model, prompts[r], outs[r], torch, mode == "on")
+            torch.cuda.synchronize()
+            times.append(time.perf_counter() - t0)
+            cached, computed, dec = cached + c, computed + p, dec + d + n
+        total = sum(len(p) for r in prompts for p in r) + int(sum(np.sum(o) for o in outs))
+        res[mode] = {"seconds": round(sum(times), 3), "round_ms": [round(t * 1e3, 1) for t in times],
+                     "cached_prompt_tokens": cached, "computed_prompt_tokens": computed,
+                     "output_tokens": dec, "tokens_per_s": round(total / sum(times), 1),
+                     "steady_tokens_per_s": round(total * (rounds - 1) / rounds / sum(times[1:]), 1)}
+        if mode == "on":
+            res[mode]["cache"] = model.prefix_cache_stats()
+        log(f"apc {mode}: {res[mode]}")
+    model.close()
+    on, off = res["on"], res["off"]
+    gain = off["seconds"] / on["seconds"]
+    flops = 2.0 * shape["n_layers"] * layer_params(shape) * (on["computed_prompt_tokens"] + on["output_tokens"])
+    roof = {"bound": "mfma", "achieved": round(flops / on["seconds"] / 1e12, 1), "peak": BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(flops / on["seconds"] / 1e12 / BF16_PEAK_TFLOPS, 4), "traffic": None,
+            "kernel": "all rounds with the cache on, linear-layer flops of computed prompt and output tokens "
+                      "over wall time"}
+    return {"metric": "agent-call throughput (prompt + output tokens/s, wall clock) with automatic prefix caching",
+            "value": on["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1, "steps": rounds, "warmup": 1,
+            "ms_per_step": round(on["seconds"] / rounds * 1e3, 1), "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "bf16",
+            "data": "synthetic: seeded prompt ids (shared preamble, per-agent persona, fresh observation), random "
+                    "N(0,0.02) bf16 weights",
+            "config": {"workload": "Llama-3-8B-shaped decoder, 25 agents x 8 rounds of one call each, one batch per "
+                                   "round; prompts = 256-token shared preamble + 192-token persona per agent + "
+                                   "observation lognormal(median 160, sigma 0.6) in [16,1024]; outputs "
+                                   "lognormal(median 18, sigma 0.6) in [4,64]; chunked prefill 512",
+                       "agents": n, "rounds": rounds},
+            "gain_vs_no_cache": round(gain, 3), "modes": res, "roofline": roof}
+
+
 def bench_prefix(args, torch, metro, synth):
     """Prefix-heavy requests: a 1024-token prefix prefilled once and forked by
     page reference into 64 requests, their suffixes (512..2048 tokens)
@@ -675,7 +766,7 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--agents", type=int, default=25)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--workload", choices=["agents", "trace", "prefix", "70b", "sched"], default="agents",
+    ap.add_argument("--workload", choices=["agents", "trace", "prefix", "70b", "sched", "apc"], default="agents",
                     help="agents (default): 25 agents, the benchmarked workload; trace: decode driven by the "
                          "seeded agent trace; prefix: prefix-heavy requests; 70b: Llama-3-70B shape at B=128; "
                          "sched: the out-of-order scheduler in closed loop with the engine vs parallel-sync")
@@ -699,7 +790,8 @@ def main():
         calibrate_copy(torch)
         return
     if args.workload != "agents":
-        fn = {"trace": bench_trace, "prefix": bench_prefix, "70b": bench_70b, "sched": bench_sched}[args.workload]
+        fn = {"trace": bench_trace, "prefix": bench_prefix, "70b": bench_70b, "sched": bench_sched,
+              "apc": bench_apc}[args.workload]
         print(json.dumps(fn(args, torch, metro, synth)), flush=True)
         return
     shape = synth.LLAMA3_8B

@@ -113,7 +113,7 @@ typedef struct metro_model_info {
   int64_t kv_pool_bytes;    /* device bytes of the KV page pool */
   int64_t kv_bytes_per_token; /* all layers, K and V */
   int32_t n_pages;          /* pages in the pool */
-  int32_t free_pages;       /* pages not referenced by any sequence */
+  int32_t free_pages;       /* pages referenced by no sequence and not held by the prefix cache */
   int32_t open_seqs;
   int32_t device;           /* HIP device ordinal */
 } metro_model_info;
@@ -149,14 +149,61 @@ metro_status metro_load_weight(metro_model* model, int32_t weight_id, int32_t la
 
 metro_status metro_model_get_info(const metro_model* model, metro_model_info* info);
 
-/* Open an empty sequence (one agent request / conversation).
+/* Open an empty sequence (one agent request / conversation).  With the
+ * prefix cache on, the pages its prefills fill are entered in the cache.
  * Errors: E_CAPACITY (max_seqs open). */
 metro_status metro_seq_open(metro_model* model, int64_t* seq);
+
+/* Automatic prefix caching: the common-prompt-prefix cache of the serving
+ * engine (§4.1; the paper reports about 20% more throughput with it on).
+ *
+ * A page (16 positions) enters the cache once a prefill has filled it while
+ * every earlier token of its sequence also came from prefills (the host has
+ * seen them all).  It is keyed by its 16 token ids and the cached page before
+ * it, so a key stands for the exact token prefix up to the page's end; a hit
+ * is never approximate.  metro_seq_open_cached attaches the longest chain of
+ * cached pages that matches a prompt, by reference; the caller then prefills
+ * only the rest.  A decode step, whose tokens live on the device, ends a
+ * sequence's entries; forked sequences enter none.
+ *
+ * The cache holds one reference per cached page.  Pages that only the cache
+ * holds are reclaimed when a call needs pages and too few are free, and when
+ * entering a page would exceed max_pages: least recently used first, a page
+ * never before the cached pages that continue it.  When two sequences fill
+ * equal prefixes, the first one's page stays cached and the second keeps a
+ * reference to it until it closes.
+ *
+ * max_pages > 0 turns the cache on (or changes its limit, evicting down to it
+ * where it can); 0 turns it off and releases every cached page.  Off by
+ * default.  Host bookkeeping only; no device work.  Errors: E_INVAL. */
+metro_status metro_prefix_cache(metro_model* model, int32_t max_pages);
+
+typedef struct metro_prefix_cache_stats {
+  int32_t pages;            /* pages the cache holds */
+  int32_t limit;            /* max_pages (0 = off) */
+  int64_t lookup_tokens;    /* prompt tokens offered to metro_seq_open_cached */
+  int64_t hit_tokens;       /* of which attached from the cache */
+  int64_t inserted;         /* pages entered so far */
+  int64_t evicted;          /* pages released so far */
+} metro_prefix_cache_stats;
+
+metro_status metro_prefix_cache_get_stats(const metro_model* model, metro_prefix_cache_stats* stats);
+
+/* Open a sequence for a prompt tokens[0 .. n_tokens) (host int32) and attach
+ * the longest chain of cached pages matching its first tokens, at most
+ * n_tokens - 1 of them, so that at least one token is left for the prefill
+ * that returns the prompt's next-token logits.  *n_cached receives the number
+ * of tokens attached (a multiple of 16; 0 with the cache off); the sequence
+ * starts at that length and the caller prefills tokens[*n_cached ..).
+ * Errors: E_INVAL (NULL, n_tokens < 0), E_CAPACITY (max_seqs open). */
+metro_status metro_seq_open_cached(metro_model* model, const int32_t* tokens, int32_t n_tokens, int64_t* seq,
+                                   int32_t* n_cached);
 
 /* Open a new sequence whose first n_tokens positions are those of src
  * (0 < n_tokens <= length of src).  Whole pages are shared by reference (never
  * written again by either sequence); a partly filled last page is copied on
  * `stream`.  This is the by-reference sharing of a common prompt prefix.
+ * The new sequence enters no pages in the prefix cache.
  * Errors: E_SEQ, E_INVAL, E_CAPACITY, E_NOPAGES, E_HIP. */
 metro_status metro_seq_fork(metro_model* model, int64_t src, int32_t n_tokens, void* stream,
                             int64_t* seq);
@@ -182,7 +229,8 @@ metro_status metro_seq_pages(const metro_model* model, int64_t seq, int32_t* pag
  *             new position
  *   next_tok  device int32 [n_items] or NULL: greedy token of that position
  * Positions are appended at length .. length+c-1 of each sequence.  Pages for
- * the new tokens are taken from the pool for all items or none.
+ * the new tokens are taken from the pool for all items or none (reclaiming
+ * pages only the prefix cache holds when too few are free).
  * Errors: E_INVAL, E_SEQ, E_CAPACITY, E_NOPAGES, E_HIP. */
 metro_status metro_prefill_chunk(metro_model* model, int32_t n_items, const int64_t* seqs,
                                  const int32_t* cu_tokens, const int32_t* tokens, float* logits,

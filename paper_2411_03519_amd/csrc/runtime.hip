@@ -626,6 +626,39 @@ metro_status metro_seq_open(metro_model* m, int64_t* seq) {
   return METRO_OK;
 }
 
+metro_status metro_seq_open_cached(metro_model* m, const int32_t* tokens, int32_t n_tokens, int64_t* seq,
+                                   int32_t* n_cached) {
+  g_err.clear();
+  metro_status st = check_live(m);
+  if (st != METRO_OK) return st;
+  if (!seq || !n_cached) return fail(METRO_E_INVAL, "NULL argument");
+  const int r = m->seqs->open_cached(tokens, n_tokens, seq, n_cached);
+  if (r != METRO_OK) return fail(static_cast<metro_status>(r), "%s", m->seqs->error().c_str());
+  return METRO_OK;
+}
+
+metro_status metro_prefix_cache(metro_model* m, int32_t max_pages) {
+  g_err.clear();
+  metro_status st = check_live(m);
+  if (st != METRO_OK) return st;
+  const int r = m->seqs->set_prefix_cache(max_pages);
+  if (r != METRO_OK) return fail(static_cast<metro_status>(r), "%s", m->seqs->error().c_str());
+  return METRO_OK;
+}
+
+metro_status metro_prefix_cache_get_stats(const metro_model* m, metro_prefix_cache_stats* out) {
+  g_err.clear();
+  if (!m || !out) return fail(METRO_E_INVAL, "NULL argument");
+  const metro::PrefixCacheStats st = m->seqs->prefix_cache_stats();
+  out->pages = st.pages;
+  out->limit = st.limit;
+  out->lookup_tokens = st.lookup_tokens;
+  out->hit_tokens = st.hit_tokens;
+  out->inserted = st.inserted;
+  out->evicted = st.evicted;
+  return METRO_OK;
+}
+
 metro_status metro_seq_fork(metro_model* m, int64_t src, int32_t n_tokens, void* stream, int64_t* seq) {
   g_err.clear();
   metro_status st = check_live(m);
@@ -755,6 +788,7 @@ metro_status metro_prefill_chunk(metro_model* m, int32_t n_items, const int64_t*
   st = launch_head(m, m->xr, n_items, 0, logits, next_tok, s);
   if (st != METRO_OK) return st;
   m->seqs->commit(seqs, add.data(), n_items);
+  m->seqs->record_prefill(seqs, cu, tokens, n_items);
   return METRO_OK;
 }
 
@@ -835,6 +869,7 @@ metro_status metro_decode_step(metro_model* m, int32_t B, const int64_t* seqs, c
   st = launch_head(m, m->x, B, xp, logits, next_tok, s);
   if (st != METRO_OK) return st;
   m->seqs->commit(seqs, add.data(), B);
+  m->seqs->record_unknown(seqs, B);
   return METRO_OK;
 }
 

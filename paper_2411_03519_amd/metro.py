@@ -41,6 +41,11 @@ class Config(ctypes.Structure):
                 ("max_context", ctypes.c_int32), ("max_seqs", ctypes.c_int32), ("kv_pool_bytes", ctypes.c_int64)]
 
 
+class PrefixCacheStats(ctypes.Structure):
+    _fields_ = [("pages", ctypes.c_int32), ("limit", ctypes.c_int32), ("lookup_tokens", ctypes.c_int64),
+                ("hit_tokens", ctypes.c_int64), ("inserted", ctypes.c_int64), ("evicted", ctypes.c_int64)]
+
+
 class ModelInfo(ctypes.Structure):
     _fields_ = [("weight_bytes", ctypes.c_int64), ("scratch_bytes", ctypes.c_int64),
                 ("kv_pool_bytes", ctypes.c_int64), ("kv_bytes_per_token", ctypes.c_int64),
@@ -58,6 +63,9 @@ _SIGS = {
     "metro_load_weight": (_i32, [_vp, _i32, _i32, _vp, _i64]),
     "metro_model_get_info": (_i32, [_vp, ctypes.POINTER(ModelInfo)]),
     "metro_seq_open": (_i32, [_vp, ctypes.POINTER(_i64)]),
+    "metro_seq_open_cached": (_i32, [_vp, _vp, _i32, ctypes.POINTER(_i64), ctypes.POINTER(_i32)]),
+    "metro_prefix_cache": (_i32, [_vp, _i32]),
+    "metro_prefix_cache_get_stats": (_i32, [_vp, ctypes.POINTER(PrefixCacheStats)]),
     "metro_seq_fork": (_i32, [_vp, _i64, _i32, _vp, ctypes.POINTER(_i64)]),
     "metro_seq_close": (_i32, [_vp, _i64]),
     "metro_seq_length": (_i32, [_vp, _i64, ctypes.POINTER(_i32)]),
@@ -179,6 +187,23 @@ class Model:
         s = _i64()
         check(lib.metro_seq_open(self._h, ctypes.byref(s)))
         return s.value
+
+    def seq_open_cached(self, tokens) -> tuple[int, int]:
+        """Open a sequence for a prompt; returns (seq, n_cached): the leading
+        tokens attached from the prefix cache, the rest to be prefilled."""
+        t = _host_i32(tokens)
+        s, n = _i64(), _i32()
+        check(lib.metro_seq_open_cached(self._h, t.ctypes.data if t.size else None, t.size, ctypes.byref(s),
+                                        ctypes.byref(n)))
+        return s.value, n.value
+
+    def prefix_cache(self, max_pages: int) -> None:
+        check(lib.metro_prefix_cache(self._h, max_pages))
+
+    def prefix_cache_stats(self) -> dict:
+        st = PrefixCacheStats()
+        check(lib.metro_prefix_cache_get_stats(self._h, ctypes.byref(st)))
+        return {f: getattr(st, f) for f, _ in PrefixCacheStats._fields_}
 
     def seq_fork(self, src: int, n_tokens: int, stream=None) -> int:
         s = _i64()

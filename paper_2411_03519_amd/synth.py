@@ -139,6 +139,28 @@ def prefix_heavy_batch(seed: int = 0, n_agents: int = 64, vocab: int = LLAMA3_8B
     return prefix, prompt_tokens(rng, lengths, vocab), 32
 
 
+def agent_call_prompts(seed: int, n_agents: int, n_rounds: int, vocab: int, preamble: int = 256,
+                       persona: int = 192, obs_median: float = 160.0, obs_sigma: float = 0.6, obs_lo: int = 16,
+                       obs_hi: int = 1024, out_median: float = 18.0, out_sigma: float = 0.6, out_lo: int = 4,
+                       out_hi: int = 64):
+    """Successive LLM calls of agents whose prompts share text: a preamble
+    common to every agent and call (instructions), a persona per agent that is
+    the same in each of its calls, and a fresh observation per call (length
+    lognormal, clipped); output lengths lognormal, clipped.  The defaults give
+    a mean call of about 640 prompt and 22 output tokens.
+    Returns (prompts[round][agent] int64 arrays, out_lens[round][agent])."""
+    rng = np.random.Generator(np.random.PCG64([seed, 428]))
+    pre = rng.integers(0, vocab, size=preamble, dtype=np.int64)
+    pers = [rng.integers(0, vocab, size=persona, dtype=np.int64) for _ in range(n_agents)]
+    prompts, outs = [], []
+    for _ in range(n_rounds):
+        obs = lognormal_lengths(rng, n_agents, obs_median, obs_sigma, obs_lo, obs_hi)
+        prompts.append([np.concatenate([pre, pers[a], rng.integers(0, vocab, size=int(obs[a]), dtype=np.int64)])
+                        for a in range(n_agents)])
+        outs.append(lognormal_lengths(rng, n_agents, out_median, out_sigma, out_lo, out_hi))
+    return prompts, outs
+
+
 def uniform_contexts(seed: int, n_agents: int, lo: int, hi: int) -> np.ndarray:
     rng = np.random.Generator(np.random.PCG64(seed))
     return rng.integers(lo, hi + 1, size=n_agents).astype(np.int64)

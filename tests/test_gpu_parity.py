@@ -11,6 +11,7 @@ import numpy as np
 import pytest
 
 from oracle import LlamaShape, OracleModel
+from oracle.prefix_cache import OraclePrefixCache
 from paper_2411_03519_amd import synth
 from tests.parity import assert_logits_close, check_tokens, noise_floor
 
@@ -237,6 +238,100 @@ def test_prefix_fork_shares_pages(metro, prefix_len):
         m.seq_close(base)
     want = np.stack([ref.prefill(ref.new_cache(), np.concatenate([prefix, s])) for s in suffixes])
     assert_logits_close(got, want, "fork")
+
+
+def run_cached_calls(m, calls, n_steps, ref_cache=None):
+    """One round of agent calls through the prefix cache: every call opens its
+    sequence with its prompt, the uncached rest of all prompts is prefilled in
+    one batch, then ``n_steps`` decode steps are fed with the greedy tokens of
+    the previous step.  Returns (n_cached per call, logits [n, 1+steps, V],
+    fed tokens [n, steps])."""
+    seqs, ks = [], []
+    for i, p in enumerate(calls):
+        s, k = m.seq_open_cached(p)
+        if ref_cache is not None:
+            want = ref_cache.open_cached(s, p)
+            assert k == want, f"call {i}: {k} tokens taken from the cache, oracle {want}"
+        seqs.append(s)
+        ks.append(k)
+    n, V = len(calls), m.vocab
+    lg = torch.empty(n, V, device="cuda")
+    nt = torch.empty(n, dtype=torch.int32, device="cuda")
+    m.prefill_chunk(seqs, [p[k:] for p, k in zip(calls, ks)], lg, nt)
+    if ref_cache is not None:
+        for s, p, k in zip(seqs, calls, ks):
+            ref_cache.prefill(s, p[k:])
+    rows, fed = [lg.cpu().numpy()], []
+    for _ in range(n_steps):
+        fed.append(nt.cpu().numpy().copy())
+        m.decode_step(seqs, nt.clone(), lg, nt)
+        rows.append(lg.cpu().numpy())
+        if ref_cache is not None:
+            for s in seqs:
+                ref_cache.decode(s)
+    for s in seqs:
+        m.seq_close(s)
+        if ref_cache is not None:
+            ref_cache.close(s)
+    return ks, np.stack(rows, axis=1), np.array(fed).T.reshape(n, n_steps)
+
+
+def test_prefix_cache_hits_match_oracle(metro):
+    """Agents' successive calls share a preamble and a persona: from the second
+    round on, each call takes over exactly the pages the cache oracle names,
+    by reference, and its logits match the oracle's full computation."""
+    w = synth.llama_weights(synth.TINY, 5, norm="random")
+    ref = OracleModel(LlamaShape(**synth.TINY), w)
+    prompts, _ = synth.agent_call_prompts(1, 4, 3, synth.TINY["vocab"], preamble=40, persona=24,
+                                          obs_median=12, obs_sigma=0.5, obs_lo=3, obs_hi=40)
+    oc = OraclePrefixCache()
+    with make_model(metro, synth.TINY, w) as m:
+        m.prefix_cache(4096)
+        for r, calls in enumerate(prompts):
+            ks, got, fed = run_cached_calls(m, calls, 3, oc)
+            if r == 0:
+                assert ks == [0] * 4
+            else:
+                assert ks == [64] * 4   # preamble + persona = 4 whole pages
+            for i, p in enumerate(calls):
+                want = ref.teacher_forced(p, fed[i])
+                assert_logits_close(got[i], want, f"round {r} call {i} (cached {ks[i]})")
+        st = m.prefix_cache_stats()
+        assert st["hit_tokens"] == 2 * 4 * 64 and st["evicted"] == 0
+        # each round enters its calls' whole prompt pages; the cache holds
+        # exactly the distinct known prefixes of the oracle
+        assert st["pages"] == len(oc.known)
+        m.prefix_cache(0)
+        assert m.prefix_cache_stats()["pages"] == 0 and m.info().free_pages == m.info().n_pages
+
+
+def test_prefix_cache_under_page_pressure(metro):
+    """A pool too small to keep every prompt: the cache gives pages back (least
+    recently used first) when a call needs them, hits stay correct, and a
+    cached open never takes over more than the no-eviction oracle allows."""
+    w = synth.llama_weights(synth.TINY, 6, norm="random")
+    ref = OracleModel(LlamaShape(**synth.TINY), w)
+    prompts, _ = synth.agent_call_prompts(2, 4, 5, synth.TINY["vocab"], preamble=40, persona=24,
+                                          obs_median=30, obs_sigma=0.5, obs_lo=8, obs_hi=60)
+    page_bytes = 2 * 2 * 64 * 16 * 2 * 2
+    oc = OraclePrefixCache()
+    with make_model(metro, synth.TINY, w, kv_pool_bytes=36 * page_bytes) as m:
+        m.prefix_cache(1000)
+        for r, calls in enumerate(prompts):
+            bound = [OraclePrefixCache.open_cached(oc, -1 - i, p) for i, p in enumerate(calls)]
+            for i in range(len(calls)):
+                oc.close(-1 - i)
+            ks, got, fed = run_cached_calls(m, calls, 2)
+            for i, p in enumerate(calls):
+                assert ks[i] % 16 == 0 and ks[i] <= bound[i]
+                oc.open(1000 * r + i)
+                oc.prefill(1000 * r + i, p)
+                want = ref.teacher_forced(p, fed[i])
+                assert_logits_close(got[i], want, f"round {r} call {i} (cached {ks[i]})")
+        st = m.prefix_cache_stats()
+        assert st["evicted"] > 0 and st["hit_tokens"] > 0
+        inf = m.info()
+        assert inf.free_pages + st["pages"] == inf.n_pages
 
 
 def test_error_conventions(metro):
