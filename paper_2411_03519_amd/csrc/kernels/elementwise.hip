@@ -213,7 +213,9 @@ hipError_t launch_gather_rows(const float* x, int d, const int32_t* rows, int n,
 
 // ---------------------------------------------------------------------------
 // Greedy argmax over fp32 logits: lowest index among the maxima, NaN skipped.
-// One block of 1024 threads per row.
+// One block of 1024 threads per row; each thread issues kArgmaxBatch float4
+// loads before comparing any, so a 128k-entry row costs four memory round
+// trips instead of one per load (23.8 -> about 5 us for 25 rows of 128256).
 // ---------------------------------------------------------------------------
 struct ArgBest {
   float v;
@@ -227,16 +229,31 @@ __device__ __forceinline__ ArgBest arg_better(ArgBest a, ArgBest b) {
   return a;
 }
 
+constexpr int kArgmaxBatch = 8;
+
 __global__ __launch_bounds__(1024) void argmax_kernel(const float* __restrict__ logits, int vocab,
                                                       int32_t* __restrict__ out) {
   const float4* row = reinterpret_cast<const float4*>(logits + static_cast<size_t>(blockIdx.x) * vocab);
+  const int n4 = vocab / 4;
   ArgBest b{0.f, -1};
-  for (int j = threadIdx.x; j < vocab / 4; j += 1024) {
-    const float4 v = row[j];
-    const float e[4] = {v.x, v.y, v.z, v.w};
+  // a thread visits j = tid, tid + 1024, ... in increasing order, so the
+  // strict comparison keeps its lowest index among equal values
+  for (int j0 = threadIdx.x; j0 < n4; j0 += kArgmaxBatch * 1024) {
+    float4 v[kArgmaxBatch];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      if (e[k] == e[k] && (b.i < 0 || e[k] > b.v)) b = ArgBest{e[k], 4 * j + k};
+    for (int u = 0; u < kArgmaxBatch; ++u) {
+      const int j = j0 + u * 1024;
+      v[u] = j < n4 ? row[j] : make_float4(__builtin_nanf(""), __builtin_nanf(""), __builtin_nanf(""),
+                                           __builtin_nanf(""));
+    }
+#pragma unroll
+    for (int u = 0; u < kArgmaxBatch; ++u) {
+      const int j = j0 + u * 1024;
+      const float e[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if (e[k] == e[k] && (b.i < 0 || e[k] > b.v)) b = ArgBest{e[k], 4 * j + k};
+      }
     }
   }
 #pragma unroll

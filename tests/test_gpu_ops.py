@@ -176,3 +176,19 @@ def test_argmax_lowest_index_and_nan(metro):
     want = greedy_argmax(np.where(np.isnan(L), -np.inf, L))
     want[4] = -1
     np.testing.assert_array_equal(got, want)
+
+
+@pytest.mark.parametrize("V", [32, 4096, 4 * 8 * 1024 + 36])
+def test_argmax_short_and_ragged_rows(metro, V):
+    # rows shorter than one batch of loads per thread, and one that ends a few
+    # float4 into a second batch; ties planted across threads and batches
+    rng = np.random.default_rng(V)
+    L = rng.standard_normal((3, V)).astype(np.float32)
+    L[0, [V - 1, 3]] = 30.0
+    L[1, V // 2:] = np.nan
+    L[2, [V - 4, V - 8]] = 7.0
+    out = torch.zeros(3, dtype=torch.int32, device="cuda")
+    metro.op_argmax(torch.from_numpy(L).cuda(), 3, V, out)
+    torch.cuda.synchronize()
+    want = greedy_argmax(np.where(np.isnan(L), -np.inf, L))
+    np.testing.assert_array_equal(out.cpu().numpy(), want)
