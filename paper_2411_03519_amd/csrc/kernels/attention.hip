@@ -248,6 +248,7 @@ struct PrefillShape {
   static constexpr int NW = HD >= 128 ? 16 : 8, NQ = 16 / NW;
 };
 constexpr int kPrefillTilesPerBlock = 16;
+constexpr int kPrefillPageIds = 512;  // page ids staged in LDS (contexts up to 8192 keys)
 
 template <int HD, int G, int NW, int NQ>
 __global__ __launch_bounds__(NW * 64) void attn_prefill_kernel(PrefillAttnArgs a) {
@@ -308,9 +309,16 @@ __global__ __launch_bounds__(NW * 64) void attn_prefill_kernel(PrefillAttnArgs a
   const int tile = wave / WPT, piece = wave % WPT;
   const size_t part = kv_offset(0, tile >> 1, a.nkv, h, 0, HD, 0) + piece * (PCH / WPT) * 8;
   const size_t pstride = static_cast<size_t>(2) * a.nkv * kPage * HD;
+  // The block's page ids go to LDS once, so that a stage's load issue waits
+  // on an LDS read rather than on a block-table load from memory (pages past
+  // the table's capacity are still read from the block table).
+  __shared__ int32_t page_ids[kPrefillPageIds];
+  for (int i = tid; i < min(n_pages, kPrefillPageIds); i += NW * 64) page_ids[i] = bt[i];
+  __syncthreads();
   auto issue = [&](int pair) __attribute__((always_inline)) {
     const int pi = min(2 * pair + (tile & 1), n_pages - 1);
-    const uint16_t* src = a.kv + static_cast<size_t>(bt[pi]) * pstride + part + 8 * lane;
+    const int id = pi < kPrefillPageIds ? page_ids[pi] : bt[pi];
+    const uint16_t* src = a.kv + static_cast<size_t>(id) * pstride + part + 8 * lane;
     const uint32_t dst = lds_address(&ring[pair % NS][tile][piece * (PCH / WPT)]);
 #pragma unroll
     for (int c = 0; c < LPW; ++c) lds_load16(src + 512 * c, dst + 1024 * c);

@@ -423,3 +423,20 @@ def test_long_contexts_split_decode_attention(metro):
     want = np.stack([g[1] for g in gens])
     assert_logits_close(logits, want, "long contexts")
     check_tokens(toks, want, "long contexts")
+
+
+def test_prefill_attention_past_staged_page_ids(metro):
+    """A context of 8300 tokens (519 pages) runs past the 512 page ids that
+    prefill attention stages in LDS; its last chunks read the rest from the
+    block table."""
+    w = synth.llama_weights(synth.TINY, 6, norm="random")
+    ref = OracleModel(LlamaShape(**synth.TINY), w)
+    rng = np.random.default_rng(26)
+    prompts = [rng.integers(0, 4096, n) for n in (8300, 97)]
+    gens = [ref.generate(p, 2, chunk=512) for p in prompts]
+    with make_model(metro, synth.TINY, w, max_batch=4, max_tokens=2048, max_context=8400,
+                    kv_pool_bytes=64 << 20) as m:
+        logits, toks = gpu_teacher_forced(m, prompts, [g[0][:-1] for g in gens], chunk=512)
+    want = np.stack([g[1] for g in gens])
+    assert_logits_close(logits, want, "prefill past staged page ids")
+    check_tokens(toks, want, "prefill past staged page ids")
