@@ -51,6 +51,13 @@ __device__ __forceinline__ f32x4 mfma_k16(uint2 a, uint2 b, f32x4 c) {
                                                    0, 0, 0);
 }
 
+// 2^x by the hardware instruction (v_exp_f32, about 1 ulp).  exp2f adds a
+// range fix-up (compare, two selects, ldexp) that only matters for results
+// below 2^-126; here x = s - m <= 0 is a softmax exponent, and such a weight
+// is below half an ulp of the running sum (>= 1) and of any output that the
+// weight-1 key contributes to, so it changes no result.
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+
 // p -> (hi, lo) bf16 pairs packed two per word
 __device__ __forceinline__ void split_bf16(float p0, float p1, uint32_t& hi, uint32_t& lo) {
   hi = pack_bf16x2(p0, p1);
@@ -147,7 +154,7 @@ __global__ __launch_bounds__(NW * 64) void attn_decode_kernel(AttnArgs a) {
           m = mn;
           float pv[4];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) pv[r] = exp2f(sv[r] - mn);
+          for (int r = 0; r < 4; ++r) pv[r] = exp2_hw(sv[r] - mn);
           l = l * corr + ((pv[0] + pv[1]) + (pv[2] + pv[3]));
           uint2 hi, lo;
           split_bf16(pv[0], pv[1], hi.x, lo.x);
@@ -371,10 +378,14 @@ __global__ __launch_bounds__(NW * 64) void attn_prefill_kernel(PrefillAttnArgs a
 #pragma unroll
         for (int i = 0; i < KQ; ++i) sc = mfma_k32(kf[pg][i], qf[n][i], sc);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int kpos = (2 * pair + pg) * kPage + 4 * grp + r;
-          sv[pg][r] = all_visible || kpos <= qpos[n] ? sc[r] : -INFINITY;
-        }
+        for (int r = 0; r < 4; ++r) sv[pg][r] = sc[r];
+      }
+      if (!all_visible) {
+#pragma unroll
+        for (int pg = 0; pg < 2; ++pg)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if ((2 * pair + pg) * kPage + 4 * grp + r > qpos[n]) sv[pg][r] = -INFINITY;
       }
       float mp = fmaxf(fmaxf(fmaxf(sv[0][0], sv[0][1]), fmaxf(sv[0][2], sv[0][3])),
                        fmaxf(fmaxf(sv[1][0], sv[1][1]), fmaxf(sv[1][2], sv[1][3])));
@@ -396,7 +407,7 @@ __global__ __launch_bounds__(NW * 64) void attn_prefill_kernel(PrefillAttnArgs a
       for (int pg = 0; pg < 2; ++pg)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          pv[pg][r] = exp2f(fmaf(sv[pg][r], qscale, -m[n]));
+          pv[pg][r] = exp2_hw(fmaf(sv[pg][r], qscale, -m[n]));
           ps += pv[pg][r];
         }
       l[n] += ps;
