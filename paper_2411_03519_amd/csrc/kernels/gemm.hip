@@ -281,10 +281,12 @@ __global__ __launch_bounds__(256) void reduce_parts_kernel(const float* __restri
 // ---------------------------------------------------------------------------
 // Tile shapes: WN x WM waves, each TN x TM tiles of 32 x 32, NS stages of
 // 32-wide k in the LDS ring.  Big: 256 x 256 blocks for long prefill chunks.
-// Mid: 128 x 128 blocks and a deeper ring for batches of a few hundred rows,
-// where there are few blocks and the weight stream must keep more in flight;
-// 8 waves of 32 x 64 (two per SIMD) ran 20-40% faster there than 4 waves of
-// 32 x 128 (one per SIMD), whose MFMA pipe idles at every barrier and LDS wait.
+// Mid: 128 x 128 blocks for batches of 65 to a few hundred rows: 4 waves of
+// 64 x 64 and a ring of 5 stages (80 KiB), so that two workgroups share a CU
+// and one's barrier and LDS waits are the other's MFMA time.  Against 8 waves
+// of 32 x 64 with an 8-stage ring (128 KiB, one workgroup per CU) this took
+// 10-20% less time at M = 80..800 over the 8B and 70B projections (probes
+// with cache-cold weights; 3 stages starved the ring, 4 were 2-10% slower).
 template <int WN_, int WM_, int TN_, int TM_, int NS_>
 struct TileShape {
   static constexpr int WN = WN_, WM = WM_, TN = TN_, TM = TM_, NS = NS_;
@@ -296,7 +298,7 @@ struct TileShape {
   static_assert(NS >= 3, "the pipeline keeps a stage in use, one landed and loads in flight");
 };
 using BigTile = TileShape<4, 2, 2, 4, 5>;
-using MidTile = TileShape<4, 2, 1, 2, 8>;
+using MidTile = TileShape<2, 2, 2, 2, 5>;
 
 __device__ __forceinline__ f32x16 mfma32(uint4 a, uint4 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
@@ -615,10 +617,10 @@ static int device_cus() {
 }
 
 // Kernel choice, from probes over M = 80 .. 12800 at the Llama-3-8B and 70B
-// shapes: the decode kernel up to 64 rows; then 128 x 128 tiles (more blocks,
-// deeper ring) for narrow products, and for wide ones up to 192 rows while
-// their tiles fit one round of the CUs (70B gate/up at M=128: 448 such tiles,
-// 271 us; 224 of 256 x 256, 231 us); 256 x 256 tiles for the LM head and for
+// shapes: the decode kernel up to 64 rows; then 128 x 128 tiles (more blocks)
+// for narrow products, and for wide ones up to 192 rows while their tiles fit
+// one round of two workgroups per CU (70B gate/up at M=80: 448 such tiles,
+// 209 us; 224 of 256 x 256, 251 us); 256 x 256 tiles for the LM head and for
 // long prefill chunks.
 GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, int64_t part_cap) {
   GemmPlan p{GemmKind::kBig, 4, 1, 1, 0};
@@ -634,7 +636,7 @@ GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, int64_t part_cap) {
   if (N >= 65536)
     p.kind = GemmKind::kBig;
   else if (N >= 16384)  // wide products: 128 x 128 tiles only while they fit one round of the CUs
-    p.kind = M <= 192 && mid_tiles <= device_cus() ? GemmKind::kMid : GemmKind::kBig;
+    p.kind = M <= 192 && mid_tiles <= 2 * device_cus() ? GemmKind::kMid : GemmKind::kBig;
   else
     p.kind = M <= kMidMaxRows ? GemmKind::kMid : GemmKind::kBig;
   if (split) {

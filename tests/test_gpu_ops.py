@@ -84,7 +84,8 @@ GEMM_CASES = [(1, 256, 64), (7, 640, 96), (16, 256, 32), (25, 4096, 512), (33, 7
               (300, 4096, 16384),    # 256 x 256 tiles, 2 k slices with a workspace
               (600, 2048, 288),      # 128 x 128 tiles, ragged in both M and N
               (1300, 2048, 4096),    # 256 x 256 tiles, 96 in one partial round: with a workspace 2 k slices each
-              (4300, 1024, 4000)]    # 272 ragged 256 x 256 tiles: the 16 past the first round in 8 k slices
+              (4300, 1024, 4000),    # 272 ragged 256 x 256 tiles: the 16 past the first round in 8 k slices
+              (129, 256, 20480)]     # wide: 320 tiles of 128 x 128 (two workgroups per CU)
 
 
 @pytest.mark.parametrize("M,K,N", GEMM_CASES + [(25, 14336, 512), (3, 1024, 4096)])
@@ -113,7 +114,8 @@ def test_gemm_f32_epilogues(metro, M, K, N, epi, split):
 
 
 @pytest.mark.parametrize("M,K,F", [(3, 256, 688), (25, 256, 48), (64, 512, 112), (96, 256, 688), (130, 384, 80),
-                                   (150, 128, 8192), (25, 128, 14336), (40, 128, 14336), (300, 128, 14336)])
+                                   (150, 128, 8192), (25, 128, 14336), (40, 128, 14336), (300, 128, 14336),
+                                   (100, 256, 14336), (180, 128, 16384)])
 def test_gemm_swiglu_epilogue(metro, M, K, F):
     print(f"swiglu M={M} K={K} F={F}", flush=True)
     rng = np.random.default_rng(M + K + F)
