@@ -864,7 +864,8 @@ def main():
         pf_tflops = pf_flops / (pf_ms / 1e3) / 1e12
         out["roofline_prefill"] = {"bound": "mfma", "achieved": round(pf_tflops, 1), "peak": BF16_PEAK_TFLOPS,
                                    "unit": "TFLOP/s", "frac": round(pf_tflops / BF16_PEAK_TFLOPS, 4),
-                                   "kernel": "gemm gate/up + SwiGLU (prefill chunks)", "launches": pf_launches}
+                                   "kernel": "gemm gate/up + SwiGLU (prefill chunks; a split last round "
+                                             "includes its fixup kernel)", "launches": pf_launches}
     model.close()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.seed)

@@ -46,7 +46,7 @@ metro_status metro_op_pack_weight(const uint16_t* W_rowmajor, int32_t ld, int32_
  * workspace: NULL, or device fp32 [8][M][N]; when given, a decode-sized GEMM
  * (M <= 1024, epilogue 0 or 1) may run the k-split form the model uses (slices in
  * the workspace, then summed in slice order into the output), and a larger one
- * (epilogue 0 or 1) may split the 256 x 256 tiles of its last, partly filled
+ * (any epilogue) may split the 256 x 256 tiles of its last, partly filled
  * round of workgroups over k the same way.  Its contents on return are
  * unspecified.
  * Errors: E_INVAL for shapes outside these rules or a NULL operand. */

@@ -522,7 +522,7 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
     for (int i = 0; i < TN; ++i) {
       const int nb = n0 + wn * TN * 32 + i * 32;  // 32-row tile of W
       if (nb >= N) continue;
-      if (EPI == kEpiSwiGLU) {
+      if (EPI == kEpiSwiGLU && !raw) {
         // the tile is two 16-row blocks of 8 gate rows then the 8 matching up
         // rows: the lane's rows 8q + 4(l/32) + i of q = 0, 2 (gate) pair with
         // those of q = 1, 3 (up) in the same lane
@@ -573,6 +573,44 @@ __global__ __launch_bounds__(256) void gemm_tail_fixup_kernel(const float* __res
     a.w += v.w;
   }
   store_tile<EPI>(f32x4{a.x, a.y, a.z, a.w}, m, n, out, ldo);
+}
+
+// The same for the gate/up product: a tile's BN rows of W are BN/16 blocks of
+// 8 gate rows then the 8 matching up rows; output column j of the tile (of
+// BN/2) takes gate row 16(j/8) + j%8 and up row 16(j/8) + 8 + j%8, summed over
+// the slices in slice order, then out_bf16[m][n0/2 + j] = bf16(silu(gate) *
+// up).  Workgroup (t, y) covers rows 8y .. 8y+7 of tail tile t, a thread 4
+// consecutive output columns.
+template <class S>
+__global__ __launch_bounds__(256) void gemm_tail_fixup_swiglu_kernel(const float* __restrict__ part, int tail_first,
+                                                                     int split, int M, int N,
+                                                                     uint16_t* __restrict__ out, int ldo) {
+  constexpr int kCols = S::BN / 8;  // threads per tile row (4 of the BN/2 output columns each)
+  static_assert(256 % kCols == 0 && S::BM % (256 / kCols) == 0, "rows of a tile split evenly");
+  const int i = blockIdx.y * (256 / kCols) + threadIdx.x / kCols;
+  const int j = 4 * (threadIdx.x % kCols);
+  const int wg = 16 * (j / 8) + j % 8;  // gate row of output column j within the tile
+  int m0, n0;
+  tile_origin<S>(tail_first + blockIdx.x, M, N, m0, n0);
+  const int m = m0 + i;
+  if (m >= M || n0 + wg >= N) return;
+  const float* p = part + static_cast<size_t>(blockIdx.x) * split * S::BM * S::BN + i * S::BN + wg;
+  float4 g = *reinterpret_cast<const float4*>(p);
+  float4 u = *reinterpret_cast<const float4*>(p + 8);
+  for (int sl = 1; sl < split; ++sl) {
+    const float* q = p + static_cast<size_t>(sl) * S::BM * S::BN;
+    const float4 gv = *reinterpret_cast<const float4*>(q);
+    const float4 uv = *reinterpret_cast<const float4*>(q + 8);
+    g.x += gv.x;
+    g.y += gv.y;
+    g.z += gv.z;
+    g.w += gv.w;
+    u.x += uv.x;
+    u.y += uv.y;
+    u.z += uv.z;
+    u.w += uv.w;
+  }
+  store_swiglu(f32x4{g.x, g.y, g.z, g.w}, f32x4{u.x, u.y, u.z, u.w}, m, n0 / 2 + j, out, ldo);
 }
 
 // ---------------------------------------------------------------------------
@@ -647,7 +685,7 @@ GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, int64_t part_cap) {
   // Last round of 256 x 256 tiles: with r tiles left for C CUs, cut each into
   // S k slices (S a power of two, r * S <= C, slices multiples of 128), so
   // that round takes 1/S of a tile's time; the fixup kernel adds the slices.
-  if (p.kind == GemmKind::kBig && p.ks == 1 && can_split && epilogue != kEpiSwiGLU) {
+  if (p.kind == GemmKind::kBig && p.ks == 1 && can_split) {
     const int tiles = ((N + BigTile::BN - 1) / BigTile::BN) * ((M + BigTile::BM - 1) / BigTile::BM);
     const int cus = device_cus(), r = tiles % cus;
     int sp = 1;
@@ -690,7 +728,10 @@ static void launch_tiled(const uint16_t* X, int ldx, const uint16_t* W, int Kp, 
   launch_kernel((gemm_tiled_kernel<S, EPI>), dim3(blocks, ks), dim3(S::NTH), 0, s, X, ldx, W, Kp, M, N, outf, outb,
                 ldo, part, tail_first, tail_split);
   if (tail_split > 1) {
-    if constexpr (EPI != kEpiSwiGLU)
+    if constexpr (EPI == kEpiSwiGLU)
+      launch_kernel((gemm_tail_fixup_swiglu_kernel<S>), dim3(tiles - tail_first, S::BM / (2048 / S::BN)),
+                    dim3(256), 0, s, part, tail_first, tail_split, M, N, outb, ldo);
+    else
       launch_kernel((gemm_tail_fixup_kernel<S, EPI>), dim3(tiles - tail_first, S::BM / (1024 / S::BN)), dim3(256),
                     0, s, part, tail_first, tail_split, M, N, outf, ldo);
   }

@@ -11,10 +11,13 @@ namespace metro {
 
 // --- launch timing ----------------------------------------------------------
 
-// Events that the next kernel dispatch records its own start and end into
-// (hipExtLaunchKernel puts them on the dispatch packet, so the interval is the
-// kernel's execution alone, as a kernel trace reports it).  Set by the runtime
-// around one launcher call while that kernel class is timed; null otherwise.
+// Events that the kernel dispatches of one launcher call record their start
+// and end into (hipExtLaunchKernel puts them on the dispatch packet, so the
+// interval is the kernels' execution, as a kernel trace reports it).  Set by
+// the runtime around one launcher call while that kernel class is timed; null
+// otherwise.  The first dispatch records the start; every dispatch records the
+// end, so a launcher that issues a second kernel (the fixup of a split GEMM)
+// is timed from the start of its first kernel to the end of its last.
 struct LaunchEvents {
   hipEvent_t start = nullptr;
   hipEvent_t stop = nullptr;
@@ -24,6 +27,7 @@ extern thread_local LaunchEvents launch_events;
 template <typename F, typename... Args>
 inline void launch_kernel(F kernel, dim3 grid, dim3 block, uint32_t shmem, hipStream_t s, Args... args) {
   hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, launch_events.start, launch_events.stop, 0u, args...);
+  launch_events.start = nullptr;
 }
 
 // --- elementwise / row kernels (elementwise.hip) ---------------------------

@@ -299,8 +299,8 @@ metro_status launch_layers(metro_model* m, int T, const int32_t* tok_dev, const 
            metro::launch_rmsnorm(m->x, d, L.ffn_norm, c.rms_eps, m->h, d, T, d, m->parts, xp, s));
     int gp = 0;
     LAUNCH(m, METRO_K_GEMM_GATE_UP, s,
-           metro::launch_gemm(m->h, d, L.wgu, d, T, 2 * c.ffn_dim, metro::kEpiSwiGLU, nullptr, m->a, m->Fp, nullptr,
-                              0, &gp, s));
+           metro::launch_gemm(m->h, d, L.wgu, d, T, 2 * c.ffn_dim, metro::kEpiSwiGLU, nullptr, m->a, m->Fp, m->parts,
+                              m->parts_cap, &gp, s));
     LAUNCH(m, METRO_K_GEMM_DOWN, s,
            metro::launch_gemm(m->a, m->Fp, L.wdown, m->Fp, T, d, metro::kEpiAddF32, m->x, nullptr, d, m->parts,
                               m->parts_cap, &xp, s));

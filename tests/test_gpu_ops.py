@@ -115,9 +115,12 @@ def test_gemm_f32_epilogues(metro, M, K, N, epi, split):
 
 @pytest.mark.parametrize("M,K,F", [(3, 256, 688), (25, 256, 48), (64, 512, 112), (96, 256, 688), (130, 384, 80),
                                    (150, 128, 8192), (25, 128, 14336), (40, 128, 14336), (300, 128, 14336),
-                                   (100, 256, 14336), (180, 128, 16384)])
-def test_gemm_swiglu_epilogue(metro, M, K, F):
-    print(f"swiglu M={M} K={K} F={F}", flush=True)
+                                   (100, 256, 14336), (180, 128, 16384),
+                                   (300, 256, 8192),     # 128 tiles of 256 x 256: with a workspace 2 k slices each
+                                   (1300, 256, 2048)])   # 96 ragged tiles: with a workspace 2 k slices each
+@pytest.mark.parametrize("split", [False, True])
+def test_gemm_swiglu_epilogue(metro, M, K, F, split):
+    print(f"swiglu M={M} K={K} F={F} split={split}", flush=True)
     rng = np.random.default_rng(M + K + F)
     X = rand_bf16(rng, (M, K))
     Wg = rand_bf16(rng, (F, K), 0.1)
@@ -128,7 +131,8 @@ def test_gemm_swiglu_epilogue(metro, M, K, F):
         packed[16 * b + 8:16 * b + 16] = Wu[8 * b:8 * b + 8]
     ldo = (F + 127) // 128 * 128
     out = torch.zeros((M, ldo), dtype=torch.int16, device="cuda")
-    metro.op_gemm(dev_u16(X), pack_dev(metro, packed, K, K), M, 2 * F, K, 2, out, ldo)
+    ws = torch.full((8, M, 2 * F), float("nan"), device="cuda") if split else None
+    metro.op_gemm(dev_u16(X), pack_dev(metro, packed, K, K), M, 2 * F, K, 2, out, ldo, workspace=ws)
     torch.cuda.synchronize()
     got = bf16_bits_to_f64(out.cpu().numpy().view(np.uint16))
     xf, wg, wu = bf16_bits_to_f64(X), bf16_bits_to_f64(Wg), bf16_bits_to_f64(Wu)

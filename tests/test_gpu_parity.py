@@ -440,3 +440,24 @@ def test_prefill_attention_past_staged_page_ids(metro):
     want = np.stack([g[1] for g in gens])
     assert_logits_close(logits, want, "prefill past staged page ids")
     check_tokens(toks, want, "prefill past staged page ids")
+
+
+def test_launch_timing_spans_split_gemm_fixup(metro):
+    """Launch timing of a GEMM whose last round is split over k covers the
+    tiled kernel and its fixup kernel: a 1100-row gate/up (256 x 256 tiles, 30
+    of them split in two) is timed no shorter than a 1000-row one (128 x 128
+    tiles, no split), not as the fixup alone."""
+    w = synth.llama_weights(synth.TINY, 9)
+    rng = np.random.default_rng(29)
+    per_launch = {}
+    for n in (1000, 1100):
+        with make_model(metro, synth.TINY, w, max_batch=4, max_tokens=1200, max_context=1200) as m:
+            s = m.seq_open()
+            m.prefill_chunk([s], [rng.integers(0, 4096, 64)])   # warm up
+            t = m.seq_open()
+            m.profile_start("gemm_gate_up", "prefill")
+            m.prefill_chunk([t], [rng.integers(0, 4096, n)])
+            ms, launches = m.profile_stop()
+            assert launches == synth.TINY["n_layers"]
+            per_launch[n] = ms / launches
+    assert per_launch[1100] >= 0.6 * per_launch[1000], per_launch
