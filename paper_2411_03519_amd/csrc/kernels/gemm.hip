@@ -656,9 +656,10 @@ static int device_cus() {
 
 // Kernel choice, from probes over M = 80 .. 12800 at the Llama-3-8B and 70B
 // shapes: the decode kernel up to 64 rows; then 128 x 128 tiles (more blocks)
-// for narrow products, and for wide ones up to 192 rows while their tiles fit
-// one round of two workgroups per CU (70B gate/up at M=80: 448 such tiles,
-// 209 us; 224 of 256 x 256, 251 us); 256 x 256 tiles for the LM head and for
+// for narrow products, and for wide ones up to 192 rows while their tiles
+// number at most the CUs (in the 70B model at M=128 gate/up took 242 us as 448
+// such tiles against 203 us as 224 of 256 x 256, although cache-cold probes
+// had ranked them the other way); 256 x 256 tiles for the LM head and for
 // long prefill chunks.
 GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, int64_t part_cap) {
   GemmPlan p{GemmKind::kBig, 4, 1, 1, 0};
@@ -674,7 +675,7 @@ GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, int64_t part_cap) {
   if (N >= 65536)
     p.kind = GemmKind::kBig;
   else if (N >= 16384)  // wide products: 128 x 128 tiles only while they fit one round of the CUs
-    p.kind = M <= 192 && mid_tiles <= 2 * device_cus() ? GemmKind::kMid : GemmKind::kBig;
+    p.kind = M <= 192 && mid_tiles <= device_cus() ? GemmKind::kMid : GemmKind::kBig;
   else
     p.kind = M <= kMidMaxRows ? GemmKind::kMid : GemmKind::kBig;
   if (split) {
