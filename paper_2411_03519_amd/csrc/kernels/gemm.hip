@@ -299,6 +299,13 @@ struct TileShape {
 };
 using BigTile = TileShape<4, 2, 2, 4, 5>;
 using MidTile = TileShape<2, 2, 2, 2, 5>;
+// Wide: 256 rows of W x 128 activation rows, 8 waves of 64 x 64, 5 stages
+// (120 KiB), for wide products at up to 256 rows when 128 x 128 tiles would be
+// too many for one round: against 256 x 256 tiles it does no matrix work on
+// absent rows at M <= 128 (70B gate/up at M=128 in a probe: 202 against 267
+// us; the LM head at M=80: 225 against 268) and gives twice the workgroups at
+// M = 129..256 (8B gate/up at M=192: 78 against 91 us).
+using WideTile = TileShape<4, 2, 2, 2, 5>;
 
 __device__ __forceinline__ f32x16 mfma32(uint4 a, uint4 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
@@ -659,8 +666,9 @@ static int device_cus() {
 // for narrow products, and for wide ones up to 192 rows while their tiles
 // number at most the CUs (in the 70B model at M=128 gate/up took 242 us as 448
 // such tiles against 203 us as 224 of 256 x 256, although cache-cold probes
-// had ranked them the other way); 256 x 256 tiles for the LM head and for
-// long prefill chunks.
+// had ranked them the other way); else 256 x 128 tiles for wide products up to
+// 128 rows, or up to 256 while they number at most the CUs; 256 x 256 tiles
+// for the rest and for long prefill chunks.
 GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, int64_t part_cap) {
   GemmPlan p{GemmKind::kBig, 4, 1, 1, 0};
   const bool can_split = part_cap > 0;
@@ -671,27 +679,32 @@ GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, int64_t part_cap) {
     if (split) p.ks = gemm_k_splits(N / (16 * p.nt), p.nt == 2 ? 512 : 256, M, Kp);
     return p;
   }
-  const int mid_tiles = ((N + MidTile::BN - 1) / MidTile::BN) * ((M + MidTile::BM - 1) / MidTile::BM);
-  if (N >= 65536)
-    p.kind = GemmKind::kBig;
-  else if (N >= 16384)  // wide products: 128 x 128 tiles only while they fit one round of the CUs
-    p.kind = M <= 192 && mid_tiles <= device_cus() ? GemmKind::kMid : GemmKind::kBig;
-  else
+  auto tiles_of = [&](int bn, int bm) { return ((N + bn - 1) / bn) * ((M + bm - 1) / bm); };
+  const int mid_tiles = tiles_of(MidTile::BN, MidTile::BM), wide_tiles = tiles_of(WideTile::BN, WideTile::BM);
+  const int cus = device_cus();
+  if (N >= 16384) {  // wide products: gate/up and the LM head
+    if (M <= 192 && mid_tiles <= cus)
+      p.kind = GemmKind::kMid;
+    else if (M <= WideTile::BM || (M <= 2 * WideTile::BM && wide_tiles <= cus))
+      p.kind = GemmKind::kWide;
+    else
+      p.kind = GemmKind::kBig;
+  } else {
     p.kind = M <= kMidMaxRows ? GemmKind::kMid : GemmKind::kBig;
-  if (split) {
-    const bool mid = p.kind == GemmKind::kMid;
-    const int bn = mid ? MidTile::BN : BigTile::BN, bm = mid ? MidTile::BM : BigTile::BM;
-    p.ks = gemm_k_splits(((N + bn - 1) / bn) * ((M + bm - 1) / bm), mid ? 512 : 256, M, Kp);
   }
-  // Last round of 256 x 256 tiles: with r tiles left for C CUs, cut each into
-  // S k slices (S a power of two, r * S <= C, slices multiples of 128), so
-  // that round takes 1/S of a tile's time; the fixup kernel adds the slices.
-  if (p.kind == GemmKind::kBig && p.ks == 1 && can_split) {
-    const int tiles = ((N + BigTile::BN - 1) / BigTile::BN) * ((M + BigTile::BM - 1) / BigTile::BM);
-    const int cus = device_cus(), r = tiles % cus;
+  const int bn = p.kind == GemmKind::kMid ? MidTile::BN : p.kind == GemmKind::kWide ? WideTile::BN : BigTile::BN;
+  const int bm = p.kind == GemmKind::kMid ? MidTile::BM : p.kind == GemmKind::kWide ? WideTile::BM : BigTile::BM;
+  const int tiles = tiles_of(bn, bm);
+  if (split) p.ks = gemm_k_splits(tiles, p.kind == GemmKind::kMid ? 512 : 256, M, Kp);
+  // Last round of 256-row tiles (one workgroup per CU): with r tiles left for
+  // C CUs, cut each into S k slices (S a power of two, r * S <= C, slices
+  // multiples of 128), so that round takes 1/S of a tile's time; the fixup
+  // kernel adds the slices.
+  if (p.kind != GemmKind::kMid && p.ks == 1 && can_split) {
+    const int r = tiles % cus;
     int sp = 1;
     while (r > 0 && sp < 8 && r * (2 * sp) <= cus && (Kp / (2 * sp)) % 128 == 0) sp *= 2;
-    if (sp > 1 && static_cast<int64_t>(r) * sp * BigTile::BM * BigTile::BN <= part_cap) {
+    if (sp > 1 && static_cast<int64_t>(r) * sp * bm * bn <= part_cap) {
       p.tail_split = sp;
       p.tail_first = tiles - r;
     }
@@ -752,6 +765,9 @@ static hipError_t launch_epi(const GemmPlan& p, const uint16_t* X, int ldx, cons
       break;
     case GemmKind::kMid:
       launch_tiled<MidTile, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, p.ks, s);
+      break;
+    case GemmKind::kWide:
+      launch_tiled<WideTile, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, p.ks, s, p.tail_split, p.tail_first);
       break;
     case GemmKind::kBig:
       launch_tiled<BigTile, EPI>(X, ldx, W, Kp, M, N, outf, outb, ldo, part, p.ks, s, p.tail_split, p.tail_first);

@@ -135,12 +135,14 @@ struct RopeKV {
 // (M <= kSplitMaxRows, fp32 epilogue) may split K over workgroups: it then
 // writes *n_parts > 0 slices part[s][m][n] ([ks][M][N], ks <= 8) instead of
 // applying the epilogue, and the consumer sums them in slice order.  A larger
-// one with 256 x 256 tiles and an fp32 epilogue may split only the tiles of
-// its last, partly filled round (up to CUs * 256 * 256 floats of part), and
-// completes them itself (*n_parts stays 0).
-// Kernel choice: up to 64 rows the weight-streaming decode GEMM; up to
-// kMidMaxRows the tiled GEMM with 128 x 128 blocks, above it 256 x 256 blocks.
-enum class GemmKind { kSkinny, kMid, kBig };
+// one with 256-row tiles (any epilogue) may split only the tiles of its last,
+// partly filled round (up to CUs * 256 * 256 floats of part), and completes
+// them itself (*n_parts stays 0).
+// Kernel choice (plan_gemm): up to 64 rows the weight-streaming decode GEMM;
+// then the tiled GEMM with 128 x 128 blocks (narrow products up to
+// kMidMaxRows rows, wide ones while they fit the CUs), 256 (W rows) x 128
+// blocks (wide products at up to 256 rows otherwise), or 256 x 256 blocks.
+enum class GemmKind { kSkinny, kMid, kWide, kBig };
 struct GemmPlan {
   GemmKind kind;
   int nt;          // row tiles per wave (decode kernel)

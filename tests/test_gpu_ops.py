@@ -74,9 +74,11 @@ def test_pack_weight_rejects_bad_shapes(metro):
 
 
 # (M, K, N): decode kernel at M <= 64; above it the tiled kernel with 128 x 128
-# blocks (narrow products up to 1000 rows, wide ones up to 192) or 256 x 256
-# blocks, with or without a k split (plan_gemm); the last two split only the
-# tiles of the last round of workgroups (on 256 CUs) when given a workspace
+# blocks (narrow products up to 1000 rows, wide ones up to 192 while they fit
+# the CUs), 256 x 128 blocks (wide products otherwise, up to 256 rows) or 256 x
+# 256 blocks, with or without a k split (plan_gemm); the 256-row tiles split
+# only the tiles of the last round of workgroups (on 256 CUs) when given a
+# workspace
 GEMM_CASES = [(1, 256, 64), (7, 640, 96), (16, 256, 32), (25, 4096, 512), (33, 768, 160), (64, 384, 1376),
               (65, 256, 160), (200, 1152, 416), (129, 128, 96), (300, 4096, 256), (1100, 384, 160),
               (200, 256, 16384), (70, 128, 65536),
@@ -85,7 +87,10 @@ GEMM_CASES = [(1, 256, 64), (7, 640, 96), (16, 256, 32), (25, 4096, 512), (33, 7
               (600, 2048, 288),      # 128 x 128 tiles, ragged in both M and N
               (1300, 2048, 4096),    # 256 x 256 tiles, 96 in one partial round: with a workspace 2 k slices each
               (4300, 1024, 4000),    # 272 ragged 256 x 256 tiles: the 16 past the first round in 8 k slices
-              (129, 256, 20480)]     # wide: 320 tiles of 128 x 128 (two workgroups per CU)
+              (129, 256, 20480),     # wide: 160 tiles of 256 x 128 over two row blocks
+              (100, 256, 69632),     # wide: 272 tiles of 256 x 128, the 16 past the first round in 2 k slices
+              (200, 256, 16384),     # wide: 128 tiles of 256 x 128, with a workspace 2 k slices each
+              (90, 128, 57344)]      # wide: 224 tiles of 256 x 128 (70B gate/up-sized, one round)
 
 
 @pytest.mark.parametrize("M,K,N", GEMM_CASES + [(25, 14336, 512), (3, 1024, 4096)])
@@ -117,7 +122,9 @@ def test_gemm_f32_epilogues(metro, M, K, N, epi, split):
                                    (150, 128, 8192), (25, 128, 14336), (40, 128, 14336), (300, 128, 14336),
                                    (100, 256, 14336), (180, 128, 16384),
                                    (300, 256, 8192),     # 128 tiles of 256 x 256: with a workspace 2 k slices each
-                                   (1300, 256, 2048)])   # 96 ragged tiles: with a workspace 2 k slices each
+                                   (1300, 256, 2048),    # 96 ragged tiles: with a workspace 2 k slices each
+                                   (90, 128, 28672),     # 224 tiles of 256 x 128 (70B gate/up-sized)
+                                   (200, 256, 14336)])   # 224 tiles of 256 x 128 over two row blocks
 @pytest.mark.parametrize("split", [False, True])
 def test_gemm_swiglu_epilogue(metro, M, K, F, split):
     print(f"swiglu M={M} K={K} F={F} split={split}", flush=True)
