@@ -351,7 +351,7 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
                                                             const uint16_t* __restrict__ W, int Kp, int M, int N,
                                                             float* __restrict__ outf, uint16_t* __restrict__ outb,
                                                             int ldo, float* __restrict__ part, int tail_first,
-                                                            int tail_split) {
+                                                            int tail_split, RopeKV rk) {
   constexpr int WM = S::WM, TN = S::TN, TM = S::TM, NS = S::NS, LPW = S::LPW;
   __shared__ uint4 wring[NS][S::WT * 64];  // per stage: WT tiles of 16 x 32 (1 KiB each)
   __shared__ uint4 xring[NS][S::XT * 64];
@@ -484,6 +484,31 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
   // group of activation rows, then adds and stores them (one round trip per
   // group rather than per value); the scheduling barrier keeps the compiler
   // from hoisting every group's loads at once.
+  if constexpr (EPI == kEpiRopeKV) {
+    // (launched without k slices) each 16-row block of a 32-row tile holds 8
+    // dims of a head's first half, then the matching 8 of its second half in
+    // the rotate-half interleave: the lane's rows 8q + 4(l/32) + i of q = 0, 2
+    // pair with those of q = 1, 3 in the same lane
+#pragma unroll
+    for (int j = 0; j < TM; ++j) {
+      const int m = m0 + wm * TM * 32 + j * 32 + lr;
+      if (m >= M) continue;
+#pragma unroll
+      for (int i = 0; i < TN; ++i) {
+        const int nb = n0 + wn * TN * 32 + i * 32;
+        if (nb >= N) continue;
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int r0 = nb + 16 * u;  // first W row of the 16-row block
+          const f32x4 a{acc[i][j][8 * u], acc[i][j][8 * u + 1], acc[i][j][8 * u + 2], acc[i][j][8 * u + 3]};
+          const f32x4 b{acc[i][j][8 * u + 4], acc[i][j][8 * u + 5], acc[i][j][8 * u + 6], acc[i][j][8 * u + 7]};
+          store_rope_kv(a, b, m, r0 / rk.hd, 8 * ((r0 % rk.hd) / 16) + 4 * lh, rk);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    }
+    return;
+  }
   const bool raw = KS > 1;
   float* const pout = unit >= 0 ? part + static_cast<size_t>(unit) * S::BM * S::BN
                       : raw     ? part + static_cast<size_t>(slice) * M * N
@@ -740,7 +765,7 @@ static void launch_tiled(const uint16_t* X, int ldx, const uint16_t* W, int Kp, 
   const int tiles = ((N + S::BN - 1) / S::BN) * ((M + S::BM - 1) / S::BM);
   const int blocks = tail_split > 1 ? tail_first + (tiles - tail_first) * tail_split : tiles;
   launch_kernel((gemm_tiled_kernel<S, EPI>), dim3(blocks, ks), dim3(S::NTH), 0, s, X, ldx, W, Kp, M, N, outf, outb,
-                ldo, part, tail_first, tail_split);
+                ldo, part, tail_first, tail_split, RopeKV{});
   if (tail_split > 1) {
     if constexpr (EPI == kEpiSwiGLU)
       launch_kernel((gemm_tail_fixup_swiglu_kernel<S>), dim3(tiles - tail_first, S::BM / (2048 / S::BN)),
@@ -798,10 +823,21 @@ hipError_t launch_gemm(const uint16_t* X, int ldx, const uint16_t* W, int Kp, in
 // 2 row tiles per wave, 4 waves, K whole: 14.4 us at M=25, N=6144, K=4096
 // (with 4 k slices the product alone takes 13.1 us, but the slice sums then
 // cost a RoPE kernel of 5.2 us)
+bool gemm_rope_kv_fused(int M, int N, int Kp) {
+  return M <= kRopeKVMaxRows || plan_gemm(M, N, Kp, kEpiStoreF32, 0).kind == GemmKind::kBig;
+}
+
 hipError_t launch_gemm_rope_kv(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, const RopeKV& rk,
                                hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  if (M > kRopeKVMaxRows || N != (rk.nq + 2 * rk.nkv) * rk.hd || rk.hd % 32 || N % 32) return hipErrorInvalidValue;
+  if (!gemm_rope_kv_fused(M, N, Kp) || N != (rk.nq + 2 * rk.nkv) * rk.hd || rk.hd % 32 || N % 32)
+    return hipErrorInvalidValue;
+  if (M > kRopeKVMaxRows) {  // 256 x 256 tiles over all of K (no workspace: no split of the last round)
+    const int tiles = ((N + BigTile::BN - 1) / BigTile::BN) * ((M + BigTile::BM - 1) / BigTile::BM);
+    launch_kernel((gemm_tiled_kernel<BigTile, kEpiRopeKV>), dim3(tiles, 1), dim3(BigTile::NTH), 0, s, X, ldx, W, Kp,
+                  M, N, nullptr, nullptr, 0, nullptr, 0, 1, rk);
+    return hipGetLastError();
+  }
   constexpr int NT = 2, NW = 4;
   auto go = [&](auto mt) {
     constexpr int MT = decltype(mt)::value;

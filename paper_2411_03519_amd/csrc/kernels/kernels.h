@@ -156,10 +156,13 @@ GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, int64_t part_cap);
 hipError_t launch_gemm(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, int epilogue,
                        float* out_f32, uint16_t* out_bf16, int ldo, float* part, int64_t part_cap, int* n_parts,
                        hipStream_t s);
-// QKV projection of at most kRopeKVMaxRows rows (N = (nq + 2 nkv) * hd) with
-// RoPE and the KV cache write in its epilogue, in place of launch_gemm +
-// launch_rope_kv; K is not split, so no slice sums are left.
+// QKV projection (N = (nq + 2 nkv) * hd) with RoPE and the KV cache write in
+// its epilogue, in place of launch_gemm + launch_rope_kv, for the shapes
+// gemm_rope_kv_fused accepts: up to kRopeKVMaxRows rows (decode kernel), or
+// the batches plan_gemm gives 256 x 256 tiles (prefill chunks); K is not split,
+// so no slice sums are left.  hipErrorInvalidValue for other shapes.
 constexpr int kRopeKVMaxRows = 64;
+bool gemm_rope_kv_fused(int M, int N, int Kp);
 hipError_t launch_gemm_rope_kv(const uint16_t* X, int ldx, const uint16_t* W, int Kp, int M, int N, const RopeKV& rk,
                                hipStream_t s);
 // Apply the fp32 epilogue to KS slices: out (=|+=) sum_s part[s].

@@ -271,7 +271,7 @@ metro_status launch_layers(metro_model* m, int T, const int32_t* tok_dev, const 
     uint16_t* kv_l = m->kv + static_cast<size_t>(l) * m->layer_stride;
     LAUNCH(m, METRO_K_RMSNORM, s,
            metro::launch_rmsnorm(m->x, d, L.attn_norm, c.rms_eps, m->h, d, T, d, m->parts, xp, s));
-    if (T <= metro::kRopeKVMaxRows) {
+    if (metro::gemm_rope_kv_fused(T, m->qkv_n, d)) {
       const metro::RopeKV rk{pos, slot, m->rope, m->q, kv_l, c.n_heads, c.n_kv_heads, c.head_dim};
       LAUNCH(m, METRO_K_GEMM_QKV, s, metro::launch_gemm_rope_kv(m->h, d, L.wqkv, d, T, m->qkv_n, rk, s));
     } else {
