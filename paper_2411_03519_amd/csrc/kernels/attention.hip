@@ -387,19 +387,34 @@ __global__ __launch_bounds__(NW * 64) void attn_prefill_kernel(PrefillAttnArgs a
           for (int r = 0; r < 4; ++r)
             if ((2 * pair + pg) * kPage + 4 * grp + r > qpos[n]) sv[pg][r] = -INFINITY;
       }
-      float mp = fmaxf(fmaxf(fmaxf(sv[0][0], sv[0][1]), fmaxf(sv[0][2], sv[0][3])),
-                       fmaxf(fmaxf(sv[1][0], sv[1][1]), fmaxf(sv[1][2], sv[1][3])));
-      mp = max_xor32(max_xor16(mp)) * qscale;  // in log2 units
       // The reference max m only moves when some column's max exceeds it by
       // more than 8 (a factor 2^8): o and l carry the same scale, so their
-      // quotient is unchanged, and p = 2^(s - m) stays below 2^8.
-      if (__any(mp > m[n] + 8.f)) {
+      // quotient is unchanged, and p = 2^(s - m) stays below 2^8.  Whether any
+      // score does is read off the exponents s*scale - m themselves, so the
+      // column maxima (a cross-lane reduction) are formed only when m moves.
+      float e[2][4];
+      bool grow = false;
+#pragma unroll
+      for (int pg = 0; pg < 2; ++pg)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          e[pg][r] = fmaf(sv[pg][r], qscale, -m[n]);
+          grow |= e[pg][r] > 8.f;
+        }
+      if (__any(grow)) {
+        float mp = fmaxf(fmaxf(fmaxf(sv[0][0], sv[0][1]), fmaxf(sv[0][2], sv[0][3])),
+                         fmaxf(fmaxf(sv[1][0], sv[1][1]), fmaxf(sv[1][2], sv[1][3])));
+        mp = max_xor32(max_xor16(mp)) * qscale;  // in log2 units
         const float mn = fmaxf(m[n], mp);
         const float corr = exp2f(m[n] - mn);
         m[n] = mn;
         l[n] *= corr;
 #pragma unroll
         for (int t = 0; t < NT; ++t) o[n][t] *= corr;
+#pragma unroll
+        for (int pg = 0; pg < 2; ++pg)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) e[pg][r] = fmaf(sv[pg][r], qscale, -m[n]);
       }
       float pv[2][4];
       float ps = 0.f;
@@ -407,7 +422,7 @@ __global__ __launch_bounds__(NW * 64) void attn_prefill_kernel(PrefillAttnArgs a
       for (int pg = 0; pg < 2; ++pg)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          pv[pg][r] = exp2_hw(fmaf(sv[pg][r], qscale, -m[n]));
+          pv[pg][r] = exp2_hw(e[pg][r]);
           ps += pv[pg][r];
         }
       l[n] += ps;
