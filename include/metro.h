@@ -133,7 +133,12 @@ const char* metro_status_name(int32_t status);
  * N(0, 0.02) values rounded to bf16, norm gains with 1.0 (the random
  * initialisation used when no checkpoint is loaded).  metro_load_weight then
  * replaces any tensor.  On success *out owns everything; free it with
- * metro_destroy_model.  Errors: E_INVAL (cfg), E_NOMEM, E_HIP. */
+ * metro_destroy_model.  Debugging: with the environment variable
+ * METRO_SYNC_CHECK set to a non-zero integer when the model is created, every
+ * kernel launch of the model is followed by a wait on its stream and an error
+ * check, so that a failing kernel is reported (E_HIP, metro_last_error) by
+ * the launch that ran it; results are unchanged, calls become synchronous.
+ * Errors: E_INVAL (cfg), E_NOMEM, E_HIP. */
 metro_status metro_create_model(const metro_config* cfg, uint64_t init_seed, metro_model** out);
 
 /* Free every device and host resource of the model (NULL is a no-op).

@@ -110,6 +110,7 @@ struct metro_model {
   hipEvent_t desc_ev[kRing] = {};
   int ring = 0;
   bool poisoned = false;
+  bool sync_check = false;  // METRO_SYNC_CHECK: wait for and check every launch
   // launch timing (metro_profile_*)
   int prof_cls = -1;
   int prof_phase = 0;
@@ -163,6 +164,10 @@ metro_status launch(metro_model* m, int cls, hipStream_t s, const char* what, Fn
   }
   hipError_t e = fn();
   metro::launch_events = {};
+  if (e == hipSuccess && m->sync_check) {  // debugging: a failing kernel is named by its own launch
+    e = hipStreamSynchronize(s);
+    if (e == hipSuccess) e = hipGetLastError();
+  }
   if (e != hipSuccess) return hip_fail(m, e, what);
   if (timed) m->prof_used[i] = 1;
   return METRO_OK;
@@ -396,6 +401,7 @@ metro_status metro_create_model(const metro_config* cfg, uint64_t init_seed, met
     free_model(m);
     return s2;
   };
+  if (const char* sc = std::getenv("METRO_SYNC_CHECK")) m->sync_check = std::atoi(sc) != 0;
   hipError_t e = hipGetDevice(&m->device);
   if (e != hipSuccess) return bail(hip_fail(nullptr, e, "hipGetDevice"));
 

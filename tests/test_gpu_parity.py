@@ -461,3 +461,24 @@ def test_launch_timing_spans_split_gemm_fixup(metro):
             assert launches == synth.TINY["n_layers"]
             per_launch[n] = ms / launches
     assert per_launch[1100] >= 0.6 * per_launch[1000], per_launch
+
+
+def test_sync_check_mode_gives_the_same_results(metro, monkeypatch):
+    """A model created with METRO_SYNC_CHECK=1 waits for and checks every
+    launch; its prefill and decode outputs equal those of a normal model."""
+    w = synth.llama_weights(synth.TINY, 10)
+    rng = np.random.default_rng(30)
+    prompts = [rng.integers(0, 4096, n) for n in (45, 130)]
+    outs = []
+    for flag in ("0", "1"):
+        monkeypatch.setenv("METRO_SYNC_CHECK", flag)
+        with make_model(metro, synth.TINY, w) as m:
+            seqs = [m.seq_open() for _ in prompts]
+            lg = torch.empty(2, m.vocab, device="cuda")
+            nt = torch.empty(2, dtype=torch.int32, device="cuda")
+            m.prefill_chunk(seqs, prompts, lg, nt)
+            lg2 = torch.empty_like(lg)
+            m.decode_step(seqs, nt, lg2)
+            outs.append((lg.cpu().numpy(), lg2.cpu().numpy()))
+    np.testing.assert_array_equal(outs[0][0], outs[1][0])
+    np.testing.assert_array_equal(outs[0][1], outs[1][1])
