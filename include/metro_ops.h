@@ -54,6 +54,18 @@ metro_status metro_op_gemm(const uint16_t* X, int32_t ldx, const uint16_t* W, in
                            int32_t epilogue, float* out_f32, uint16_t* out_bf16, int32_t ldo, float* workspace,
                            void* stream);
 
+/* The kernels metro_op_gemm would run for a product (the model chooses by the
+ * same rules), for inspection and tests; host only, no device work.
+ * has_workspace: nonzero as for a non-NULL workspace.  *kind: 0 decode kernel
+ * (weight streaming, up to 64 rows), 1 tiled with 128 x 128 blocks, 2 tiled
+ * with 256 (W rows) x 128 blocks, 3 tiled with 256 x 256 blocks.  *k_slices:
+ * k slices of every block (> 1 only with a workspace); *tail_split: k slices
+ * of each block of the last, partly filled round of workgroups (1: none).
+ * Counts compute units of the current device (256 when there is none).
+ * Errors: E_INVAL (shape rules of metro_op_gemm, NULL outputs). */
+metro_status metro_op_gemm_plan(int32_t M, int32_t N, int32_t Kp, int32_t epilogue, int32_t has_workspace,
+                                int32_t* kind, int32_t* k_slices, int32_t* tail_split);
+
 /* RMSNorm (Zhang & Sennrich 2019): h[r, :] = bf16(x[r, :] / sqrt(mean(x[r, :]^2)
  * + eps) * g), x fp32 [rows, d], g bf16 [d], h bf16 [rows, d], d % 4 == 0, d <= 8192. */
 metro_status metro_op_rmsnorm(float* x, const uint16_t* g, float eps, uint16_t* h, int32_t rows, int32_t d,

@@ -952,6 +952,19 @@ metro_status metro_op_gemm(const uint16_t* X, int32_t ldx, const uint16_t* W, in
   return METRO_OK;
 }
 
+metro_status metro_op_gemm_plan(int32_t M, int32_t N, int32_t Kp, int32_t epilogue, int32_t has_workspace,
+                                int32_t* kind, int32_t* k_slices, int32_t* tail_split) {
+  g_err.clear();
+  if (!kind || !k_slices || !tail_split || M <= 0 || N <= 0 || Kp <= 0 || Kp % 128 || N % 32 ||
+      epilogue < metro::kEpiStoreF32 || epilogue > metro::kEpiSwiGLU)
+    return fail(METRO_E_INVAL, "gemm plan: bad shape (Kp %% 128, N %% 32) or epilogue");
+  const metro::GemmPlan p = metro::plan_gemm(M, N, Kp, epilogue, has_workspace ? 8LL * M * N : 0);
+  *kind = static_cast<int32_t>(p.kind);
+  *k_slices = p.ks;
+  *tail_split = p.tail_split;
+  return METRO_OK;
+}
+
 metro_status metro_op_rmsnorm(float* x, const uint16_t* g, float eps, uint16_t* h, int32_t rows, int32_t d,
                               void* stream) {
   g_err.clear();

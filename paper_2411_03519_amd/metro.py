@@ -76,6 +76,7 @@ _SIGS = {
     "metro_profile_stop": (_i32, [_vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_i64)]),
     "metro_op_pack_weight": (_i32, [_vp, _i32, _i32, _i32, _i32, _vp, _vp]),
     "metro_op_gemm": (_i32, [_vp, _i32, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp]),
+    "metro_op_gemm_plan": (_i32, [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp]),
     "metro_op_rmsnorm": (_i32, [_vp, _vp, ctypes.c_float, _vp, _i32, _i32, _vp]),
     "metro_op_argmax": (_i32, [_vp, _i32, _i32, _vp, _vp]),
     "metro_sched_create": (_i32, [_vp, _vp, ctypes.POINTER(_vp)]),
@@ -269,6 +270,17 @@ def op_gemm(X, W, M: int, N: int, Kp: int, epilogue: int, out, ldo: int, ldx: in
     b16 = out if epilogue == EPI_SWIGLU else None
     check(lib.metro_op_gemm(_ptr(X), ldx if ldx is not None else Kp, _ptr(W), Kp, M, N, epilogue, _ptr(f32),
                             _ptr(b16), ldo, _ptr(workspace), _stream(stream)))
+
+
+GEMM_KINDS = ("decode", "tile128x128", "tile256x128", "tile256x256")
+
+
+def op_gemm_plan(M: int, N: int, Kp: int, epilogue: int, workspace: bool = False):
+    """(kernel kind name, k slices, tail split) that op_gemm would use; host only."""
+    kind, ks, tail = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    check(lib.metro_op_gemm_plan(M, N, Kp, epilogue, int(bool(workspace)), ctypes.byref(kind), ctypes.byref(ks),
+                                 ctypes.byref(tail)))
+    return GEMM_KINDS[kind.value], ks.value, tail.value
 
 
 def op_rmsnorm(x, g, eps: float, h, rows: int, d: int, stream=None):

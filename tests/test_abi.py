@@ -46,3 +46,47 @@ def test_binding_reports_abi_and_errors_without_gpu(repo_root):
     assert metro.lib.metro_create_model(ctypes.byref(bad), 0, ctypes.byref(h)) == -1
     assert b"d_model" in metro.lib.metro_last_error()
     assert metro.lib.metro_seq_open(None, ctypes.byref(ctypes.c_int64())) == -1
+
+
+# Llama-3-8B (d 4096, QKV 6144, gate/up 2 x 14336, down K 14336) and 70B (d 8192,
+# gate/up 2 x 28672) products; compute units counted as 256 (no device here).
+PLAN_CASES = [
+    # M, N, Kp, epilogue, workspace -> kind, k slices, tail split
+    (25, 6144, 4096, 0, True, "decode", 2, 1),          # decode QKV: too few blocks, K split
+    (25, 28672, 4096, 2, True, "decode", 1, 1),         # SwiGLU never splits K
+    (64, 4096, 14336, 1, False, "decode", 1, 1),        # no workspace, no split
+    (65, 4096, 4096, 1, False, "tile128x128", 1, 1),    # past 64 rows: tiled
+    (1000, 6144, 4096, 0, False, "tile128x128", 1, 1),  # narrow up to 1000 rows
+    (1001, 6144, 4096, 0, False, "tile256x256", 1, 1),
+    (128, 28672, 4096, 2, True, "tile128x128", 1, 1),   # wide, 224 tiles <= CUs
+    (192, 28672, 4096, 2, True, "tile256x128", 1, 1),   # 448 128 x 128 tiles > CUs, 224 256 x 128
+    (128, 57344, 8192, 2, True, "tile256x128", 1, 1),   # 70B gate/up: 448 128-wide tiles > CUs
+    (200, 28672, 4096, 2, True, "tile256x128", 1, 1),   # 224 256 x 128 tiles <= CUs
+    (300, 28672, 4096, 2, True, "tile256x256", 1, 1),
+    (5376, 4096, 14336, 1, True, "tile256x256", 1, 2),  # 336 tiles: last 80 cut in 2 k slices
+    (5376, 4096, 14336, 1, False, "tile256x256", 1, 1),
+    (12800, 28672, 4096, 2, True, "tile256x256", 1, 1), # last round 224 of 256 CUs: no split
+]
+
+
+@pytest.mark.parametrize("M,N,Kp,epi,ws,kind,ks,tail", PLAN_CASES)
+def test_gemm_plan_rules(repo_root, M, N, Kp, epi, ws, kind, ks, tail):
+    if not os.path.exists(os.path.join(repo_root, "paper_2411_03519_amd", "libmetro.so")):
+        pytest.skip("libmetro.so not built")
+    from paper_2411_03519_amd import metro
+    got = metro.op_gemm_plan(M, N, Kp, epi, ws)
+    assert got[0] == kind
+    if kind == "decode" and ks > 1:
+        assert got[1] > 1  # the exact slice count follows the block count
+    else:
+        assert got[1] == ks
+    assert got[2] == tail
+
+
+def test_gemm_plan_rejects_bad_shapes(repo_root):
+    if not os.path.exists(os.path.join(repo_root, "paper_2411_03519_amd", "libmetro.so")):
+        pytest.skip("libmetro.so not built")
+    from paper_2411_03519_amd import metro
+    for args in ((0, 4096, 4096, 0), (64, 4016, 4096, 0), (64, 4096, 4000, 0), (64, 4096, 4096, 7)):
+        with pytest.raises(metro.MetroError):
+            metro.op_gemm_plan(*args)
