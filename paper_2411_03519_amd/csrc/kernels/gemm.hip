@@ -340,12 +340,27 @@ __host__ __device__ __forceinline__ void tile_origin(int t, int M, int N, int& m
   m0 = (first_m + in % gm) * S::BM;
 }
 
-// Work of one workgroup.  Without a tail split, workgroup (x, y) takes tile x
-// over k slice y of gridDim.y.  With one (tail_split = S > 1), workgroups
-// x < tail_first take tile x over all of K, and the last tiles, which would
-// leave most CUs idle in the final round, are cut into S k slices each:
-// workgroup tail_first + u takes slice u % S of tile tail_first + u / S and
-// stores its fp32 sums to part[u][BM][BN] for gemm_tail_fixup_kernel.
+// Workgroups are handed to the 8 XCDs in turn (workgroup b to XCD b % 8), and
+// each XCD has its own L2.  Work item of workgroup b (of `total`) such that
+// every XCD gets a contiguous run of the work list: in tile_origin order the
+// row tiles that read the same W columns are neighbours, so they run on one
+// XCD and share its L2 instead of each fetching W through the fabric.  In the
+// model (agent trace, 8B) this gained 2.5%; for prefill-sized 256 x 256 grids
+// it cost 1% and is not applied there.
+__device__ __forceinline__ int xcd_contiguous(int b, int total) {
+  constexpr int kXcds = 8;
+  const int q = total / kXcds, r = total % kXcds, x = b % kXcds, s = b / kXcds;
+  return x * q + min(x, r) + s;
+}
+
+// Work of one workgroup.  Without a tail split the grid's tiles x k slices
+// (slice-major list, tiles in tile_origin order) are spread over the XCDs by
+// xcd_contiguous (256 x 256 tiles: only up to kSplitMaxRows rows; above, the
+// list in grid order).  With one (tail_split = S > 1), workgroups x <
+// tail_first take tile x over all of K, and the last tiles, which would leave
+// most CUs idle in the final round, are cut into S k slices each: workgroup
+// tail_first + u takes slice u % S of tile tail_first + u / S and stores its
+// fp32 sums to part[u][BM][BN] for gemm_tail_fixup_kernel.
 template <class S, int EPI>
 __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __restrict__ X, int ldx,
                                                             const uint16_t* __restrict__ W, int Kp, int M, int N,
@@ -367,6 +382,10 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
     tile = tail_first + unit / tail_split;
     KS = tail_split;
     slice = unit % tail_split;
+  } else if (tail_split == 1 && (S::BM * S::BN < 256 * 256 || M <= kSplitMaxRows)) {
+    const int i = xcd_contiguous(blockIdx.y * gridDim.x + blockIdx.x, gridDim.x * gridDim.y);
+    slice = i / gridDim.x;
+    tile = i % gridDim.x;
   }
   const int kspan = Kp / KS, k0 = slice * kspan;
   const int nk = kspan / 32;
@@ -662,14 +681,28 @@ static int skinny_tiles(int N, int Kp, int epilogue) {
   return N <= 8192 && Kp <= 4096 ? 2 : 4;
 }
 
-// Workgroups split K while fewer than `target` cover the product; slices stay
-// multiples of 128, and the slice sums (ks * M * N fp32, written and read
-// again) stay within a quarter of the weight bytes (N * Kp bf16), i.e.
-// 8 * ks * M <= Kp: probes at M = 128..512 over the 8B and 70B shapes found
-// the best split there (8B QKV at M=256: 8 slices 49.8 us, 2 slices 35.5 us).
+// Decode kernel: workgroups split K while fewer than `target` cover the
+// product; slices stay multiples of 128, and the slice sums (ks * M * N fp32,
+// written and read again) stay within a quarter of the weight bytes (N * Kp
+// bf16), i.e. 8 * ks * M <= Kp.
 static int gemm_k_splits(int blocks, int target, int M, int Kp) {
   int ks = 1;
   while (blocks * ks < target && ks < 8 && (Kp / (2 * ks)) % 128 == 0 && 8 * (2 * ks) * M <= Kp) ks *= 2;
+  return ks;
+}
+
+// Tiled kernels: the most k slices (a power of two up to 8, slices multiples
+// of 128) whose workgroups still fit one round of the CUs, with slice sums up
+// to half the weight bytes (4 * ks * M <= Kp).  At M = 80..256 the narrow
+// 8B/70B products ran fastest with one round of workgroups (8B O at M=200: 4
+// slices, 256 workgroups, 26 us; 2 slices 30 us; 8B down at M=200: 4 slices
+// 50 us, 8 slices over 512 workgroups 57 us); in the model this took the
+// agent trace from 11.7k to 12.2k tokens/s and the 70B step (B=128) from
+// 2.47k to 2.57k against the former rule (fewer than 512 workgroups for
+// 128 x 128 tiles, slice sums within a quarter of the weights).
+static int tiled_k_splits(int tiles, int cus, int M, int Kp) {
+  int ks = 1;
+  while (ks < 8 && tiles * (2 * ks) <= cus && (Kp / (2 * ks)) % 128 == 0 && 4 * (2 * ks) * M <= Kp) ks *= 2;
   return ks;
 }
 
@@ -720,7 +753,7 @@ GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, int64_t part_cap) {
   const int bn = p.kind == GemmKind::kMid ? MidTile::BN : p.kind == GemmKind::kWide ? WideTile::BN : BigTile::BN;
   const int bm = p.kind == GemmKind::kMid ? MidTile::BM : p.kind == GemmKind::kWide ? WideTile::BM : BigTile::BM;
   const int tiles = tiles_of(bn, bm);
-  if (split) p.ks = gemm_k_splits(tiles, p.kind == GemmKind::kMid ? 512 : 256, M, Kp);
+  if (split) p.ks = tiled_k_splits(tiles, cus, M, Kp);
   // Last round of 256-row tiles (one workgroup per CU): with r tiles left for
   // C CUs, cut each into S k slices (S a power of two, r * S <= C, slices
   // multiples of 128), so that round takes 1/S of a tile's time; the fixup

@@ -63,6 +63,13 @@ PLAN_CASES = [
     (128, 57344, 8192, 2, True, "tile256x128", 1, 1),   # 70B gate/up: 448 128-wide tiles > CUs
     (200, 28672, 4096, 2, True, "tile256x128", 1, 1),   # 224 256 x 128 tiles <= CUs
     (300, 28672, 4096, 2, True, "tile256x256", 1, 1),
+    (80, 4096, 4096, 1, True, "tile128x128", 8, 1),    # 32 tiles x 8 slices: one round of 256 CUs
+    (80, 6144, 4096, 0, True, "tile128x128", 4, 1),    # 48 tiles: 8 slices would need two rounds
+    (200, 4096, 4096, 1, True, "tile128x128", 4, 1),   # 64 tiles x 4; 4 * 4 * 200 <= 4096
+    (256, 4096, 4096, 1, True, "tile128x128", 4, 1),
+    (300, 4096, 4096, 1, True, "tile128x128", 2, 1),   # 96 tiles: 4 slices would need two rounds
+    (200, 4096, 14336, 1, True, "tile128x128", 4, 1),  # 8B down
+    (128, 8192, 28672, 1, True, "tile128x128", 4, 1),  # 70B down
     (5376, 4096, 14336, 1, True, "tile256x256", 1, 2),  # 336 tiles: last 80 cut in 2 k slices
     (5376, 4096, 14336, 1, False, "tile256x256", 1, 1),
     (12800, 28672, 4096, 2, True, "tile256x256", 1, 1), # last round 224 of 256 CUs: no split
