@@ -82,7 +82,11 @@ def test_pack_weight_rejects_bad_shapes(metro):
 GEMM_CASES = [(1, 256, 64), (7, 640, 96), (16, 256, 32), (25, 4096, 512), (33, 768, 160), (64, 384, 1376),
               (65, 256, 160), (200, 1152, 416), (129, 128, 96), (300, 4096, 256), (1100, 384, 160),
               (200, 256, 16384), (70, 128, 65536),
-              (129, 1024, 512),      # 128 x 128 tiles, 2 k slices with a workspace
+              (129, 1024, 512),      # 128 x 128 tiles; no k split (slice sums would pass half the weights)
+              (80, 4096, 4096),      # 32 tiles of 128 x 128, with a workspace 8 k slices (one round of 256)
+              (200, 4096, 4096),     # 64 tiles of 128 x 128, with a workspace 4 k slices
+              (65, 1024, 160),       # 2 ragged tiles x 2 k slices: fewer workgroups than XCDs
+              (150, 2048, 416),      # 8 ragged tiles x 2 k slices
               (300, 4096, 16384),    # 256 x 256 tiles, 2 k slices with a workspace
               (600, 2048, 288),      # 128 x 128 tiles, ragged in both M and N
               (1300, 2048, 4096),    # 256 x 256 tiles, 96 in one partial round: with a workspace 2 k slices each
