@@ -735,6 +735,7 @@ GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, int64_t part_cap) {
     p.kind = GemmKind::kSkinny;
     p.nt = skinny_tiles(N, Kp, epilogue);
     if (split) p.ks = gemm_k_splits(N / (16 * p.nt), p.nt == 2 ? 512 : 256, M, Kp);
+    while (p.ks > 1 && static_cast<int64_t>(p.ks) * M * N > part_cap) p.ks /= 2;
     return p;
   }
   auto tiles_of = [&](int bn, int bm) { return ((N + bn - 1) / bn) * ((M + bm - 1) / bm); };
@@ -754,6 +755,7 @@ GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, int64_t part_cap) {
   const int bm = p.kind == GemmKind::kMid ? MidTile::BM : p.kind == GemmKind::kWide ? WideTile::BM : BigTile::BM;
   const int tiles = tiles_of(bn, bm);
   if (split) p.ks = tiled_k_splits(tiles, cus, M, Kp);
+  while (p.ks > 1 && static_cast<int64_t>(p.ks) * M * N > part_cap) p.ks /= 2;  // slice sums fit the workspace
   // Last round of 256-row tiles (one workgroup per CU): with r tiles left for
   // C CUs, cut each into S k slices (S a power of two, r * S <= C, slices
   // multiples of 128), so that round takes 1/S of a tile's time; the fixup
