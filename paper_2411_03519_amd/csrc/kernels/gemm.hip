@@ -751,10 +751,24 @@ GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, int64_t part_cap) {
   } else {
     p.kind = M <= kMidMaxRows ? GemmKind::kMid : GemmKind::kBig;
   }
+  const int kind_tiles = p.kind == GemmKind::kMid    ? mid_tiles
+                         : p.kind == GemmKind::kWide ? wide_tiles
+                                                     : tiles_of(BigTile::BN, BigTile::BM);
+  if (split) p.ks = tiled_k_splits(kind_tiles, cus, M, Kp);
+  // Narrow products whose 128 x 128 tiles fill under three quarters of the
+  // CUs even with k slices take 256 x 128 tiles when those reach at least as
+  // many workgroups (70B QKV at M=128: 40 tiles x 4 slices, 55 us, against
+  // 80 x 2 of 128 x 128, 63 us, in a probe).
+  if (split && p.kind == GemmKind::kMid && 4 * mid_tiles * p.ks < 3 * cus) {
+    const int wks = tiled_k_splits(wide_tiles, cus, M, Kp);
+    if (wide_tiles * wks >= mid_tiles * p.ks) {
+      p.kind = GemmKind::kWide;
+      p.ks = wks;
+    }
+  }
   const int bn = p.kind == GemmKind::kMid ? MidTile::BN : p.kind == GemmKind::kWide ? WideTile::BN : BigTile::BN;
   const int bm = p.kind == GemmKind::kMid ? MidTile::BM : p.kind == GemmKind::kWide ? WideTile::BM : BigTile::BM;
   const int tiles = tiles_of(bn, bm);
-  if (split) p.ks = tiled_k_splits(tiles, cus, M, Kp);
   while (p.ks > 1 && static_cast<int64_t>(p.ks) * M * N > part_cap) p.ks /= 2;  // slice sums fit the workspace
   // Last round of 256-row tiles (one workgroup per CU): with r tiles left for
   // C CUs, cut each into S k slices (S a power of two, r * S <= C, slices

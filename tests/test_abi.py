@@ -70,6 +70,7 @@ PLAN_CASES = [
     (300, 4096, 4096, 1, True, "tile128x128", 2, 1),   # 96 tiles: 4 slices would need two rounds
     (200, 4096, 14336, 1, True, "tile128x128", 4, 1),  # 8B down
     (128, 8192, 28672, 1, True, "tile128x128", 4, 1),  # 70B down
+    (128, 10240, 8192, 0, True, "tile256x128", 4, 1),  # 70B QKV: 80 x 2 of 128 x 128 -> 40 x 4 of 256 x 128
     (5376, 4096, 14336, 1, True, "tile256x256", 1, 2),  # 336 tiles: last 80 cut in 2 k slices
     (5376, 4096, 14336, 1, False, "tile256x256", 1, 1),
     (12800, 28672, 4096, 2, True, "tile256x256", 1, 1), # last round 224 of 256 CUs: no split

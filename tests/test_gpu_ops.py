@@ -87,6 +87,7 @@ GEMM_CASES = [(1, 256, 64), (7, 640, 96), (16, 256, 32), (25, 4096, 512), (33, 7
               (200, 4096, 4096),     # 64 tiles of 128 x 128, with a workspace 4 k slices
               (65, 1024, 160),       # 2 ragged tiles x 2 k slices: fewer workgroups than XCDs
               (150, 2048, 416),      # 8 ragged tiles x 2 k slices
+              (200, 4096, 5120),     # narrow, 80 tiles of 128 x 128 x 2 slices -> 40 of 256 x 128 x 4 slices
               (300, 4096, 16384),    # 256 x 256 tiles, 2 k slices with a workspace
               (600, 2048, 288),      # 128 x 128 tiles, ragged in both M and N
               (1300, 2048, 4096),    # 256 x 256 tiles, 96 in one partial round: with a workspace 2 k slices each
