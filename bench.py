@@ -11,10 +11,16 @@ then 64 tokens are generated greedily per agent: the first from the prefill,
 
 Reported ``value``: decode tokens/s = 25 * 63 * steps / (GPU time of the
 decode steps), timed with HIP events on the launch stream.  ``ms_per_step``
-is the whole step (prefill + decode).  ``roofline`` is for the dominant
-decode kernel (the gate/up projection GEMM with the SwiGLU epilogue), whose
-launches are timed with HIP events inside the library during the timed
-region; ``cpu_baseline`` times the CPU oracle on a bounded sample.
+is the whole step (prefill + decode).  ``roofline`` is the whole decode step:
+its algorithmic bytes (weights, KV read and write, fp32 logits) over the
+decode time, against the HBM peak; ``roofline_prefill`` the whole prefill's
+algorithmic flops over the prefill time, against the bf16 matrix-core peak.
+``roofline_kernel`` is the dominant decode kernel (the gate/up projection
+GEMM with the SwiGLU epilogue), whose launches are timed with HIP events
+inside the library during the timed region, with its HBM traffic from the
+committed counter summary; ``roofline_prefill_kernel`` the same GEMM during
+the first warm-up step's prefill.  ``cpu_baseline`` times the CPU oracle on a
+bounded sample.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1]
 """
@@ -837,16 +843,25 @@ def main():
     log(f"timed: {args.steps} steps, wall {wall:.2f}s, step {step_ms:.1f} ms, prefill {prefill_ms / args.steps:.1f}"
         f" ms/step ({prefill_tps:.0f} tok/s), decode {decode_ms / args.steps:.1f} ms/step ({value:.0f} tok/s)")
 
+    # roofline of the path: the whole decode step (algorithmic bytes of the 63
+    # steps, contexts growing by one token per step) and the whole prefill
+    step_bytes = sum(decode_step_bytes(shape, lens + k) for k in range(n_new - 1))
+    roofline = hbm_roofline(step_bytes * args.steps, decode_ms / 1e3,
+                            "whole decode step (weights + KV read and write + fp32 logits)")
+    roofline["bytes_per_step"] = int(step_bytes // (n_new - 1))
+    items = sum(-(-int(L) // chunk) for L in lens)      # LM-head rows: one per item of every prefill call
+    pf_all_flops = prefill_flops(shape, [np.arange(L) for L in lens], items)
+    pf_all_tflops = pf_all_flops * args.steps / (prefill_ms / 1e3) / 1e12
     # roofline of the dominant decode kernel: algorithmic bytes per launch
     d, F = shape["d_model"], shape["ffn_dim"]
     gu_bytes = 2 * F * d * 2 + n * d * 2 + n * F * 2   # W_gate|W_up + h in + SwiGLU out (bf16)
     gu_avg_s = gu_ms / 1e3 / gu_launches
     achieved = gu_bytes / gu_avg_s / 1e9
-    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
-                "kernel": "gemm gate/up + SwiGLU (decode, M=25, N=28672, K=4096)",
-                "bytes_per_launch": gu_bytes, "avg_launch_us": round(gu_avg_s * 1e6, 2),
-                "launches": gu_launches}
+    roofline_kernel = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                       "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
+                       "kernel": "gemm gate/up + SwiGLU (decode, M=25, N=28672, K=4096)",
+                       "bytes_per_launch": gu_bytes, "avg_launch_us": round(gu_avg_s * 1e6, 2),
+                       "launches": gu_launches}
     out = {"metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
            "warmup": args.warmup, "ms_per_step": round(step_ms, 2), "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "bf16",
@@ -856,16 +871,30 @@ def main():
                       "agents": n, "prompt_tokens": int(lens.sum()), "decode_steps": n_new - 1,
                       "ready_batch": n, "page_size": 16},
            "roofline": roofline,
+           "roofline_prefill": {"bound": "mfma", "achieved": round(pf_all_tflops, 1), "peak": BF16_PEAK_TFLOPS,
+                                "unit": "TFLOP/s", "frac": round(pf_all_tflops / BF16_PEAK_TFLOPS, 4),
+                                "traffic": None,
+                                "kernel": "whole prefill (linear layers + causal attention + LM head rows)",
+                                "flops_per_step": pf_all_flops},
+           "roofline_kernel": roofline_kernel,
+           "targets": {"decode_hbm_frac": 0.60, "prefill_mfma_frac": 0.50},
+           "tolerance": {"stated": {"logits_max_abs": 2e-2, "logits_rel_l2": 1e-2, "greedy": "exact"},
+                         "note": "met as stated at the tiny shape; at 8B/70B widths no fp32-accumulating "
+                                 "evaluation meets 2e-2 max-abs (the oracle's own float32 evaluation misses "
+                                 "it), so the bounds there are 1.25x the oracle's float32-vs-float64 spread "
+                                 "on the same inputs and greedy choices may differ at fp32-undecidable steps "
+                                 "(tests/parity.py)"},
            "decode_ms_per_step": round(decode_ms / args.steps, 2),
            "prefill_ms_per_step": round(prefill_ms / args.steps, 2),
            "prefill_tokens_per_s": round(prefill_tps, 1)}
     if args.warmup > 0 and pf_launches:
         pf_flops = 2.0 * 2 * F * d * lens.sum() * shape["n_layers"]
         pf_tflops = pf_flops / (pf_ms / 1e3) / 1e12
-        out["roofline_prefill"] = {"bound": "mfma", "achieved": round(pf_tflops, 1), "peak": BF16_PEAK_TFLOPS,
-                                   "unit": "TFLOP/s", "frac": round(pf_tflops / BF16_PEAK_TFLOPS, 4),
-                                   "kernel": "gemm gate/up + SwiGLU (prefill chunks; a split last round "
-                                             "includes its fixup kernel)", "launches": pf_launches}
+        out["roofline_prefill_kernel"] = {"bound": "mfma", "achieved": round(pf_tflops, 1),
+                                          "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                          "frac": round(pf_tflops / BF16_PEAK_TFLOPS, 4),
+                                          "kernel": "gemm gate/up + SwiGLU (prefill chunks; a split last round "
+                                                    "includes its fixup kernel)", "launches": pf_launches}
     model.close()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.seed)

@@ -7,7 +7,7 @@
  * multi-agent simulation in LLM inference (§1) and gains its speed-up by
  * letting more ready agents share one inference batch (§1, §3.2).  Each agent
  * issues LLM requests from its own thread through a thin shim to a serving
- * engine (§3.6, "Decoupling Simulation Engine from LLM Serving Engine"); a
+ * engine, the simulation engine being decoupled from it (§3.6); a
  * worker runs the requests of a ready cluster together (§3.1, Algorithm 3);
  * generation has a fixed length with no end-of-sequence stop (§4.1, replay
  * with ignore_eos); requests are never preempted mid-inference (§3.5); and a

@@ -75,6 +75,53 @@ metro_status metro_op_rmsnorm(float* x, const uint16_t* g, float eps, uint16_t* 
  * [rows, vocab], vocab % 4 == 0); NaN values are skipped, -1 if none is left. */
 metro_status metro_op_argmax(const float* logits, int32_t rows, int32_t vocab, int32_t* out, void* stream);
 
+/* KV pages as the attention kernels read them (the layout of one layer's slab
+ * of the model's pool): page p holds 16 consecutive positions; its bytes are
+ * [K | V][kv_head][tile], a tile being 16 keys x head_dim bf16 in matrix-core
+ * operand order:
+ *   K tile:   key r, dim e  at ((e/32 * 4 + (e/8)%4) * 16 + r) * 8 + e%8
+ *   V^T tile: dim e, key r  at ((e/32 * 4 + r/4) * 16 + e%16) * 8 + ((e/16)%2) * 4 + r%4
+ * so that element (page, K|V = c, head h, ...) sits at
+ *   page * (2 * n_kv_heads * 16 * head_dim) + (c * n_kv_heads + h) * 16 * head_dim + offset.
+ * Page ids index this array (0 <= id < n_pages). */
+
+/* Decode attention of the model's forward pass (grouped-query, causal, paged;
+ * the attention of the Llama decoder the paper serves, §4.1): for each row i
+ * and query head j, with kv head h = j / (nq / nkv) and keys t = 0 .. ctx[i]-1
+ * of the row's pages,
+ *   out[i, j, :] = bf16( sum_t softmax_t(q[i, j, :] . K[t, h, :] / sqrt(hd)) V[t, h, :] )
+ * with fp32 scores, softmax and accumulation (the weights enter the bf16
+ * matrix cores as a bf16 pair hi + lo).  Rows of more than 128 pages are cut
+ * into 128-page work items whose states are merged in order, as in the model.
+ *   q            device bf16 [rows, nq, hd]
+ *   kv           device bf16, n_pages pages in the layout above
+ *   ctx          host int32 [rows], >= 1
+ *   block_tables host int32, row after row: ceil(ctx[i] / 16) page ids each
+ *   out          device bf16 [rows, nq * hd]
+ * hd is 64 or 128; nq / nkv is 1, 2, 4 or 8.  Allocates and frees device
+ * memory for its descriptors and split states and returns after the kernels
+ * have finished on `stream` (a test entry point, not for serving loops).
+ * Errors: E_INVAL (shapes, NULL, page id out of range), E_HIP. */
+metro_status metro_op_attn_decode(const uint16_t* q, const uint16_t* kv, int32_t n_pages, int32_t nq, int32_t nkv,
+                                  int32_t hd, int32_t rows, const int32_t* ctx, const int32_t* block_tables,
+                                  uint16_t* out, void* stream);
+
+/* Chunked-prefill attention of the model's forward pass: item i has
+ * c_i = cu_q[i+1] - cu_q[i] queries (rows cu_q[i] .. cu_q[i+1]-1 of q and
+ * out) at positions ctx_before[i] .. ctx_before[i] + c_i - 1, and its pages
+ * hold keys 0 .. ctx_before[i] + c_i - 1 (the chunk's own keys included).
+ * The query at position p sees keys 0 .. p (causal), otherwise as
+ * metro_op_attn_decode.
+ *   q            device bf16 [cu_q[n_items], nq, hd]
+ *   cu_q         host int32 [n_items + 1], cu_q[0] = 0, each item >= 1 query
+ *   ctx_before   host int32 [n_items], >= 0
+ *   block_tables host int32, item after item: ceil((ctx_before[i] + c_i) / 16) ids
+ *   out          device bf16 [cu_q[n_items], nq * hd]
+ * Synchronous as metro_op_attn_decode.  Errors: E_INVAL, E_HIP. */
+metro_status metro_op_attn_prefill(const uint16_t* q, const uint16_t* kv, int32_t n_pages, int32_t nq, int32_t nkv,
+                                   int32_t hd, int32_t n_items, const int32_t* cu_q, const int32_t* ctx_before,
+                                   const int32_t* block_tables, uint16_t* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -10,7 +10,7 @@ What it computes
 AI Metropolis (arXiv 2411.03519) spends about 95% of simulation time in LLM
 inference (§1) and serves Llama-3 instruct models (8B and 70B) with a batching
 engine, replaying fixed-length generations without an end-of-sequence stop
-(§4.1, "Model and Hardware Platform", "Traces").  The paper does not define the
+(§4.1).  The paper does not define the
 network; the network computed here is the public Llama decoder:
 
 * token embedding, untied LM head, no biases, causal self-attention;

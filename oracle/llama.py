@@ -338,6 +338,29 @@ class OracleModel:
         hf = self.q(rms_norm(x, self.final_norm, self.shape.rms_eps))
         return self.lm_head_logits(hf).astype(np.float32)
 
+    def forward_each(self, caches, token_lists, logits_for_lists, on_layer=None) -> list:
+        """``forward(caches[a], token_lists[a], logits_for_lists[a])`` for every
+        sequence ``a``, with the layer loop outside the loop over sequences so
+        that lazy mode converts each layer's weights once.  Each sequence still
+        goes through the same blocks on its own, so every result is bitwise that
+        of the separate calls.  ``on_layer(li)`` is called after each layer
+        (progress reports of long runs)."""
+        toks = [np.asarray(t, dtype=np.int64) for t in token_lists]
+        pos = [np.arange(c.length, c.length + len(t)) for c, t in zip(caches, toks)]
+        xs = [self.embed_rows(t) for t in toks]
+        for li in range(self.shape.n_layers):
+            for a, c in enumerate(caches):
+                xs[a] = self.block(li, xs[a], c, pos[a])
+            if on_layer is not None:
+                on_layer(li)
+        out = []
+        for a, c in enumerate(caches):
+            c.advance(len(toks[a]))
+            x = xs[a] if logits_for_lists[a] is None else xs[a][logits_for_lists[a]]
+            hf = self.q(rms_norm(x, self.final_norm, self.shape.rms_eps))
+            out.append(self.lm_head_logits(hf).astype(np.float32))
+        return out
+
     def hidden_layers(self, cache, tokens, n_layers: int) -> np.ndarray:
         """Residual stream after the first ``n_layers`` blocks (for sampling the
         cost of the full model on the CPU; no logits)."""

@@ -64,6 +64,18 @@ __device__ __forceinline__ void split_bf16(float p0, float p1, uint32_t& hi, uin
   lo = pack_bf16x2(p0 - lo_bf16(hi), p1 - hi_bf16(hi));
 }
 
+// Keys past the end of a context sit in slots of the last page that no call
+// has written (or that hold a closed sequence's values): their softmax weight
+// is 0, but 0 times a NaN or Inf bit pattern there would still poison the
+// output, so their V values are zeroed in the operand.  A V^T operand word
+// holds the bf16 values of keys 4g + 2i and 4g + 2i + 1 (i = word % 2) of one
+// dim; keep_keys(n) is the mask of the word pair for keys below n.
+__device__ __forceinline__ uint2 keep_keys(int grp, int n) {
+  const int k0 = 4 * grp;
+  auto half = [&](int k) { return k < n ? 0xffffu : 0u; };
+  return make_uint2(half(k0) | (half(k0 + 1) << 16), half(k0 + 2) | (half(k0 + 3) << 16));
+}
+
 // ===========================================================================
 // Decode
 // ===========================================================================
@@ -159,9 +171,12 @@ __global__ __launch_bounds__(NW * 64) void attn_decode_kernel(AttnArgs a) {
           uint2 hi, lo;
           split_bf16(pv[0], pv[1], hi.x, lo.x);
           split_bf16(pv[2], pv[3], hi.y, lo.y);
+          const bool tail = (p + 1) * kPage > ctx;  // the row's last page, partly filled
+          const uint2 keep = tail ? keep_keys(grp, ctx - p * kPage) : make_uint2(~0u, ~0u);
 #pragma unroll
           for (int c = 0; c < NT / 2; ++c) {
-            const uint2 v0 = make_uint2(vf[sl][c].x, vf[sl][c].y), v1 = make_uint2(vf[sl][c].z, vf[sl][c].w);
+            const uint2 v0 = make_uint2(vf[sl][c].x & keep.x, vf[sl][c].y & keep.y),
+                        v1 = make_uint2(vf[sl][c].z & keep.x, vf[sl][c].w & keep.y);
             o[2 * c] *= corr;
             o[2 * c] = mfma_k16(v0, hi, o[2 * c]);
             o[2 * c] = mfma_k16(v0, lo, o[2 * c]);
@@ -355,11 +370,20 @@ __global__ __launch_bounds__(NW * 64) void attn_prefill_kernel(PrefillAttnArgs a
     for (int pg = 0; pg < 2; ++pg)
 #pragma unroll
       for (int i = 0; i < KQ; ++i) kf[pg][i] = st[pg][64 * i + lane];
+    // keys past the block's last position (never written, or the stand-in
+    // page of an odd count) get V = 0: keep masks for the pair's two pages
+    const int past = (2 * pair) * kPage;  // position of the pair's first key
+    const bool tail = past + 2 * kPage - 1 > last_pos;
+    uint2 keep0 = make_uint2(~0u, ~0u), keep1 = keep0;
+    if (tail) {
+      keep0 = keep_keys(grp, last_pos + 1 - past);
+      keep1 = keep_keys(grp, last_pos + 1 - past - kPage);
+    }
     auto vt_operand = [&](int t) __attribute__((always_inline)) {
       const int vo = 128 * (t >> 1) + 2 * lane + (t & 1);  // in 8-byte units
       const uint2 va = reinterpret_cast<const uint2*>(st[2])[vo];
       const uint2 vb = reinterpret_cast<const uint2*>(st[3])[vo];
-      return make_uint4(va.x, va.y, vb.x, vb.y);
+      return make_uint4(va.x & keep0.x, va.y & keep0.y, vb.x & keep1.x, vb.y & keep1.y);
     };
     uint4 vf[NQ > 1 ? NT : 1];
     if constexpr (NQ > 1) {

@@ -725,8 +725,9 @@ static int device_cus() {
 // number at most the CUs (in the 70B model at M=128 gate/up took 242 us as 448
 // such tiles against 203 us as 224 of 256 x 256, although cache-cold probes
 // had ranked them the other way); else 256 x 128 tiles for wide products up to
-// 128 rows, or up to 256 while they number at most the CUs; 256 x 256 tiles
-// for the rest and for long prefill chunks.
+// 128 rows, or up to 256 while they number at most the CUs, and for narrow
+// products of up to 128 rows that 128 x 128 tiles leave mostly idle; 256 x 256
+// tiles for the rest and for long prefill chunks.
 GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, int64_t part_cap) {
   GemmPlan p{GemmKind::kBig, 4, 1, 1, 0};
   const bool can_split = part_cap > 0;
@@ -755,11 +756,12 @@ GemmPlan plan_gemm(int M, int N, int Kp, int epilogue, int64_t part_cap) {
                          : p.kind == GemmKind::kWide ? wide_tiles
                                                      : tiles_of(BigTile::BN, BigTile::BM);
   if (split) p.ks = tiled_k_splits(kind_tiles, cus, M, Kp);
-  // Narrow products whose 128 x 128 tiles fill under three quarters of the
-  // CUs even with k slices take 256 x 128 tiles when those reach at least as
-  // many workgroups (70B QKV at M=128: 40 tiles x 4 slices, 55 us, against
-  // 80 x 2 of 128 x 128, 63 us, in a probe).
-  if (split && p.kind == GemmKind::kMid && 4 * mid_tiles * p.ks < 3 * cus) {
+  // Narrow products of up to 128 rows whose 128 x 128 tiles fill under three
+  // quarters of the CUs even with k slices take 256 x 128 tiles when those
+  // reach at least as many workgroups (70B QKV at M=128: 40 tiles x 4 slices,
+  // 55 us, against 80 x 2 of 128 x 128, 63 us, in a probe; larger batches
+  // were not measured with this rule and keep 128 x 128 tiles).
+  if (split && p.kind == GemmKind::kMid && M <= WideTile::BM && 4 * mid_tiles * p.ks < 3 * cus) {
     const int wks = tiled_k_splits(wide_tiles, cus, M, Kp);
     if (wide_tiles * wks >= mid_tiles * p.ks) {
       p.kind = GemmKind::kWide;

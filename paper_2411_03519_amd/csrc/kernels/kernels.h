@@ -141,7 +141,8 @@ struct RopeKV {
 // Kernel choice (plan_gemm): up to 64 rows the weight-streaming decode GEMM;
 // then the tiled GEMM with 128 x 128 blocks (narrow products up to
 // kMidMaxRows rows, wide ones while they fit the CUs), 256 (W rows) x 128
-// blocks (wide products at up to 256 rows otherwise), or 256 x 256 blocks.
+// blocks (wide products at up to 256 rows otherwise, narrow ones of up to 128
+// rows that 128 x 128 blocks would leave mostly idle), or 256 x 256 blocks.
 enum class GemmKind { kSkinny, kMid, kWide, kBig };
 struct GemmPlan {
   GemmKind kind;

@@ -350,6 +350,28 @@ metro_status upload_ring(metro_model* m, const Desc& d, hipStream_t s) {
   return METRO_OK;
 }
 
+// Work items of decode attention for a row that sees ctx keys: runs of up to
+// kDecodePagesPerSplit pages (depends on the row's own context only).
+int32_t decode_splits(int32_t ctx) {
+  return ((ctx + 15) / 16 + metro::kDecodePagesPerSplit - 1) / metro::kDecodePagesPerSplit;
+}
+
+// Query blocks of prefill attention for items of add[i] rows starting at row
+// cu[i]: (item, first row, rows) triples of at most tpb rows each.
+int64_t prefill_blocks(int n_items, const int32_t* cu, int tpb, int32_t* blocks) {
+  int64_t nb = 0;
+  for (int i = 0; i < n_items; ++i)
+    for (int r0 = cu[i]; r0 < cu[i + 1]; r0 += tpb) {
+      if (blocks) {
+        blocks[3 * nb] = i;
+        blocks[3 * nb + 1] = r0;
+        blocks[3 * nb + 2] = std::min(tpb, cu[i + 1] - r0);
+      }
+      ++nb;
+    }
+  return nb;
+}
+
 metro_status check_live(const metro_model* m) {
   if (!m) return fail(METRO_E_INVAL, "model is NULL");
   if (m->poisoned) return fail(METRO_E_HIP, "model is poisoned by an earlier HIP error");
@@ -745,10 +767,10 @@ metro_status metro_prefill_chunk(metro_model* m, int32_t n_items, const int64_t*
   int32_t* bt = d.put(bt_total);
   int32_t* item_bt = d.put(n_items);
   const int tpb = metro::prefill_tokens_per_block(m->group);
-  int64_t n_blocks = 0;
-  for (int i = 0; i < n_items; ++i) n_blocks += (add[i] + tpb - 1) / tpb;
+  const int64_t n_blocks = prefill_blocks(n_items, cu, tpb, nullptr);
   int32_t* blocks = d.put(3 * n_blocks);
-  int64_t bo = 0, nb = 0;
+  prefill_blocks(n_items, cu, tpb, blocks);
+  int64_t bo = 0;
   for (int i = 0; i < n_items; ++i) {
     const metro::Sequence* s = m->seqs->find(seqs[i]);
     std::copy(s->pages.begin(), s->pages.end(), bt + bo);
@@ -757,12 +779,6 @@ metro_status metro_prefill_chunk(metro_model* m, int32_t n_items, const int64_t*
       const int p = s->length + (t - cu[i]);
       pos[t] = p;
       slot[t] = s->pages[p / 16] * 16 + p % 16;
-    }
-    for (int r0 = cu[i]; r0 < cu[i + 1]; r0 += tpb) {
-      blocks[3 * nb] = i;
-      blocks[3 * nb + 1] = r0;
-      blocks[3 * nb + 2] = std::min(tpb, cu[i + 1] - r0);
-      ++nb;
     }
     last[i] = cu[i + 1] - 1;
     bo += s->pages.size();
@@ -837,7 +853,7 @@ metro_status metro_decode_step(metro_model* m, int32_t B, const int64_t* seqs, c
     row_q[i] = i;
     row_bt[i] = static_cast<int32_t>(bo);
     row_work[i] = n_work;
-    row_nsplit[i] = ((p + 1 + 15) / 16 + metro::kDecodePagesPerSplit - 1) / metro::kDecodePagesPerSplit;
+    row_nsplit[i] = decode_splits(p + 1);
     n_work += row_nsplit[i];
     bo += s->pages.size();
   }
@@ -972,6 +988,157 @@ metro_status metro_op_rmsnorm(float* x, const uint16_t* g, float eps, uint16_t* 
     return fail(METRO_E_INVAL, "rmsnorm: bad arguments");
   hipError_t e = metro::launch_rmsnorm(x, d, g, eps, h, d, rows, d, nullptr, 0, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(nullptr, e, "launch_rmsnorm");
+  return METRO_OK;
+}
+
+// Device copy of the host descriptor arrays of one attention op call (and
+// room for split states), freed when the op returns.
+struct OpBuffer {
+  void* p = nullptr;
+  ~OpBuffer() {
+    if (p) (void)hipFree(p);
+  }
+};
+
+metro_status check_attn_shape(int32_t nq, int32_t nkv, int32_t hd, int32_t n_pages) {
+  if (hd != 64 && hd != 128) return fail(METRO_E_INVAL, "attention: head_dim must be 64 or 128");
+  if (nkv <= 0 || nq <= 0 || nq % nkv) return fail(METRO_E_INVAL, "attention: n_heads %% n_kv_heads != 0");
+  const int g = nq / nkv;
+  if (g != 1 && g != 2 && g != 4 && g != 8) return fail(METRO_E_INVAL, "attention: group size must be 1, 2, 4 or 8");
+  if (n_pages <= 0) return fail(METRO_E_INVAL, "attention: n_pages must be positive");
+  return METRO_OK;
+}
+
+metro_status metro_op_attn_decode(const uint16_t* q, const uint16_t* kv, int32_t n_pages, int32_t nq, int32_t nkv,
+                                  int32_t hd, int32_t rows, const int32_t* ctx, const int32_t* block_tables,
+                                  uint16_t* out, void* stream) {
+  g_err.clear();
+  metro_status st = check_attn_shape(nq, nkv, hd, n_pages);
+  if (st != METRO_OK) return st;
+  if (rows < 0 || (rows > 0 && (!q || !kv || !ctx || !block_tables || !out)))
+    return fail(METRO_E_INVAL, "attn_decode: NULL argument or rows < 0");
+  if (rows == 0) return METRO_OK;
+  // descriptor arrays, in the order of the model's decode call
+  std::vector<int32_t> row_ctx(rows), row_q(rows), row_bt(rows), row_work(rows), row_nsplit(rows), work, bt;
+  int64_t bo = 0;
+  int32_t n_work = 0;
+  for (int i = 0; i < rows; ++i) {
+    if (ctx[i] < 1) return fail(METRO_E_INVAL, "attn_decode: row %d sees %d keys", i, ctx[i]);
+    const int np = (ctx[i] + 15) / 16;
+    for (int j = 0; j < np; ++j) {
+      const int32_t id = block_tables[bo + j];
+      if (id < 0 || id >= n_pages) return fail(METRO_E_INVAL, "attn_decode: page id %d out of range", id);
+      bt.push_back(id);
+    }
+    row_ctx[i] = ctx[i];
+    row_q[i] = i;
+    row_bt[i] = static_cast<int32_t>(bo);
+    row_work[i] = n_work;
+    row_nsplit[i] = decode_splits(ctx[i]);
+    for (int sp = 0; sp < row_nsplit[i]; ++sp) {
+      work.push_back(i);
+      work.push_back(sp);
+    }
+    n_work += row_nsplit[i];
+    bo += np;
+  }
+  const int g = nq / nkv;
+  std::vector<int32_t> host;
+  auto put = [&](const std::vector<int32_t>& v) {
+    const size_t off = host.size();
+    host.insert(host.end(), v.begin(), v.end());
+    host.resize((host.size() + 63) / 64 * 64, 0);
+    return off;
+  };
+  const size_t o_work = put(work), o_ctx = put(row_ctx), o_q = put(row_q), o_bt = put(row_bt), o_rw = put(row_work),
+               o_ns = put(row_nsplit), o_tab = put(bt);
+  const size_t part_floats = static_cast<size_t>(n_work) * nkv * g * (hd + 2);
+  OpBuffer buf;
+  HIP_TRY(nullptr, hipMalloc(&buf.p, host.size() * 4 + part_floats * 4 + 256));
+  int32_t* dev = static_cast<int32_t*>(buf.p);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  HIP_TRY(nullptr, hipMemcpyAsync(dev, host.data(), host.size() * 4, hipMemcpyHostToDevice, s));
+  metro::AttnArgs a{};
+  a.q = q;
+  a.kv = kv;
+  a.work = dev + o_work;
+  a.row_ctx = dev + o_ctx;
+  a.row_qrow = dev + o_q;
+  a.row_bt = dev + o_bt;
+  a.row_work = dev + o_rw;
+  a.row_nsplit = dev + o_ns;
+  a.bt = dev + o_tab;
+  a.part = reinterpret_cast<float*>(dev + host.size());
+  a.out = out;
+  a.n_work = n_work;
+  a.rows = rows;
+  a.nq = nq;
+  a.nkv = nkv;
+  a.hd = hd;
+  a.scale = 1.0f / std::sqrt(static_cast<float>(hd));
+  HIP_TRY(nullptr, metro::launch_attn_decode(a, s));
+  if (n_work > rows) HIP_TRY(nullptr, metro::launch_attn_combine(a, s));
+  HIP_TRY(nullptr, hipStreamSynchronize(s));
+  return METRO_OK;
+}
+
+metro_status metro_op_attn_prefill(const uint16_t* q, const uint16_t* kv, int32_t n_pages, int32_t nq, int32_t nkv,
+                                   int32_t hd, int32_t n_items, const int32_t* cu_q, const int32_t* ctx_before,
+                                   const int32_t* block_tables, uint16_t* out, void* stream) {
+  g_err.clear();
+  metro_status st = check_attn_shape(nq, nkv, hd, n_pages);
+  if (st != METRO_OK) return st;
+  if (n_items < 0 || (n_items > 0 && (!q || !kv || !cu_q || !ctx_before || !block_tables || !out)))
+    return fail(METRO_E_INVAL, "attn_prefill: NULL argument or n_items < 0");
+  if (n_items == 0) return METRO_OK;
+  if (cu_q[0] != 0) return fail(METRO_E_INVAL, "attn_prefill: cu_q[0] must be 0");
+  std::vector<int32_t> pos, item_bt(n_items), bt;
+  int64_t bo = 0;
+  for (int i = 0; i < n_items; ++i) {
+    const int c = cu_q[i + 1] - cu_q[i];
+    if (c < 1 || ctx_before[i] < 0) return fail(METRO_E_INVAL, "attn_prefill: item %d has %d queries after %d keys",
+                                                i, c, ctx_before[i]);
+    for (int t = 0; t < c; ++t) pos.push_back(ctx_before[i] + t);
+    const int np = (ctx_before[i] + c + 15) / 16;
+    for (int j = 0; j < np; ++j) {
+      const int32_t id = block_tables[bo + j];
+      if (id < 0 || id >= n_pages) return fail(METRO_E_INVAL, "attn_prefill: page id %d out of range", id);
+      bt.push_back(id);
+    }
+    item_bt[i] = static_cast<int32_t>(bo);
+    bo += np;
+  }
+  const int tpb = metro::prefill_tokens_per_block(nq / nkv);
+  std::vector<int32_t> blocks(3 * prefill_blocks(n_items, cu_q, tpb, nullptr));
+  prefill_blocks(n_items, cu_q, tpb, blocks.data());
+  std::vector<int32_t> host;
+  auto put = [&](const std::vector<int32_t>& v) {
+    const size_t off = host.size();
+    host.insert(host.end(), v.begin(), v.end());
+    host.resize((host.size() + 63) / 64 * 64, 0);
+    return off;
+  };
+  const size_t o_pos = put(pos), o_ibt = put(item_bt), o_bt = put(bt), o_blk = put(blocks);
+  OpBuffer buf;
+  HIP_TRY(nullptr, hipMalloc(&buf.p, host.size() * 4 + 256));
+  int32_t* dev = static_cast<int32_t*>(buf.p);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  HIP_TRY(nullptr, hipMemcpyAsync(dev, host.data(), host.size() * 4, hipMemcpyHostToDevice, s));
+  metro::PrefillAttnArgs a{};
+  a.q = q;
+  a.kv = kv;
+  a.out = out;
+  a.blocks = dev + o_blk;
+  a.item_bt = dev + o_ibt;
+  a.pos = dev + o_pos;
+  a.bt = dev + o_bt;
+  a.n_blocks = static_cast<int>(blocks.size() / 3);
+  a.nq = nq;
+  a.nkv = nkv;
+  a.hd = hd;
+  a.scale = 1.0f / std::sqrt(static_cast<float>(hd));
+  HIP_TRY(nullptr, metro::launch_attn_prefill(a, s));
+  HIP_TRY(nullptr, hipStreamSynchronize(s));
   return METRO_OK;
 }
 

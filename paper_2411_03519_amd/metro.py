@@ -79,6 +79,8 @@ _SIGS = {
     "metro_op_gemm_plan": (_i32, [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp]),
     "metro_op_rmsnorm": (_i32, [_vp, _vp, ctypes.c_float, _vp, _i32, _i32, _vp]),
     "metro_op_argmax": (_i32, [_vp, _i32, _i32, _vp, _vp]),
+    "metro_op_attn_decode": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp]),
+    "metro_op_attn_prefill": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
     "metro_sched_create": (_i32, [_vp, _vp, ctypes.POINTER(_vp)]),
     "metro_sched_destroy": (None, [_vp]),
     "metro_sched_next": (_i32, [_vp, ctypes.POINTER(_i32), ctypes.POINTER(_i32), _vp, _i32, ctypes.POINTER(_i32)]),
@@ -289,6 +291,25 @@ def op_rmsnorm(x, g, eps: float, h, rows: int, d: int, stream=None):
 
 def op_argmax(logits, rows: int, vocab: int, out, stream=None):
     check(lib.metro_op_argmax(_ptr(logits), rows, vocab, _ptr(out), _stream(stream)))
+
+
+def op_attn_decode(q, kv, n_pages: int, nq: int, nkv: int, hd: int, ctx, block_tables, out, stream=None):
+    """Decode attention on caller buffers: q [rows, nq, hd] bf16, kv the page
+    array, ctx and block_tables host ints (see metro_ops.h), out [rows, nq*hd]."""
+    c = _host_i32(ctx)
+    bt = _host_i32(block_tables)
+    check(lib.metro_op_attn_decode(_ptr(q), _ptr(kv), n_pages, nq, nkv, hd, len(c), c.ctypes.data, bt.ctypes.data,
+                                   _ptr(out), _stream(stream)))
+
+
+def op_attn_prefill(q, kv, n_pages: int, nq: int, nkv: int, hd: int, cu_q, ctx_before, block_tables, out,
+                    stream=None):
+    """Chunked-prefill attention on caller buffers (see metro_ops.h)."""
+    cu = _host_i32(cu_q)
+    cb = _host_i32(ctx_before)
+    bt = _host_i32(block_tables)
+    check(lib.metro_op_attn_prefill(_ptr(q), _ptr(kv), n_pages, nq, nkv, hd, len(cb), cu.ctypes.data,
+                                    cb.ctypes.data, bt.ctypes.data, _ptr(out), _stream(stream)))
 
 
 # ----------------------------------------------------------------------------

@@ -7,15 +7,25 @@ At Llama-3 widths these figures are below what fp32 arithmetic can reach:
 every bf16 re-quantisation point (h, q/k/v, o, the SwiGLU product) turns a
 perturbation of relative size delta into about sqrt(delta * ulp), so the
 oracle evaluated in float32 already differs from its float64 evaluation by
-max-abs ~3.4e-2 (rel-L2 ~5.6e-3) at 8B widths and depth 2, and by max-abs
+max-abs ~3e-2 (rel-L2 ~5e-3) at 8B widths and depth 2, and by max-abs
 ~1.2e-1, rel-L2 ~2.1e-2 at full depth (32 layers).  Each bound is therefore
-the larger of the fixed figure and twice that measured float32-vs-float64
-spread of the oracle on the same inputs (``noise_floor``).
+the larger of the fixed figure and 1.25 times that measured float32-vs-float64
+spread of the oracle on the same inputs (``noise_floor``): the GPU, another
+fp32-accumulating evaluation of the same function, must land no further from
+the float64 values than the oracle's own float32 evaluation, within a 25%
+margin for the sampling of the maximum.
 
-Greedy tokens: compared step by step under teacher forcing (both sides are fed
-the oracle's tokens).  A different choice is a failure when the oracle's top-2
-margin at that step is >= the max-abs bound; below it the two candidates are
-tied within tolerance and the step is counted as a tie-divergence instead.
+Greedy tokens (the oracle's float64 choice is the reference):
+- a different choice where the oracle's top-2 margin is below 2e-2 is a
+  tie-divergence: counted, reported and capped;
+- at a larger margin it is accepted only with evidence that fp32 arithmetic
+  cannot decide the step: the oracle's own float32 evaluation also diverges
+  there, or the margin is below that row's float32-vs-float64 max-abs spread
+  and the GPU has no more such divergences than the float32 evaluation has
+  over the same steps (plus one).  Two fp32 evaluations with different
+  summation orders flip at different near-ties, so a same-step match cannot
+  be required of every one; the count keeps the GPU's flip rate at that of a
+  legitimate fp32 evaluation.  Without float32 logits any such choice fails.
 """
 
 from __future__ import annotations
@@ -24,6 +34,8 @@ import numpy as np
 
 MAX_ABS = 2e-2
 REL_L2 = 1e-2
+FLOOR_FACTOR = 1.25
+TIE_MARGIN = 2e-2
 
 
 def logits_errors(got: np.ndarray, want: np.ndarray):
@@ -37,8 +49,9 @@ def logits_errors(got: np.ndarray, want: np.ndarray):
 def assert_logits_close(got, want, what="", max_abs_bound=MAX_ABS, rel_bound=REL_L2):
     assert np.all(np.isfinite(got)), f"{what}: non-finite logits"
     max_abs, rel = logits_errors(got, want)
+    stated = "meets" if max_abs <= MAX_ABS and rel <= REL_L2 else "misses"
     msg = (f"{what}: max-abs {max_abs:.3e} (bound {max_abs_bound:.3e}), "
-           f"max rel-L2 {rel:.3e} (bound {rel_bound:.3e})")
+           f"max rel-L2 {rel:.3e} (bound {rel_bound:.3e}); {stated} the stated 2e-2 / 1e-2")
     print(msg, flush=True)
     assert max_abs <= max_abs_bound and rel <= rel_bound, msg
     return max_abs, rel
@@ -46,10 +59,10 @@ def assert_logits_close(got, want, what="", max_abs_bound=MAX_ABS, rel_bound=REL
 
 def noise_floor(f64_logits, f32_logits):
     """(max-abs bound, rel-L2 bound) from the float32-vs-float64 spread of the
-    oracle itself: each the larger of the fixed figure and twice the spread."""
+    oracle itself: each the larger of the fixed figure and 1.25 times the spread."""
     spread, rel = logits_errors(f32_logits, f64_logits)
     print(f"oracle float32 vs float64: max-abs {spread:.3e}, max rel-L2 {rel:.3e}", flush=True)
-    return max(MAX_ABS, 2.0 * spread), max(REL_L2, 2.0 * rel)
+    return max(MAX_ABS, FLOOR_FACTOR * spread), max(REL_L2, FLOOR_FACTOR * rel)
 
 
 def top2_margin(logits: np.ndarray) -> np.ndarray:
@@ -57,12 +70,38 @@ def top2_margin(logits: np.ndarray) -> np.ndarray:
     return s[..., -1] - s[..., -2]
 
 
-def check_tokens(got_tok: np.ndarray, want_logits: np.ndarray, what="", tie=MAX_ABS) -> int:
-    """Greedy choices of the GPU against the oracle's logits of the same step.
-    Returns the number of tie-divergences; raises on a real mismatch."""
+def check_tokens(got_tok: np.ndarray, want_logits: np.ndarray, what="", f32_logits=None,
+                 max_ties: int | None = None) -> int:
+    """Greedy choices of the GPU against the oracle's float64 logits of the same
+    steps (see the module docstring).  Returns the number of divergences (ties
+    and fp32-undecidable steps together); raises on any other mismatch, or on
+    more than ``max_ties`` tie-divergences (default: a tenth of the steps,
+    at least one)."""
+    want_logits = np.asarray(want_logits)
     want_tok = np.argmax(want_logits, axis=-1)
     margin = top2_margin(want_logits)
-    diff = np.asarray(got_tok).reshape(want_tok.shape) != want_tok
-    bad = diff & (margin >= tie)
-    assert not np.any(bad), f"{what}: token mismatch at margin {margin[bad]}"
-    return int(np.sum(diff))
+    got_tok = np.asarray(got_tok).reshape(want_tok.shape)
+    diff = got_tok != want_tok
+    ties = diff & (margin < TIE_MARGIN)
+    wide = diff & ~ties
+    n_steps = diff.size
+    cap = max_ties if max_ties is not None else max(1, n_steps // 10)
+    matched = unmatched = f32_wide = 0
+    if np.any(wide):
+        assert f32_logits is not None, f"{what}: token mismatch at margin {margin[wide]} (no float32 evidence)"
+        f32 = np.asarray(f32_logits, np.float64).reshape(want_logits.shape)
+        f32_div = np.argmax(f32, axis=-1) != want_tok
+        spread = np.max(np.abs(f32 - want_logits), axis=-1)
+        inside = margin < spread
+        bad = wide & ~f32_div & ~inside
+        assert not np.any(bad), f"{what}: token mismatch at margin {margin[bad]} beyond the fp32 spread {spread[bad]}"
+        matched = int(np.sum(wide & f32_div))
+        unmatched = int(np.sum(wide & ~f32_div))
+        f32_wide = int(np.sum(f32_div & (margin >= TIE_MARGIN)))
+        assert unmatched <= f32_wide + 1, (f"{what}: {unmatched} unmatched divergences at margins >= 2e-2, the "
+                                          f"float32 oracle has {f32_wide} over the same steps")
+    print(f"{what}: {n_steps} greedy choices, {int(ties.sum())} tie-divergences (margin < 2e-2, cap {cap}), "
+          f"{matched + unmatched} at larger margins ({matched} where the float32 oracle diverges too; "
+          f"float32 oracle: {f32_wide})", flush=True)
+    assert int(ties.sum()) <= cap, f"{what}: {int(ties.sum())} tie-divergences > cap {cap}"
+    return int(diff.sum())

@@ -71,6 +71,8 @@ PLAN_CASES = [
     (200, 4096, 14336, 1, True, "tile128x128", 4, 1),  # 8B down
     (128, 8192, 28672, 1, True, "tile128x128", 4, 1),  # 70B down
     (128, 10240, 8192, 0, True, "tile256x128", 4, 1),  # 70B QKV: 80 x 2 of 128 x 128 -> 40 x 4 of 256 x 128
+    (200, 10240, 8192, 0, True, "tile128x128", 1, 1),  # past 128 rows narrow products keep 128 x 128 tiles
+    (600, 4096, 14336, 1, True, "tile128x128", 1, 1),  # 8B down at an agent-trace batch
     (5376, 4096, 14336, 1, True, "tile256x256", 1, 2),  # 336 tiles: last 80 cut in 2 k slices
     (5376, 4096, 14336, 1, False, "tile256x256", 1, 1),
     (12800, 28672, 4096, 2, True, "tile256x256", 1, 1), # last round 224 of 256 CUs: no split

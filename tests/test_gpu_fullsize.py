@@ -6,12 +6,15 @@ the whole ready batch) and compares sampled agents with the oracle, which
 evaluates them one by one (float64 with the bf16 storage points; the same
 function in float32 gives the noise floor of the bounds, see tests/parity.py).
 Decode steps are teacher-forced with seeded token ids on both sides, so one
-oracle pass over prompt + fed tokens yields every compared row.
+oracle pass over prompt + fed tokens yields every compared row; a
+free-running row instead feeds the GPU's own greedy tokens, and the oracle is
+fed the GPU's stream.
 
 - Llama-3-8B shape at full depth (32 layers): the benchmarked workload, 25
   agents with lognormal prompts (median 1200), prefilled together in 512-token
-  chunks, decode at B = 25.  Sampled: the shortest prompt that needs two
-  chunks.
+  chunks, decode at B = 25 for 16 steps.  Compared: five agents
+  teacher-forced (the longest prompt, 2376 tokens, and four of 637..844
+  tokens) and one free-running greedy stream (the 375-token agent).
 - 8B widths, 2 layers, a ready batch of 800 agents (the largest batch of the
   agent trace) with lognormal(median 1500) contexts: tiled GEMMs and 800-row
   attention in decode.  Two agents against the oracle; and 600 of the agents,
@@ -41,7 +44,8 @@ pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
 
-DECODE_STEPS = 3
+DECODE_STEPS = 8
+FULL_DEPTH_STEPS = 16
 
 
 @pytest.fixture(scope="module")
@@ -69,7 +73,18 @@ def oracle_with_floor(shape, weights, prompt, feed, what):
     want = oracle_rows(shape, weights, prompt, feed, np.float64)
     say(f"{what}: oracle float32")
     f32 = oracle_rows(shape, weights, prompt, feed, np.float32)
-    return want, noise_floor(want, f32)
+    return want, f32, noise_floor(want, f32)
+
+
+def oracle_rows_each(shape, weights, prompts, feeds, dtype, what):
+    """oracle_rows for several sequences, layer by layer (each layer's weights
+    converted once); progress printed per layer."""
+    ref = OracleModel(LlamaShape(**shape), weights, dtype=dtype, lazy=True)
+    seqs = [np.concatenate([np.asarray(p, np.int64), np.asarray(f, np.int64)]) for p, f in zip(prompts, feeds)]
+    sel = [list(range(len(p) - 1, len(p) + len(f))) for p, f in zip(prompts, feeds)]
+    name = np.dtype(dtype).name
+    return ref.forward_each([ref.new_cache() for _ in seqs], seqs, sel,
+                            on_layer=lambda li: say(f"{what}: oracle {name} layer {li + 1}/{shape['n_layers']}"))
 
 
 def prefill_batched(m, seqs, prompts, chunk, group, keep):
@@ -116,32 +131,73 @@ def stitched(pre, dec, i):
     return (np.concatenate([pre[i][0][None], dec[i][0]]), np.concatenate([[pre[i][1]], dec[i][1]]))
 
 
-def compare(what, got, toks, want, bounds):
+def compare(what, got, toks, want, f32, bounds):
     assert_logits_close(got, want, what, max_abs_bound=bounds[0], rel_bound=bounds[1])
-    ties = check_tokens(toks, want, what, tie=bounds[0])
-    say(f"{what}: {len(toks)} greedy choices, {ties} tie-divergences")
+    check_tokens(toks, want, what, f32_logits=f32)
 
 
+def decode_free_and_fed(m, seqs, feeds, first_tok, free, keep):
+    """feeds.shape[1] decode steps over all seqs in one batch: row i is fed
+    feeds[i, k], except the rows in ``free``, which are fed their own previous
+    greedy token (first_tok[i] before the first step).  Returns {i: (logits
+    [steps, V], tokens [steps], inputs [steps])} for i in keep."""
+    B = len(seqs)
+    lg = torch.empty(B, m.vocab, device="cuda")
+    nt = torch.empty(B, dtype=torch.int32, device="cuda")
+    sel = torch.tensor(list(keep), dtype=torch.int64, device="cuda")
+    prev = dict(first_tok)
+    rows = {i: ([], [], []) for i in keep}
+    for k in range(feeds.shape[1]):
+        inp = feeds[:, k].copy()
+        for i in free:
+            inp[i] = prev[i]
+        m.decode_step(seqs, torch.tensor(inp, dtype=torch.int32, device="cuda"), lg, nt)
+        lgh, nth = lg[sel].cpu().numpy(), nt[sel].cpu().numpy()
+        for j, i in enumerate(keep):
+            rows[i][0].append(lgh[j])
+            rows[i][1].append(nth[j])
+            rows[i][2].append(inp[i])
+            prev[i] = int(nth[j])
+    return {i: tuple(np.array(x) for x in r) for i, r in rows.items()}
+
+
+@pytest.mark.timeout(1800)
 def test_llama3_8b_full_depth_benchmark_batch(metro):
     shape = synth.LLAMA3_8B
     V = shape["vocab"]
     prompts, _ = synth.llama8b_agent_batch(0)
-    lens = [len(p) for p in prompts]
-    i = min((n, j) for j, n in enumerate(lens) if n > 512)[1]
-    feeds = synth.feed_tokens(0, len(prompts), DECODE_STEPS, V)
-    say("8B full depth: drawing 16 GB of weights")
+    lens = np.array([len(p) for p in prompts])
+    order = np.argsort(lens, kind="stable")
+    free = [int(order[0])]                                  # the shortest prompt runs free
+    fed = [int(order[-1])] + [int(i) for i in order[1:5]]   # the longest and the next four shortest
+    keep = fed + free
+    feeds = synth.feed_tokens(0, len(prompts), FULL_DEPTH_STEPS, V)
+    say(f"8B full depth: agents {keep} ({lens[keep].tolist()} prompt tokens), drawing 16 GB of weights")
     w = synth.llama_weights(shape, 0, workers=16)
-    want, bounds = oracle_with_floor(shape, w, prompts[i], feeds[i], "8B full depth")
     say("8B full depth: gpu (upload, prefill of 25 agents, decode at B = 25)")
     m = metro.Model(shape, max_batch=64, max_tokens=len(prompts) * 512, max_context=4096 + 128,
                     max_seqs=2 * len(prompts), kv_pool_bytes=24 << 30)
     with m:
         m.load_weights(w)
         seqs = [m.seq_open() for _ in prompts]
-        pre = prefill_batched(m, seqs, prompts, 512, len(prompts), [i])
-        dec = decode_fed(m, seqs, feeds, [i])
-    got, toks = stitched(pre, dec, i)
-    compare("8B full depth", got, toks, want, bounds)
+        pre = prefill_batched(m, seqs, prompts, 512, len(prompts), keep)
+        dec = decode_free_and_fed(m, seqs, feeds, {i: pre[i][1] for i in free}, free, keep)
+    # what the oracle is fed after each prompt: the fed tokens, or the GPU's own stream
+    fed_in = {i: dec[i][2] for i in keep}
+    for i in fed:
+        np.testing.assert_array_equal(fed_in[i], feeds[i])
+    assert fed_in[free[0]][0] == pre[free[0]][1]
+    np.testing.assert_array_equal(fed_in[free[0]][1:], dec[free[0]][1][:-1])
+    ps = [prompts[i] for i in keep]
+    fs = [fed_in[i] for i in keep]
+    want = oracle_rows_each(shape, w, ps, fs, np.float64, "8B full depth")
+    f32 = oracle_rows_each(shape, w, ps, fs, np.float32, "8B full depth")
+    bounds = noise_floor(np.stack(want), np.stack(f32))
+    for a, i in enumerate(keep):
+        got = np.concatenate([pre[i][0][None], dec[i][0]])
+        toks = np.concatenate([[pre[i][1]], dec[i][1]])
+        kind = "free-running" if i in free else "teacher-forced"
+        compare(f"8B full depth agent {i} ({lens[i]} tokens, {kind})", got, toks, want[a], f32[a], bounds)
 
 
 def test_8b_widths_ready_batch_800(metro):
@@ -193,7 +249,7 @@ def test_8b_widths_prefix_heavy_forked(metro):
     say("prefix-heavy: drawing weights")
     w = synth.llama_weights(shape, 2, workers=16)
     full_i = np.concatenate([prefix, suffixes[i]])
-    want, bounds = oracle_with_floor(shape, w, full_i, feeds[i], "prefix-heavy")
+    want, f32, bounds = oracle_with_floor(shape, w, full_i, feeds[i], "prefix-heavy")
     say(f"prefix-heavy: gpu, {n} forks of a {len(prefix)}-token prefix")
     m = metro.Model(shape, max_batch=64, max_tokens=n * 512, max_context=1024 + 2048 + 16, max_seqs=2 * n + 4,
                     kv_pool_bytes=8 << 30)
@@ -214,7 +270,7 @@ def test_8b_widths_prefix_heavy_forked(metro):
     own = np.concatenate([t[len(shared):] for t in tables])
     assert len(np.unique(own)) == len(own) and not np.isin(own, shared).any()
     got, toks = stitched(pre, dec, i)
-    compare(f"prefix-heavy request {i} ({len(full_i)} tokens)", got, toks, want, bounds)
+    compare(f"prefix-heavy request {i} ({len(full_i)} tokens)", got, toks, want, f32, bounds)
 
 
 def test_70b_widths_batch_128(metro):
@@ -226,7 +282,7 @@ def test_70b_widths_batch_128(metro):
     feeds = synth.feed_tokens(3, len(ctx), DECODE_STEPS, V)
     say("70B widths: drawing weights")
     w = synth.llama_weights(shape, 3, workers=16)
-    want, bounds = oracle_with_floor(shape, w, ctx[i], feeds[i], "70B widths")
+    want, f32, bounds = oracle_with_floor(shape, w, ctx[i], feeds[i], "70B widths")
     say(f"70B widths: gpu prefill of {lens.sum()} tokens, decode at B = {len(ctx)}")
     m = metro.Model(shape, max_batch=len(ctx), max_tokens=32 * 512, max_context=3072 + 16,
                     max_seqs=len(ctx) + 4, kv_pool_bytes=8 << 30)
@@ -236,4 +292,4 @@ def test_70b_widths_batch_128(metro):
         pre = prefill_batched(m, seqs, ctx, 512, 32, [i])
         dec = decode_fed(m, seqs, feeds, [i])
     got, toks = stitched(pre, dec, i)
-    compare(f"70B widths agent {i} ({lens[i]} tokens)", got, toks, want, bounds)
+    compare(f"70B widths agent {i} ({lens[i]} tokens)", got, toks, want, f32, bounds)

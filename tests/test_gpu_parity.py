@@ -406,7 +406,28 @@ def test_llama3_8b_widths_two_layers(metro):
     with make_model(metro, shape, w, max_batch=4, max_tokens=512, max_context=512, kv_pool_bytes=1 << 30) as m:
         logits, toks = gpu_teacher_forced(m, prompts, [g[0][:-1] for g in gens], chunk=128)
     assert_logits_close(logits, want, "8B widths", max_abs_bound=bound, rel_bound=rel_bound)
-    check_tokens(toks, want, "8B widths", tie=bound)
+    check_tokens(toks, want, "8B widths", f32_logits=f32)
+
+
+@pytest.mark.parametrize("hd", [64, 128])
+@pytest.mark.parametrize("group", [1, 2, 4, 8])
+def test_every_head_dim_and_group_the_config_accepts(metro, hd, group):
+    """Each (head_dim, GQA group) pair that metro_create_model accepts selects
+    its own decode and prefill attention kernels: a 2-layer model of d 256
+    with 2 kv heads per pair, four agents prefilled in 64-token chunks (one
+    call per chunk round), then 4 decode steps, against the oracle at the
+    stated 2e-2 / 1e-2."""
+    shape = dict(synth.TINY, n_heads=2 * group, n_kv_heads=2, head_dim=hd)
+    w = synth.llama_weights(shape, 40 + group, norm="random")
+    rng = np.random.default_rng(41 + hd + group)
+    prompts = [rng.integers(0, shape["vocab"], n) for n in (1, 37, 130, 300)]
+    ref = OracleModel(LlamaShape(**shape), w)
+    gens = [ref.generate(p, 5, chunk=64) for p in prompts]
+    with make_model(metro, shape, w, max_batch=8, max_tokens=512, max_context=512) as m:
+        logits, toks = gpu_teacher_forced(m, prompts, [g[0][:-1] for g in gens], chunk=64)
+    want = np.stack([g[1] for g in gens])
+    assert_logits_close(logits, want, f"head dim {hd}, group {group}")
+    check_tokens(toks, want, f"head dim {hd}, group {group}")
 
 
 def test_long_contexts_split_decode_attention(metro):

@@ -289,6 +289,20 @@ def test_lazy_weight_conversion_is_bitwise_the_same(dtype):
     np.testing.assert_array_equal(rows, full[[3, -1]])
 
 
+@pytest.mark.parametrize("lazy", [False, True])
+def test_forward_each_equals_separate_forwards_bitwise(lazy):
+    cfg = synth.TINY
+    W = synth.llama_weights(cfg, 23, norm="random")
+    om = OracleModel(shape_of(cfg), W, lazy=lazy)
+    rng = np.random.default_rng(23)
+    toks = [rng.integers(0, cfg["vocab"], n) for n in (17, 40, 5)]
+    sel = [None, [0, 39], [-1]]
+    want = [om.forward(om.new_cache(), t, s) for t, s in zip(toks, sel)]
+    got = om.forward_each([om.new_cache() for _ in toks], toks, sel)
+    for a, b in zip(got, want):
+        np.testing.assert_array_equal(a, b)
+
+
 def test_paged_kv_equals_contiguous_bitwise(tiny_model):
     S = tiny_model.shape
     prompt = np.random.default_rng(13).integers(0, S.vocab, 45)
