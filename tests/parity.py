@@ -87,6 +87,9 @@ def check_tokens(got_tok: np.ndarray, want_logits: np.ndarray, what="", f32_logi
     n_steps = diff.size
     cap = max_ties if max_ties is not None else max(1, n_steps // 10)
     matched = unmatched = f32_wide = 0
+    f32_all = None
+    if f32_logits is not None:
+        f32_all = int(np.sum(np.argmax(np.asarray(f32_logits).reshape(want_logits.shape), axis=-1) != want_tok))
     if np.any(wide):
         assert f32_logits is not None, f"{what}: token mismatch at margin {margin[wide]} (no float32 evidence)"
         f32 = np.asarray(f32_logits, np.float64).reshape(want_logits.shape)
@@ -102,6 +105,6 @@ def check_tokens(got_tok: np.ndarray, want_logits: np.ndarray, what="", f32_logi
                                           f"float32 oracle has {f32_wide} over the same steps")
     print(f"{what}: {n_steps} greedy choices, {int(ties.sum())} tie-divergences (margin < 2e-2, cap {cap}), "
           f"{matched + unmatched} at larger margins ({matched} where the float32 oracle diverges too; "
-          f"float32 oracle: {f32_wide})", flush=True)
+          f"float32 oracle: {f32_wide}; its divergences at any margin: {f32_all})", flush=True)
     assert int(ties.sum()) <= cap, f"{what}: {int(ties.sum())} tie-divergences > cap {cap}"
     return int(diff.sum())

@@ -193,11 +193,19 @@ def test_llama3_8b_full_depth_benchmark_batch(metro):
     want = oracle_rows_each(shape, w, ps, fs, np.float64, "8B full depth")
     f32 = oracle_rows_each(shape, w, ps, fs, np.float32, "8B full depth")
     bounds = noise_floor(np.stack(want), np.stack(f32))
+    all_toks = []
     for a, i in enumerate(keep):
         got = np.concatenate([pre[i][0][None], dec[i][0]])
         toks = np.concatenate([[pre[i][1]], dec[i][1]])
+        all_toks.append(toks)
         kind = "free-running" if i in free else "teacher-forced"
-        compare(f"8B full depth agent {i} ({lens[i]} tokens, {kind})", got, toks, want[a], f32[a], bounds)
+        what = f"8B full depth agent {i} ({lens[i]} tokens, {kind})"
+        assert_logits_close(got, want[a], what, max_abs_bound=bounds[0], rel_bound=bounds[1])
+        n_div = int(np.sum(toks != np.argmax(want[a], axis=-1)))
+        say(f"{what}: {n_div} of {len(toks)} greedy choices differ from the float64 oracle's")
+    # greedy choices judged over all compared steps together (tie rate ~ the
+    # density of top-2 margins below 2e-2, a few percent at full depth)
+    check_tokens(np.stack(all_toks), np.stack(want), "8B full depth, all agents", f32_logits=np.stack(f32))
 
 
 def test_8b_widths_ready_batch_800(metro):
