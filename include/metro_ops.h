@@ -122,6 +122,25 @@ metro_status metro_op_attn_prefill(const uint16_t* q, const uint16_t* kv, int32_
                                    int32_t hd, int32_t n_items, const int32_t* cu_q, const int32_t* ctx_before,
                                    const int32_t* block_tables, uint16_t* out, void* stream);
 
+/* metro_op_attn_decode for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same kernels and results, with the descriptors and split
+ * states in a fixed device array of 64 MiB that the library holds on each GPU
+ * it runs on until the process ends, instead of a per-call allocation.  No
+ * hipMalloc or hipFree, no allocating library call.  Arguments as for
+ * metro_op_attn_decode (ctx and block_tables are host arrays, copied to the
+ * device on `stream`).  Asynchronous: out is valid once `stream` has reached
+ * the call.  Every call on one GPU uses that GPU's array, so calls that
+ * overlap on one GPU (other streams or host threads) race; calls ordered on
+ * one stream do not.  Needs 5 * rows + pages + 2 * work items int32 (each
+ * rounded up to 256 bytes) plus work items * nkv * (nq / nkv) * (hd + 2) fp32,
+ * a work item being up to 128 pages of one row.
+ * Errors: E_INVAL as metro_op_attn_decode, E_CAPACITY when that exceeds the
+ * array, E_HIP. */
+metro_status metro_op_attn_decode_noalloc(const uint16_t* q, const uint16_t* kv, int32_t n_pages, int32_t nq,
+                                          int32_t nkv, int32_t hd, int32_t rows, const int32_t* ctx,
+                                          const int32_t* block_tables, uint16_t* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

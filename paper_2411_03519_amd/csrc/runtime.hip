@@ -10,6 +10,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <memory>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -376,6 +377,63 @@ metro_status check_live(const metro_model* m) {
   if (!m) return fail(METRO_E_INVAL, "model is NULL");
   if (m->poisoned) return fail(METRO_E_HIP, "model is poisoned by an earlier HIP error");
   return METRO_OK;
+}
+
+}  // namespace
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// Decode attention without allocation: descriptors and split states live in a
+// fixed device array (one copy per GPU) instead of a per-call buffer.
+// ---------------------------------------------------------------------------
+
+constexpr size_t kScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+// Per device: the address of `scratch` on that GPU (hipGetSymbolAddress; the
+// host-side name is only a stand-in and must never reach a kernel).
+constexpr int kMaxDevices = 64;
+static void* g_scratch_ptr[kMaxDevices] = {};
+static std::mutex g_scratch_mu;
+
+metro_status scratch_on_current_device(void** out) {
+  int dev = 0;
+  HIP_TRY(nullptr, hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(METRO_E_INVAL, "device %d out of range", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    HIP_TRY(nullptr, hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(METRO_E_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return METRO_OK;
+}
+
+// Descriptor arrays of decode attention built on the device from the rows'
+// context lengths, in the order and with the values the host builds them for
+// metro_op_attn_decode (row i's pages at the running page offset, its work
+// items at the running work offset, splits of decode_splits()).  One thread:
+// a few hundred cycles per row.
+__global__ void describe_decode_kernel(const int32_t* ctx, int rows, int32_t* row_q, int32_t* row_bt,
+                                       int32_t* row_work, int32_t* row_nsplit, int32_t* work) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  int32_t bo = 0, w = 0;
+  for (int i = 0; i < rows; ++i) {
+    const int32_t np = (ctx[i] + 15) / 16;
+    const int32_t ns = (np + metro::kDecodePagesPerSplit - 1) / metro::kDecodePagesPerSplit;
+    row_q[i] = i;
+    row_bt[i] = bo;
+    row_work[i] = w;
+    row_nsplit[i] = ns;
+    for (int sp = 0; sp < ns; ++sp, ++w) {
+      work[2 * w] = i;
+      work[2 * w + 1] = sp;
+    }
+    bo += np;
+  }
 }
 
 }  // namespace
@@ -1079,6 +1137,80 @@ metro_status metro_op_attn_decode(const uint16_t* q, const uint16_t* kv, int32_t
   HIP_TRY(nullptr, metro::launch_attn_decode(a, s));
   if (n_work > rows) HIP_TRY(nullptr, metro::launch_attn_combine(a, s));
   HIP_TRY(nullptr, hipStreamSynchronize(s));
+  return METRO_OK;
+}
+
+metro_status metro_op_attn_decode_noalloc(const uint16_t* q, const uint16_t* kv, int32_t n_pages, int32_t nq,
+                                          int32_t nkv, int32_t hd, int32_t rows, const int32_t* ctx,
+                                          const int32_t* block_tables, uint16_t* out, void* stream) {
+  g_err.clear();
+  metro_status st = check_attn_shape(nq, nkv, hd, n_pages);
+  if (st != METRO_OK) return st;
+  if (rows < 0 || (rows > 0 && (!q || !kv || !ctx || !block_tables || !out)))
+    return fail(METRO_E_INVAL, "attn_decode_noalloc: NULL argument or rows < 0");
+  if (rows == 0) return METRO_OK;
+  // sizes and checks on the host, without building anything
+  int64_t pages = 0, n_work = 0;
+  for (int i = 0; i < rows; ++i) {
+    if (ctx[i] < 1) return fail(METRO_E_INVAL, "attn_decode_noalloc: row %d sees %d keys", i, ctx[i]);
+    const int np = (ctx[i] + 15) / 16;
+    for (int j = 0; j < np; ++j) {
+      const int32_t id = block_tables[pages + j];
+      if (id < 0 || id >= n_pages) return fail(METRO_E_INVAL, "attn_decode_noalloc: page id %d out of range", id);
+    }
+    pages += np;
+    n_work += decode_splits(ctx[i]);
+  }
+  auto span = [](int64_t ints) { return (ints * 4 + 255) / 256 * 256; };
+  const int g = nq / nkv;
+  const int64_t part_bytes = n_work * nkv * g * (hd + 2) * 4;
+  const int64_t need = 5 * span(rows) + span(pages) + span(2 * n_work) + part_bytes;
+  if (need > static_cast<int64_t>(kScratchBytes))
+    return fail(METRO_E_CAPACITY, "attn_decode_noalloc: %lld scratch bytes needed, %zu available",
+                (long long)need, kScratchBytes);
+  void* base = nullptr;
+  st = scratch_on_current_device(&base);
+  if (st != METRO_OK) return st;
+  char* at = static_cast<char*>(base);
+  auto take = [&](int64_t bytes) {
+    char* p = at;
+    at += bytes;
+    return p;
+  };
+  int32_t* d_ctx = reinterpret_cast<int32_t*>(take(span(rows)));
+  int32_t* d_q = reinterpret_cast<int32_t*>(take(span(rows)));
+  int32_t* d_bto = reinterpret_cast<int32_t*>(take(span(rows)));
+  int32_t* d_work0 = reinterpret_cast<int32_t*>(take(span(rows)));
+  int32_t* d_ns = reinterpret_cast<int32_t*>(take(span(rows)));
+  int32_t* d_bt = reinterpret_cast<int32_t*>(take(span(pages)));
+  int32_t* d_work = reinterpret_cast<int32_t*>(take(span(2 * n_work)));
+  float* d_part = reinterpret_cast<float*>(take(part_bytes));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  HIP_TRY(nullptr, hipMemcpyAsync(d_ctx, ctx, rows * 4, hipMemcpyHostToDevice, s));
+  HIP_TRY(nullptr, hipMemcpyAsync(d_bt, block_tables, pages * 4, hipMemcpyHostToDevice, s));
+  hipLaunchKernelGGL(describe_decode_kernel, dim3(1), dim3(64), 0, s, d_ctx, rows, d_q, d_bto, d_work0, d_ns,
+                     d_work);
+  HIP_TRY(nullptr, hipGetLastError());
+  metro::AttnArgs a{};
+  a.q = q;
+  a.kv = kv;
+  a.work = d_work;
+  a.row_ctx = d_ctx;
+  a.row_qrow = d_q;
+  a.row_bt = d_bto;
+  a.row_work = d_work0;
+  a.row_nsplit = d_ns;
+  a.bt = d_bt;
+  a.part = d_part;
+  a.out = out;
+  a.n_work = static_cast<int>(n_work);
+  a.rows = rows;
+  a.nq = nq;
+  a.nkv = nkv;
+  a.hd = hd;
+  a.scale = 1.0f / std::sqrt(static_cast<float>(hd));
+  HIP_TRY(nullptr, metro::launch_attn_decode(a, s));
+  if (n_work > rows) HIP_TRY(nullptr, metro::launch_attn_combine(a, s));
   return METRO_OK;
 }
 

@@ -81,6 +81,7 @@ _SIGS = {
     "metro_op_argmax": (_i32, [_vp, _i32, _i32, _vp, _vp]),
     "metro_op_attn_decode": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp]),
     "metro_op_attn_prefill": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
+    "metro_op_attn_decode_noalloc": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp]),
     "metro_sched_create": (_i32, [_vp, _vp, ctypes.POINTER(_vp)]),
     "metro_sched_destroy": (None, [_vp]),
     "metro_sched_next": (_i32, [_vp, ctypes.POINTER(_i32), ctypes.POINTER(_i32), _vp, _i32, ctypes.POINTER(_i32)]),
@@ -300,6 +301,15 @@ def op_attn_decode(q, kv, n_pages: int, nq: int, nkv: int, hd: int, ctx, block_t
     bt = _host_i32(block_tables)
     check(lib.metro_op_attn_decode(_ptr(q), _ptr(kv), n_pages, nq, nkv, hd, len(c), c.ctypes.data, bt.ctypes.data,
                                    _ptr(out), _stream(stream)))
+
+
+def op_attn_decode_noalloc(q, kv, n_pages: int, nq: int, nkv: int, hd: int, ctx, block_tables, out, stream=None):
+    """op_attn_decode without device allocation (the library's fixed scratch
+    array; asynchronous on the stream)."""
+    c = _host_i32(ctx)
+    bt = _host_i32(block_tables)
+    check(lib.metro_op_attn_decode_noalloc(_ptr(q), _ptr(kv), n_pages, nq, nkv, hd, len(c), c.ctypes.data,
+                                           bt.ctypes.data, _ptr(out), _stream(stream)))
 
 
 def op_attn_prefill(q, kv, n_pages: int, nq: int, nkv: int, hd: int, cu_q, ctx_before, block_tables, out,
