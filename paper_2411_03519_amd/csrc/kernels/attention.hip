@@ -67,13 +67,14 @@ __device__ __forceinline__ void split_bf16(float p0, float p1, uint32_t& hi, uin
 // Keys past the end of a context sit in slots of the last page that no call
 // has written (or that hold a closed sequence's values): their softmax weight
 // is 0, but 0 times a NaN or Inf bit pattern there would still poison the
-// output, so their V values are zeroed in the operand.  A V^T operand word
-// holds the bf16 values of keys 4g + 2i and 4g + 2i + 1 (i = word % 2) of one
-// dim; keep_keys(n) is the mask of the word pair for keys below n.
-__device__ __forceinline__ uint2 keep_keys(int grp, int n) {
-  const int k0 = 4 * grp;
-  auto half = [&](int k) { return k < n ? 0xffffu : 0u; };
-  return make_uint2(half(k0) | (half(k0 + 1) << 16), half(k0 + 2) | (half(k0 + 3) << 16));
+// output, so their V values are zeroed.  Decode: in the operand of the row's
+// partly filled last page, which is taken outside the page ring so the ring
+// holds no extra registers; a V^T operand word holds the bf16 values of two
+// consecutive keys k, k + 1 of one dim (k in the low half), and
+// keep_below(w, k, n) keeps those below n.  Prefill: in LDS, for the last
+// page pair of a query block.
+__device__ __forceinline__ uint32_t keep_below(uint32_t w, int k, int n) {
+  return k + 1 < n ? w : (k < n ? (w & 0xffffu) : 0u);
 }
 
 // ===========================================================================
@@ -139,7 +140,57 @@ __global__ __launch_bounds__(NW * 64) void attn_decode_kernel(AttnArgs a) {
     for (int c = 0; c < NT / 2; ++c) vf[sl][c] = *reinterpret_cast<const uint4*>(vp + 512 * c + 8 * lane);
   };
 
-  const int np = wave < n_pages ? (n_pages - wave + NW - 1) / NW : 0;
+  // One page: scores, online softmax, P.V.  `last` marks the row's partly
+  // filled last page: keys from ctx on get no weight and V = 0.
+  auto page_step = [&](const uint4* kp, uint4* vp, int p, bool last) __attribute__((always_inline)) {
+    f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < KQ; ++i) s = mfma_k32(kp[i], qf[i], s);
+    float sv[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sv[r] = (!last || p * kPage + 4 * grp + r < ctx) ? s[r] * qscale : -INFINITY;
+    float mp = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+    mp = fmaxf(mp, __shfl_xor(mp, 16, kWave));
+    mp = fmaxf(mp, __shfl_xor(mp, 32, kWave));
+    const float mn = fmaxf(m, mp);
+    const float corr = exp2f(m - mn);
+    m = mn;
+    float pv[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) pv[r] = exp2_hw(sv[r] - mn);
+    l = l * corr + ((pv[0] + pv[1]) + (pv[2] + pv[3]));
+    uint2 hi, lo;
+    split_bf16(pv[0], pv[1], hi.x, lo.x);
+    split_bf16(pv[2], pv[3], hi.y, lo.y);
+    if (last) {
+      const int n = ctx - p * kPage, k0 = 4 * grp;
+#pragma unroll
+      for (int c = 0; c < NT / 2; ++c) {
+        vp[c].x = keep_below(vp[c].x, k0, n);
+        vp[c].y = keep_below(vp[c].y, k0 + 2, n);
+        vp[c].z = keep_below(vp[c].z, k0, n);
+        vp[c].w = keep_below(vp[c].w, k0 + 2, n);
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < NT / 2; ++c) {
+      const uint2 v0 = make_uint2(vp[c].x, vp[c].y), v1 = make_uint2(vp[c].z, vp[c].w);
+      o[2 * c] *= corr;
+      o[2 * c] = mfma_k16(v0, hi, o[2 * c]);
+      o[2 * c] = mfma_k16(v0, lo, o[2 * c]);
+      o[2 * c + 1] *= corr;
+      o[2 * c + 1] = mfma_k16(v1, hi, o[2 * c + 1]);
+      o[2 * c + 1] = mfma_k16(v1, lo, o[2 * c + 1]);
+    }
+  };
+
+  // Full pages go through the register ring; a partly filled last page of the
+  // row (in this split) is taken afterwards by the wave it falls to, so the
+  // ring carries no masking.  Each wave's pages and their order are the same
+  // either way.
+  const bool part_last = (ctx % kPage) != 0 && p0 + n_pages == ceil_div(ctx, kPage);
+  const int n_full = n_pages - (part_last ? 1 : 0);
+  const int np = wave < n_full ? (n_full - wave + NW - 1) / NW : 0;
   for (int j0 = 0; j0 < np; j0 += 64) {
     const int nj = min(64, np - j0);
     // lane j: id of the wave's page j0 + j
@@ -150,44 +201,14 @@ __global__ __launch_bounds__(NW * 64) void attn_decode_kernel(AttnArgs a) {
 #pragma unroll
       for (int sl = 0; sl < PD; ++sl) {
         const int it = base + sl;
-        if (it < nj) {
-          const int p = p0 + wave + NW * (j0 + it);
-          f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int i = 0; i < KQ; ++i) s = mfma_k32(kf[sl][i], qf[i], s);
-          float sv[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) sv[r] = (p * kPage + 4 * grp + r < ctx) ? s[r] * qscale : -INFINITY;
-          float mp = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
-          mp = fmaxf(mp, __shfl_xor(mp, 16, kWave));
-          mp = fmaxf(mp, __shfl_xor(mp, 32, kWave));
-          const float mn = fmaxf(m, mp);
-          const float corr = exp2f(m - mn);
-          m = mn;
-          float pv[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) pv[r] = exp2_hw(sv[r] - mn);
-          l = l * corr + ((pv[0] + pv[1]) + (pv[2] + pv[3]));
-          uint2 hi, lo;
-          split_bf16(pv[0], pv[1], hi.x, lo.x);
-          split_bf16(pv[2], pv[3], hi.y, lo.y);
-          const bool tail = (p + 1) * kPage > ctx;  // the row's last page, partly filled
-          const uint2 keep = tail ? keep_keys(grp, ctx - p * kPage) : make_uint2(~0u, ~0u);
-#pragma unroll
-          for (int c = 0; c < NT / 2; ++c) {
-            const uint2 v0 = make_uint2(vf[sl][c].x & keep.x, vf[sl][c].y & keep.y),
-                        v1 = make_uint2(vf[sl][c].z & keep.x, vf[sl][c].w & keep.y);
-            o[2 * c] *= corr;
-            o[2 * c] = mfma_k16(v0, hi, o[2 * c]);
-            o[2 * c] = mfma_k16(v0, lo, o[2 * c]);
-            o[2 * c + 1] *= corr;
-            o[2 * c + 1] = mfma_k16(v1, hi, o[2 * c + 1]);
-            o[2 * c + 1] = mfma_k16(v1, lo, o[2 * c + 1]);
-          }
-        }
+        if (it < nj) page_step(kf[sl], vf[sl], p0 + wave + NW * (j0 + it), false);
         load_page(sl, __builtin_amdgcn_readlane(pid, min(it + PD, nj - 1)));
       }
     }
+  }
+  if (part_last && wave == n_full % NW) {
+    load_page(0, bt[n_full]);
+    page_step(kf[0], vf[0], p0 + n_full, true);
   }
   l += __shfl_xor(l, 16, kWave);
   l += __shfl_xor(l, 32, kWave);
@@ -253,6 +274,25 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(AttnArgs a) {
     O += pp[d] * f;
   }
   a.out[(static_cast<size_t>(a.row_qrow[row]) * a.nq + j) * hd + d] = f32_to_bf16(O / L);
+}
+
+// Zero the V^T entries of keys n0 and beyond in the two V^T page tiles of a
+// prefill stage (2 x 16 keys x HD bf16 in LDS), one 32-bit word (two keys of
+// one dim) per step.  Out of line: inlined, its index arithmetic raised the
+// register count of the whole kernel.
+template <int HD>
+__device__ __attribute__((noinline)) void zero_v_past(uint32_t* vt, int n0, int tid, int nthreads) {
+  constexpr int kWordsPerPage = kPage * HD / 2;
+  for (int w = tid; w < 2 * kWordsPerPage; w += nthreads) {
+    const int pg = w / kWordsPerPage, in = w % kWordsPerPage;
+    // word in of a tile: element pair 2*in, 2*in + 1 = keys 4g + 2j, +1 of dim e
+    const int j = in & 1, g = (in >> 6) & 3;   // (((e/32)*4 + g)*16 + e%16)*8 + u*4 + (2j|2j+1)
+    const int k = pg * kPage + 4 * g + 2 * j;
+    uint32_t v = vt[w];
+    if (k >= n0) v = 0u;
+    else if (k + 1 >= n0) v &= 0xffffu;
+    vt[w] = v;
+  }
 }
 
 // ===========================================================================
@@ -360,6 +400,13 @@ __global__ __launch_bounds__(NW * 64) void attn_prefill_kernel(PrefillAttnArgs a
     lds_barrier();
     if (pair + 3 < n_pairs) issue(pair + 3);
     const uint4(*st)[PCH] = ring[pair % NS];
+    // Keys past the block's last position (never written, or the stand-in
+    // page of an odd count) get V = 0 in the stage before any wave reads it:
+    // only the last pair can hold them, so only it pays the extra barrier.
+    if (const int n0 = last_pos + 1 - 2 * pair * kPage; n0 < 2 * kPage) {
+      zero_v_past<HD>(reinterpret_cast<uint32_t*>(&ring[pair % NS][2][0]), n0, tid, NW * 64);
+      __syncthreads();
+    }
 
     // K operand of both pages (A of S^T): key row col, dims 32i + 8grp .. +7;
     // V^T operand over the pair: dims of tile t, keys 4grp .. 4grp+3 of each
@@ -370,20 +417,11 @@ __global__ __launch_bounds__(NW * 64) void attn_prefill_kernel(PrefillAttnArgs a
     for (int pg = 0; pg < 2; ++pg)
 #pragma unroll
       for (int i = 0; i < KQ; ++i) kf[pg][i] = st[pg][64 * i + lane];
-    // keys past the block's last position (never written, or the stand-in
-    // page of an odd count) get V = 0: keep masks for the pair's two pages
-    const int past = (2 * pair) * kPage;  // position of the pair's first key
-    const bool tail = past + 2 * kPage - 1 > last_pos;
-    uint2 keep0 = make_uint2(~0u, ~0u), keep1 = keep0;
-    if (tail) {
-      keep0 = keep_keys(grp, last_pos + 1 - past);
-      keep1 = keep_keys(grp, last_pos + 1 - past - kPage);
-    }
     auto vt_operand = [&](int t) __attribute__((always_inline)) {
       const int vo = 128 * (t >> 1) + 2 * lane + (t & 1);  // in 8-byte units
       const uint2 va = reinterpret_cast<const uint2*>(st[2])[vo];
       const uint2 vb = reinterpret_cast<const uint2*>(st[3])[vo];
-      return make_uint4(va.x & keep0.x, va.y & keep0.y, vb.x & keep1.x, vb.y & keep1.y);
+      return make_uint4(va.x, va.y, vb.x, vb.y);
     };
     uint4 vf[NQ > 1 ? NT : 1];
     if constexpr (NQ > 1) {
