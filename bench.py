@@ -238,16 +238,63 @@ def hbm_roofline(bytes_total, seconds, what):
             "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": what}
 
 
+def sched_trace_batches(metro, synth, seed, n_agents=1000, ticks=200):
+    """Ready batches of the agent trace with the readiness of the library's
+    out-of-order scheduler (the rules of §3.3: coupled clusters, a blocking
+    radius that grows with the step gap; radius_p 4, max_vel 1, Chebyshev)
+    instead of the constant radius 5: on the seeded world of SimWorld, each
+    tick hands out every ready cluster, decodes one token for every member
+    with budget left (a busy step's budget is its work in tokens), and
+    acknowledges a cluster with its members' moves once all budgets are
+    spent."""
+    world = synth.SimWorld(seed, n_agents, grid=(100, 140))
+    sched = metro.Scheduler(world.start, 4.0, 1.0, metro.DIST_CHEBYSHEV, target_step=10 ** 6)
+    pos = [tuple(int(v) for v in p) for p in world.start]
+    budget = {}       # agent -> tokens left in its current step
+    cluster_of = {}   # cluster -> (step, members)
+    batches = []
+
+    def ack(cid):
+        step, members = cluster_of.pop(cid)
+        new = [world.move(a, step, pos[a]) for a in members]
+        for a, p in zip(members, new):
+            pos[a] = p
+        sched.ack(cid, new)
+
+    for _ in range(ticks):
+        while True:                      # hand out; idle clusters finish at once
+            got = sched.next()
+            if got is None:
+                break
+            cid, step, members = got
+            cluster_of[cid] = (step, members)
+            for a in members:
+                budget[a] = world.work(a, step)
+            if all(budget[a] == 0 for a in members):
+                ack(cid)
+        run = np.array(sorted(a for a, b in budget.items() if b > 0), np.int64)
+        batches.append(run)
+        for a in run:
+            budget[a] -= 1
+        for cid in [c for c, (_, m) in cluster_of.items() if all(budget[a] == 0 for a in m)]:
+            ack(cid)
+    return batches
+
+
 def bench_trace(args, torch, metro, synth):
     """Decode driven by the seeded agent trace: 1000 agents with lognormal
     (median 1500) starting contexts, prefilled before timing; each of 200 ticks
     decodes one token for every ready agent (ready batches of ~50..800); then a
-    fixed-batch sweep over agents 0..B-1."""
+    fixed-batch sweep over agents 0..B-1.  ``--trace-rule sched`` takes the
+    ready batches from the library's scheduler (sched_trace_batches)."""
     shape = synth.LLAMA3_8B
     V = shape["vocab"]
     ctx = synth.trace_start_contexts(args.seed)
     n = len(ctx)
-    batches = [b for b in synth.agent_trace(args.seed) if len(b)]
+    if args.trace_rule == "sched":
+        batches = [b for b in sched_trace_batches(metro, synth, args.seed, n) if len(b)]
+    else:
+        batches = [b for b in synth.agent_trace(args.seed) if len(b)]
     sweep, sweep_steps = [50, 100, 200, 400, 800], 3
     lens = np.array([len(c) for c in ctx], np.int64)
     extra = np.zeros(n, np.int64)
@@ -309,50 +356,59 @@ def bench_trace(args, torch, metro, synth):
             "ms_per_step": round(sum(ms), 2), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
             "dtype": "bf16", "data": "synthetic: seeded agent trace and token ids, random N(0,0.02) bf16 weights",
             "config": {"workload": "Llama-3-8B-shaped decoder driven by a seeded agent trace: 1000 agents on a "
-                                   "100x140 grid, Chebyshev radius 5, 200 ticks; contexts lognormal(median 1500) "
-                                   "clipped to [256,4096], prefilled before timing",
+                                   "100x140 grid, 200 ticks, readiness "
+                                   + ("of the out-of-order scheduler (rules of §3.3, radius_p 4, max_vel 1)"
+                                      if args.trace_rule == "sched" else "Chebyshev radius 5")
+                                   + "; contexts lognormal(median 1500) clipped to [256,4096], prefilled before "
+                                     "timing",
                        "ticks": len(batches), "decode_tokens": tokens, "batch_min": int(sizes.min()),
                        "batch_median": float(np.median(sizes)), "batch_max": int(sizes.max()),
                        "context_tokens": int(lens.sum())},
             "roofline": roof, "fixed_batch": fixed}
 
 
-def sched_calls(world, seed, step, agent, vocab):
-    """The LLM call of one agent step: None for an idle step, else (prompt
-    token ids, tokens to generate); prompts lognormal(median 640, sigma 0.5)
-    clipped to [128, 2048] (the paper's calls average 642.6 tokens in and 21.9
-    out, §4.2), 8 output tokens per unit of the step's work, 8..128."""
+def sched_chain(world, seed, step, agent, vocab, max_calls):
+    """The LLM calls of one agent step, issued one after another (an agent
+    step of the paper's simulation chains calls such as perceive, plan and
+    react): none for an idle step, else min(work, max_calls) calls, each a
+    prompt of lognormal(median 640, sigma 0.5) tokens clipped to [128, 2048]
+    and lognormal(median 18, sigma 0.6) outputs clipped to [4, 64] (the
+    paper's calls average 642.6 tokens in and 21.9 out, §4.2)."""
     work = world.work(agent, step)
-    if work == 0:
-        return None
-    rng = np.random.Generator(np.random.PCG64([seed, 11, agent, step]))
-    plen = int(np.clip(np.rint(np.exp(rng.normal(np.log(640.0), 0.5))), 128, 2048))
-    return rng.integers(0, vocab, size=plen, dtype=np.int64), int(np.clip(8 * work, 8, 128))
+    calls = []
+    for k in range(min(work, max_calls)):
+        rng = np.random.Generator(np.random.PCG64([seed, 11, agent, step, k]))
+        plen = int(np.clip(np.rint(np.exp(rng.normal(np.log(640.0), 0.5))), 128, 2048))
+        n_out = int(np.clip(np.rint(np.exp(rng.normal(np.log(18.0), 0.6))), 4, 64))
+        calls.append((rng.integers(0, vocab, size=plen, dtype=np.int64), n_out))
+    return calls
 
 
-def run_sched_loop(model, sched, world, seed, shape, torch, max_batch, chunk=512, group=16, mixed=False,
-                   max_tokens=16 * 512, hold_tokens=0, hold_iters=0):
-    """Closed loop of scheduler and engine: hand-out clusters run one LLM call
-    per agent step (idle steps none); each engine iteration prefills the calls
-    that arrived (chunked, ``group`` calls per prefill call) and then decodes one
-    token for every running call; a cluster is acknowledged, with its agents'
-    moves, when its last call finishes.  With ``mixed`` an iteration that has
-    arrivals runs one forward for both: every running call's next token as a
-    one-token item plus the arrivals' prompt chunks (up to ``max_tokens``), so
-    the weights are read once for both.  Arrived calls wait (at most
-    ``hold_iters`` iterations) until their prompts add up to ``hold_tokens``,
-    unless nothing else runs, so that prompts are prefilled in larger batches.
-    Returns wall seconds and counters."""
+def run_engine_loop(model, metro, sched, world, seed, shape, torch, max_items, max_tokens=8192, chunk=512,
+                    priority=True, max_calls=4):
+    """Closed loop of the scheduler (metro_sched_*) and the library's mixed
+    continuous batching (metro_engine_*): every ready cluster is handed out;
+    each member submits the first call of its step's chain, tagged with its
+    step; each finished call submits the next; a cluster is acknowledged, with
+    its agents' moves, once every member's chain is done.  One engine step is
+    one forward.  Returns wall seconds, token counts and the achieved
+    parallelism (outstanding requests averaged over the run, §4.2)."""
     V = shape["vocab"]
+    eng = metro.Engine(model, max_tokens=max_tokens, chunk=chunk, max_items=max_items, priority=priority)
     pos = [tuple(int(v) for v in p) for p in world.start]
-    last = torch.zeros(max_batch + 8, dtype=torch.int32, device="cuda")
-    free_slots = list(range(max_batch + 8))
-    clusters = {}       # cluster -> [step, members, calls still running]
-    arriving, running = [], []   # calls: dict(seq, slot, left, cluster)
-    stats = {"prefill_tokens": 0, "decode_tokens": 0, "iterations": 0, "batch_sum": 0, "agent_steps": 0,
-             "calls": 0, "max_running": 0}
-    logits = None
-    nxt = torch.empty(max_batch, dtype=torch.int32, device="cuda")
+    clusters = {}      # cluster -> [step, members, chains still running]
+    chains = {}        # request id -> (cluster, agent, step, calls still to issue)
+    stats = {"forwards": 0, "agent_steps": 0, "calls": 0}
+    next_id = [0]
+    area = 0.0
+
+    def submit(cid, agent, step, calls):
+        rid = next_id[0]
+        next_id[0] += 1
+        prompt, n_out = calls[0]
+        eng.submit(rid, step, prompt, n_out)
+        chains[rid] = (cid, agent, step, calls[1:])
+        stats["calls"] += 1
 
     def finish(cid):
         step, members, _ = clusters.pop(cid)
@@ -365,164 +421,86 @@ def run_sched_loop(model, sched, world, seed, shape, torch, max_batch, chunk=512
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     while True:
-        # hand out every ready cluster (idle clusters finish at once and may free others)
         while True:
             got = sched.next()
             if got is None:
                 break
             cid, step, members = got
-            calls = [(a, sched_calls(world, seed, step, a, V)) for a in members]
-            calls = [(a, c) for a, c in calls if c is not None]
-            clusters[cid] = [step, members, len(calls)]
-            if not calls:
+            work = [(a, sched_chain(world, seed, step, a, V, max_calls)) for a in members]
+            work = [(a, c) for a, c in work if c]
+            clusters[cid] = [step, members, len(work)]
+            if not work:
                 finish(cid)
                 continue
-            for a, (prompt, n_out) in calls:
-                arriving.append({"seq": model.seq_open(), "slot": free_slots.pop(), "prompt": prompt,
-                                 "left": n_out, "cluster": cid})
-                stats["calls"] += 1
-        if not arriving and not running:
+            for a, calls in work:
+                submit(cid, a, step, calls)
+        if not chains:
             break
-        # hold back the arrivals until enough prompt tokens wait (or too long)
-        if arriving and hold_tokens > 0 and any(c["left"] > 0 for c in running):
-            waited = stats["iterations"] - min(c.get("since", stats["iterations"]) for c in arriving)
-            if sum(len(c["prompt"]) for c in arriving) < hold_tokens and waited < hold_iters:
-                for c in arriving:
-                    c.setdefault("since", stats["iterations"])
-                held, arriving = arriving, []
-            else:
-                held = []
-        else:
-            held = []
-        mixed_done = False
-        if mixed and arriving:
-            # one forward: every running call's next token as a one-token item,
-            # then the arrivals' prompt chunks while the token budget lasts;
-            # further forwards for what is left of the prompts
-            mixed_done = True
-            live = [c for c in running if c["left"] > 0][:max_batch]
-            host_last = last.cpu().numpy()
-            items = [(c, host_last[c["slot"]:c["slot"] + 1].astype(np.int64), True) for c in live]
-            pend = [(c, 0) for c in arriving]
-            while items or pend:
-                budget = max_tokens - len(items)
-                rest = []
-                for c, off in pend:
-                    take = min(chunk, len(c["prompt"]) - off)
-                    if len(items) < max_batch and take <= budget:
-                        items.append((c, c["prompt"][off:off + take], off + take >= len(c["prompt"])))
-                        budget -= take
-                        if off + take < len(c["prompt"]):
-                            rest.append((c, off + take))
-                    else:
-                        rest.append((c, off))
-                nt = torch.empty(len(items), dtype=torch.int32, device="cuda")
-                model.prefill_chunk([c["seq"] for c, _, _ in items], [t for _, t, _ in items], None, nt)
-                upd = [j for j, (_, _, fin) in enumerate(items) if fin]
-                if upd:
-                    slots = torch.tensor([items[j][0]["slot"] for j in upd], dtype=torch.int64, device="cuda")
-                    last[slots] = nt[torch.tensor(upd, dtype=torch.int64, device="cuda")]
-                for c, _, fin in items:
-                    if fin:   # a decode token, or the first token of a finished prompt
-                        c["left"] -= 1
-                        stats["decode_tokens"] += 1
-                stats["iterations"] += 1
-                stats["batch_sum"] += len(items)
-                items, pend = [], rest
-            for c in arriving:
-                stats["prefill_tokens"] += len(c["prompt"])
-            running.extend(arriving)
-            arriving = []
-        # prefill the calls that arrived; their first token comes from the prefill
-        for g0 in range(0, len(arriving), group):
-            batch = arriving[g0:g0 + group]
-            off = 0
-            while True:
-                items = [c for c in batch if off < len(c["prompt"])]
-                if not items:
-                    break
-                nt = torch.empty(len(items), dtype=torch.int32, device="cuda")
-                model.prefill_chunk([c["seq"] for c in items], [c["prompt"][off:off + chunk] for c in items], None, nt)
-                done = [j for j, c in enumerate(items) if off + chunk >= len(c["prompt"])]
-                if done:
-                    slots = torch.tensor([items[j]["slot"] for j in done], dtype=torch.int64, device="cuda")
-                    last[slots] = nt[torch.tensor(done, dtype=torch.int64, device="cuda")]
-                off += chunk
-            for c in batch:
-                stats["prefill_tokens"] += len(c["prompt"])
-                c["left"] -= 1
-                stats["decode_tokens"] += 1
-            running.extend(batch)
-        arriving = []
-        # one decode token for every running call that still has tokens to make
-        live = [] if mixed_done else [c for c in running if c["left"] > 0]
-        if live:
-            for b0 in range(0, len(live), max_batch):
-                part = live[b0:b0 + max_batch]
-                idx = torch.tensor([c["slot"] for c in part], dtype=torch.int64, device="cuda")
-                model.decode_step([c["seq"] for c in part], last[idx], logits, nxt[:len(part)])
-                last[idx] = nxt[:len(part)]
-                for c in part:
-                    c["left"] -= 1
-                stats["decode_tokens"] += len(part)
-                stats["iterations"] += 1
-                stats["batch_sum"] += len(part)
-            stats["max_running"] = max(stats["max_running"], len(live))
-        arriving = held
-        # retire finished calls; acknowledge finished clusters
-        still = []
-        for c in running:
-            if c["left"] > 0:
-                still.append(c)
+        outstanding = len(chains)
+        t1 = time.perf_counter()
+        eng.step()
+        area += outstanding * (time.perf_counter() - t1)
+        stats["forwards"] += 1
+        for rid in eng.finished():
+            eng.result(rid)
+            cid, agent, step, rest = chains.pop(rid)
+            if rest:
+                submit(cid, agent, step, rest)
                 continue
-            model.seq_close(c["seq"])
-            free_slots.append(c["slot"])
-            cl = clusters[c["cluster"]]
+            cl = clusters[cid]
             cl[2] -= 1
             if cl[2] == 0:
-                finish(c["cluster"])
-        running = still
+                finish(cid)
     torch.cuda.synchronize()
     stats["seconds"] = time.perf_counter() - t0
+    es = eng.stats()
+    eng.close()
+    # output tokens: one per decode item plus each call's first token (from its last prompt chunk)
+    stats.update(prompt_tokens=es["prompt_tokens"], decode_tokens=es["decode_tokens"] + stats["calls"],
+                 items=es["items"])
+    stats["achieved_parallelism"] = area / stats["seconds"]
     return stats
 
 
 def bench_sched(args, torch, metro, synth):
-    """The out-of-order scheduler (Algorithm 3) in closed loop with the engine,
-    against the parallel-sync baseline (Algorithm 1) on the same seeded world
-    and calls (100 x 140 grid, radius_p 4, max_vel 1): 25 agents for 16 steps
-    (the paper's village size) and 200 agents for 4 steps."""
+    """The out-of-order scheduler (Algorithm 3) in closed loop with the
+    library's mixed continuous batching, against the parallel-sync baseline
+    (Algorithm 1) on the same seeded world and calls (100 x 140 grid, radius_p
+    4, max_vel 1, chains of up to 4 calls per busy agent step), with step
+    priority on and off: 25 agents for 12 steps (the paper's village size),
+    200 agents for 3 steps and 500 agents for 2."""
     shape = synth.LLAMA3_8B
-    cases = [(25, 16), (200, 4)]
-    max_batch = max(n for n, _ in cases)
-    pages = max_batch * ((2048 + 128 + 15) // 16 + 1) + 64
-    model = metro.Model(shape, max_batch=max_batch, max_tokens=16 * 512, max_context=2048 + 128 + 16,
-                        max_seqs=max_batch + 16, kv_pool_bytes=pages * 16 * kv_token_bytes(shape), seed=args.seed)
+    cases = [(25, 12), (200, 3), (500, 2)]
+    max_items = 256
+    pages = 640 * ((2048 + 64 + 15) // 16 + 1) + 64
+    model = metro.Model(shape, max_batch=max_items, max_tokens=8192 + max_items, max_context=2048 + 64 + 16,
+                        max_seqs=1024, kv_pool_bytes=pages * 16 * kv_token_bytes(shape), seed=args.seed)
     warm = synth.SimWorld(args.seed + 1, 8)
-    run_sched_loop(model, metro.Scheduler(warm.start, 4.0, 1.0, target_step=1), warm, args.seed, shape, torch,
-                   max_batch)
+    run_engine_loop(model, metro, metro.Scheduler(warm.start, 4.0, 1.0, target_step=1), warm, args.seed, shape,
+                    torch, max_items)
     out = {}
     for n_agents, steps in cases:
         world = synth.SimWorld(args.seed, n_agents, grid=(100, 140))
         res = {}
-        policies = {"separate": {}, "mixed": {"mixed": True},
-                    "mixed+hold": {"mixed": True, "hold_tokens": 8192, "hold_iters": 8}}
-        for policy, kw in policies.items():
+        for priority in (True, False):
+            pol = "priority" if priority else "no_priority"
             for mode in ("parallel_sync", "out_of_order"):
                 sched = metro.Scheduler(world.start, 4.0, 1.0, metro.DIST_CHEBYSHEV, steps,
                                         sync=mode == "parallel_sync")
-                st = run_sched_loop(model, sched, world, args.seed, shape, torch, max_batch, **kw)
+                st = run_engine_loop(model, metro, sched, world, args.seed, shape, torch, max_items,
+                                     priority=priority, max_calls=args.max_calls)
                 st["seconds"] = round(st["seconds"], 3)
-                st["tokens_per_s"] = round((st["prefill_tokens"] + st["decode_tokens"]) / st["seconds"], 1)
-                st["mean_batch"] = round(st["batch_sum"] / max(1, st["iterations"]), 1)
-                res[f"{mode}/{policy}"] = st
-                log(f"sched {n_agents} agents x {steps} steps, {mode}, {policy} forwards: {st}")
-            res[f"speedup_vs_parallel_sync/{policy}"] = round(
-                res[f"parallel_sync/{policy}"]["seconds"] / res[f"out_of_order/{policy}"]["seconds"], 3)
+                st["achieved_parallelism"] = round(st["achieved_parallelism"], 2)
+                st["tokens_per_s"] = round((st["prompt_tokens"] + st["decode_tokens"]) / st["seconds"], 1)
+                st["mean_items"] = round(st["items"] / max(1, st["forwards"]), 1)
+                res[f"{mode}/{pol}"] = st
+                log(f"sched {n_agents} agents x {steps} steps, {mode}, {pol}: {st}")
+            res[f"speedup_vs_parallel_sync/{pol}"] = round(
+                res[f"parallel_sync/{pol}"]["seconds"] / res[f"out_of_order/{pol}"]["seconds"], 3)
         out[f"{n_agents}x{steps}"] = res
     model.close()
-    head = out["200x4"]["out_of_order/mixed"]
-    flops = 2.0 * shape["n_layers"] * layer_params(shape) * (head["prefill_tokens"] + head["decode_tokens"])
+    head = out["200x3"]["out_of_order/priority"]
+    flops = 2.0 * shape["n_layers"] * layer_params(shape) * (head["prompt_tokens"] + head["decode_tokens"])
     roof = {"bound": "mfma", "achieved": round(flops / head["seconds"] / 1e12, 1), "peak": BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s", "frac": round(flops / head["seconds"] / 1e12 / BF16_PEAK_TFLOPS, 4), "traffic": None,
             "kernel": "whole closed loop, linear-layer flops of every prefill and decode token over wall time"}
@@ -531,12 +509,13 @@ def bench_sched(args, torch, metro, synth):
             "ms_per_step": round(head["seconds"] * 1e3, 1), "higher_is_better": True, "scaling": "weak",
             "vs_baseline": None, "dtype": "bf16",
             "data": "synthetic: seeded world (SplitMix64 moves and work), prompt ids and random N(0,0.02) weights",
-            "config": {"workload": "Llama-3-8B-shaped decoder serving agents on a 100x140 grid: one LLM call per "
-                                   "busy agent step (prompts lognormal median 640, 8-128 output tokens), radius_p "
-                                   "4, max_vel 1, Chebyshev distance; 200 agents x 4 steps (value: mixed "
-                                   "prefill/decode forwards) and 25 x 16; separate and mixed forwards",
+            "config": {"workload": f"Llama-3-8B-shaped decoder serving agents on a 100x140 grid: chains of up to "
+                                   f"{args.max_calls} LLM calls per busy agent step (prompts lognormal median 640, outputs median "
+                                   "18), radius_p 4, max_vel 1, Chebyshev distance; library mixed continuous "
+                                   "batching (8192-token forwards, 512-token chunks) with step priority on/off; "
+                                   "value: 200 agents x 3 steps, out of order, priority",
                        "cases": [f"{n}x{s}" for n, s in cases]},
-            "speedup_vs_parallel_sync": out["200x4"]["speedup_vs_parallel_sync/mixed"],
+            "speedup_vs_parallel_sync": out["200x3"]["speedup_vs_parallel_sync/priority"],
             "cases": out, "roofline": roof}
 
 
@@ -776,6 +755,11 @@ def main():
                     help="agents (default): 25 agents, the benchmarked workload; trace: decode driven by the "
                          "seeded agent trace; prefix: prefix-heavy requests; 70b: Llama-3-70B shape at B=128; "
                          "sched: the out-of-order scheduler in closed loop with the engine vs parallel-sync")
+    ap.add_argument("--max-calls", type=int, default=4,
+                    help="sched workload: longest chain of LLM calls in one busy agent step")
+    ap.add_argument("--trace-rule", choices=["radius5", "sched"], default="radius5",
+                    help="trace workload: ready batches from the constant Chebyshev-5 readiness rule (default) or "
+                         "from the library's out-of-order scheduler with the rules of §3.3")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device copy three times (counter calibration) and exit")
     args = ap.parse_args()

@@ -80,6 +80,87 @@ metro_status metro_sched_ack(metro_sched* s, int32_t cluster, const int32_t* xy)
 metro_status metro_sched_state(const metro_sched* s, int32_t* steps, int32_t* xy, int32_t* state,
                                int32_t* running, int32_t* done);
 
+/* ---------------------------------------------------------------------------
+ * Mixed continuous batching of the agents' LLM requests: the serving loop
+ * between the scheduler above and the model of metro.h.
+ *
+ * Each request carries the step of the agent that issued it (§3.5: every
+ * request includes a step count, and smaller counts run first).  One
+ * metro_engine_step runs one forward pass holding
+ *   1. the next token of every running request (prompt done, outputs left):
+ *      a one-token item each, lowest step first when more than max_items run
+ *      (a request is never preempted mid-generation, §3.5);
+ *   2. in the token budget left (max_tokens minus those tokens), prompt chunks
+ *      of at most `chunk` tokens of waiting requests, admitted lowest step
+ *      first, ties by submission order (priority = 1), or in submission order
+ *      alone (priority = 0), until max_items items or the budget is used; a
+ *      request's last chunk yields its first output token.
+ * So prompt prefill and decode share each pass over the weights (chunked
+ * prefill mixed with decode, the prior art cited in §5).  A forward with no
+ * prompt chunk runs metro_decode_step, otherwise metro_prefill_chunk.  After
+ * the forward the engine waits for the greedy tokens on `stream`, appends
+ * them to their requests and retires those that have all n_out tokens (their
+ * sequences are closed).
+ *
+ * With model == NULL the engine only plans: metro_engine_step forms the items
+ * as above and appends stand-in tokens without device work (for checking the
+ * admission rules on a host without a GPU).
+ * Errors: METRO_E_INVAL (NULL, bad sizes, a live request id), METRO_E_SEQ
+ * (unknown request), METRO_E_NOMEM, and whatever the model calls return
+ * (e.g. METRO_E_NOPAGES: no request's state changes, the step may be retried
+ * after others retire). */
+typedef struct metro_engine metro_engine;
+
+typedef struct {
+  int32_t max_tokens; /* tokens of one forward (decode tokens + prompt chunks), <= the model's max_tokens */
+  int32_t chunk;      /* prompt tokens of one request per forward */
+  int32_t max_items;  /* requests in one forward, <= the model's max_batch */
+  int32_t priority;   /* 1: lowest step first (§3.5); 0: submission order */
+} metro_engine_config;
+
+typedef struct {
+  int64_t forwards;      /* forward passes run */
+  int64_t items;         /* items over all forwards */
+  int64_t prompt_tokens; /* prompt tokens prefilled */
+  int64_t decode_tokens; /* one-token decode items */
+  int32_t live;          /* requests not yet finished */
+  int32_t waiting;       /* of which not yet through their prompt */
+} metro_engine_stats;
+
+/* Create an engine on a model (or NULL: planning only); the model must
+ * outlive it.  Errors: METRO_E_INVAL, METRO_E_NOMEM. */
+metro_status metro_engine_create(metro_model* model, const metro_engine_config* cfg, metro_engine** out);
+
+/* Close the sequences of unfinished requests and free the engine. */
+void metro_engine_destroy(metro_engine* engine);
+
+/* Queue a request: generate n_out tokens greedily after prompt[0 .. n_prompt)
+ * (host int32, copied).  Opens its sequence through the model's prefix
+ * cache (metro_seq_open_cached; with the cache off every prompt token is
+ * prefilled).  request must not name a live request. */
+metro_status metro_engine_submit(metro_engine* engine, int64_t request, int32_t step, const int32_t* prompt,
+                                 int32_t n_prompt, int32_t n_out);
+
+/* One forward (see above); *n_items = its items (0: nothing to run).
+ * Returns after the forward's tokens are on the host. */
+metro_status metro_engine_step(metro_engine* engine, void* stream, int32_t* n_items);
+
+/* The items of the last metro_engine_step, in forward order: request ids,
+ * tokens of each item, and 1 for a decode token, 0 for a prompt chunk.
+ * Writes min(cap, n) entries and n to *n. */
+metro_status metro_engine_last_plan(const metro_engine* engine, int64_t* requests, int32_t* tokens, int32_t* decode,
+                                    int32_t cap, int32_t* n);
+
+/* Requests retired since the last call, in retirement order (at most cap;
+ * the rest stay queued). */
+metro_status metro_engine_finished(metro_engine* engine, int64_t* requests, int32_t cap, int32_t* n);
+
+/* Output tokens of a request so far (min(cap, n) written, n to *n).  A
+ * finished request whose tokens all fit is released: its id may be reused. */
+metro_status metro_engine_result(metro_engine* engine, int64_t request, int32_t* tokens, int32_t cap, int32_t* n);
+
+metro_status metro_engine_get_stats(const metro_engine* engine, metro_engine_stats* stats);
+
 #ifdef __cplusplus
 }
 #endif

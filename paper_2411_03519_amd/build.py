@@ -24,6 +24,7 @@ BUILD = os.path.join(ROOT, "_build")
 SOURCES = [
     "csrc/kv_pool.cpp",
     "csrc/scheduler.cpp",
+    "csrc/engine.cpp",
     "csrc/runtime.hip",
     "csrc/kernels/elementwise.hip",
     "csrc/kernels/gemm.hip",

@@ -87,6 +87,14 @@ _SIGS = {
     "metro_sched_next": (_i32, [_vp, ctypes.POINTER(_i32), ctypes.POINTER(_i32), _vp, _i32, ctypes.POINTER(_i32)]),
     "metro_sched_ack": (_i32, [_vp, _i32, _vp]),
     "metro_sched_state": (_i32, [_vp, _vp, _vp, _vp, ctypes.POINTER(_i32), ctypes.POINTER(_i32)]),
+    "metro_engine_create": (_i32, [_vp, _vp, ctypes.POINTER(_vp)]),
+    "metro_engine_destroy": (None, [_vp]),
+    "metro_engine_submit": (_i32, [_vp, _i64, _i32, _vp, _i32, _i32]),
+    "metro_engine_step": (_i32, [_vp, _vp, ctypes.POINTER(_i32)]),
+    "metro_engine_last_plan": (_i32, [_vp, _vp, _vp, _vp, _i32, ctypes.POINTER(_i32)]),
+    "metro_engine_finished": (_i32, [_vp, _vp, _i32, ctypes.POINTER(_i32)]),
+    "metro_engine_result": (_i32, [_vp, _i64, _vp, _i32, ctypes.POINTER(_i32)]),
+    "metro_engine_get_stats": (_i32, [_vp, _vp]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _f = getattr(lib, _name)
@@ -379,3 +387,83 @@ class Scheduler:
         check(lib.metro_sched_state(self._h, steps.ctypes.data, xy.ctypes.data, st.ctypes.data,
                                      ctypes.byref(running), ctypes.byref(done)))
         return {"steps": steps, "xy": xy, "state": st, "running": running.value, "done": bool(done.value)}
+
+
+# ----------------------------------------------------------------------------
+# Mixed continuous batching engine (include/metro_sched.h)
+# ----------------------------------------------------------------------------
+
+class EngineConfig(ctypes.Structure):
+    _fields_ = [("max_tokens", ctypes.c_int32), ("chunk", ctypes.c_int32), ("max_items", ctypes.c_int32),
+                ("priority", ctypes.c_int32)]
+
+
+class EngineStats(ctypes.Structure):
+    _fields_ = [("forwards", ctypes.c_int64), ("items", ctypes.c_int64), ("prompt_tokens", ctypes.c_int64),
+                ("decode_tokens", ctypes.c_int64), ("live", ctypes.c_int32), ("waiting", ctypes.c_int32)]
+
+
+class Engine:
+    """metro_engine_*: requests in (``submit``), one forward per ``step()``,
+    finished request ids from ``finished()``, their tokens from ``result()``.
+    ``model`` None: planning only (no device work)."""
+
+    def __init__(self, model, max_tokens: int, chunk: int, max_items: int, priority: bool = True):
+        self._h = ctypes.c_void_p()
+        self.max_items = max_items
+        cfg = EngineConfig(max_tokens, chunk, max_items, 1 if priority else 0)
+        h = ctypes.c_void_p()
+        check(lib.metro_engine_create(model._h if model is not None else None, ctypes.byref(cfg), ctypes.byref(h)))
+        self._h = h
+        self._model = model
+
+    def close(self):
+        if self._h and lib is not None:
+            lib.metro_engine_destroy(self._h)
+        self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        self.close()
+
+    def submit(self, request: int, step: int, prompt, n_out: int) -> None:
+        p = _host_i32(prompt)
+        check(lib.metro_engine_submit(self._h, request, step, p.ctypes.data, len(p), n_out))
+
+    def step(self, stream=None) -> int:
+        n = ctypes.c_int32()
+        s = _stream(stream) if self._model is not None else None
+        check(lib.metro_engine_step(self._h, s, ctypes.byref(n)))
+        return n.value
+
+    def last_plan(self):
+        """[(request, tokens, is_decode)] of the last step, in forward order."""
+        cap = self.max_items
+        ids = np.zeros(cap, np.int64)
+        tok = np.zeros(cap, np.int32)
+        dec = np.zeros(cap, np.int32)
+        n = ctypes.c_int32()
+        check(lib.metro_engine_last_plan(self._h, ids.ctypes.data, tok.ctypes.data, dec.ctypes.data, cap,
+                                         ctypes.byref(n)))
+        return [(int(ids[i]), int(tok[i]), bool(dec[i])) for i in range(n.value)]
+
+    def finished(self):
+        out = []
+        buf = np.zeros(256, np.int64)
+        while True:
+            n = ctypes.c_int32()
+            check(lib.metro_engine_finished(self._h, buf.ctypes.data, len(buf), ctypes.byref(n)))
+            out += [int(x) for x in buf[:n.value]]
+            if n.value < len(buf):
+                return out
+
+    def result(self, request: int):
+        n = ctypes.c_int32()
+        check(lib.metro_engine_result(self._h, request, None, 0, ctypes.byref(n)))
+        buf = np.zeros(max(1, n.value), np.int32)
+        check(lib.metro_engine_result(self._h, request, buf.ctypes.data, len(buf), ctypes.byref(n)))
+        return buf[:n.value].copy()
+
+    def stats(self) -> dict:
+        st = EngineStats()
+        check(lib.metro_engine_get_stats(self._h, ctypes.byref(st)))
+        return {k: getattr(st, k) for k, _ in EngineStats._fields_}

@@ -503,3 +503,44 @@ def test_sync_check_mode_gives_the_same_results(metro, monkeypatch):
             outs.append((lg.cpu().numpy(), lg2.cpu().numpy()))
     np.testing.assert_array_equal(outs[0][0], outs[1][0])
     np.testing.assert_array_equal(outs[0][1], outs[1][1])
+
+
+@pytest.mark.parametrize("priority", [True, False])
+def test_engine_mixed_batches_match_oracle(metro, priority):
+    """The library's mixed continuous batching (metro_engine_*): requests with
+    different steps arrive over time; forwards mix one-token decode items with
+    prompt chunks under a 96-token budget (32 per chunk), then run decode-only.
+    Each request's greedy stream must be the oracle's (teacher-forced on the
+    stream itself; the first difference, if any, a tie)."""
+    w = synth.llama_weights(synth.TINY, 11, norm="random")
+    ref = OracleModel(LlamaShape(**synth.TINY), w)
+    rng = np.random.default_rng(31)
+    reqs = [(i, int(rng.integers(0, 4)), rng.integers(0, synth.TINY["vocab"], int(n)), int(k))
+            for i, (n, k) in enumerate([(70, 6), (5, 9), (130, 3), (33, 7), (64, 5), (1, 4)])]
+    with make_model(metro, synth.TINY, w, max_batch=8, max_tokens=128, max_context=256) as m:
+        eng = metro.Engine(m, max_tokens=96, chunk=32, max_items=8, priority=priority)
+        mixed = 0
+        for rid, step, prompt, n_out in reqs[:3]:
+            eng.submit(rid, step, prompt, n_out)
+        forwards = 0
+        while True:
+            if forwards == 2:
+                for rid, step, prompt, n_out in reqs[3:]:
+                    eng.submit(rid, step, prompt, n_out)
+            n = eng.step()
+            if n == 0 and forwards > 2:
+                break
+            plan = eng.last_plan()
+            mixed += any(d for _, _, d in plan) and any(not d for _, _, d in plan)
+            forwards += 1
+        assert sorted(eng.finished()) == [r[0] for r in reqs]
+        streams = {rid: eng.result(rid) for rid, *_ in reqs}
+        st = eng.stats()
+        eng.close()
+    assert mixed > 0, "no forward mixed decode tokens with prompt chunks"
+    assert st["prompt_tokens"] == sum(len(r[2]) for r in reqs)
+    for rid, step, prompt, n_out in reqs:
+        s = streams[rid]
+        assert len(s) == n_out
+        want = ref.teacher_forced(prompt, s[:-1])
+        check_tokens(s, want, f"engine request {rid}")
