@@ -24,6 +24,12 @@
  * bfloat16; products accumulate in fp32; the residual stream, RMS statistics,
  * attention scores, softmax and attention accumulation are fp32; logits are
  * fp32.  Greedy choice = lowest index among the maximal fp32 logits.
+ * Batch dependence: a projection's kernel and k split are chosen from the
+ * number of rows of the call, so a sequence's results depend on how many
+ * others share its call by fp32 rounding (at Llama-3-8B widths, depth 2,
+ * logits move by up to a few 1e-2 between batch sizes, the size of the fp32
+ * noise itself); calls of equal row count give bitwise equal rows whatever
+ * the other sequences are, and page placement never changes a result.
  *
  * Conventions for every call below.
  *  - Return value: METRO_OK or a negative metro_status; metro_last_error()

@@ -94,10 +94,10 @@ __device__ __forceinline__ uint32_t keep_below(uint32_t w, int k, int n) {
 // fill the CUs twice over, more resident waves pay once it is not.  Smaller
 // splits than 128 pages only moved time into the combine kernel.
 constexpr int kDecodeWaves = 16;
-constexpr int kDecodeRing2MaxBlocks = 512;  // workgroups up to which PD = 2
+constexpr int kDecodeRing2MaxWaves = 512 * 16;  // waves of the grid up to which PD = 2
 
 template <int HD, int G, int NW, int PD, int PS = kDecodePagesPerSplit>
-__global__ __launch_bounds__(NW * 64) void attn_decode_kernel(AttnArgs a) {
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(4))) void attn_decode_kernel(AttnArgs a) {
   constexpr int KQ = HD / 32;  // score MFMAs per page
   constexpr int NT = HD / 16;  // output tiles (pairs share one 16-byte V load)
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -535,7 +535,7 @@ template <int HD>
 static hipError_t launch_decode_hd(const AttnArgs& a, hipStream_t s) {
   constexpr int NW = kDecodeWaves;
   const dim3 grid(a.n_work * a.nkv), block(NW * 64);
-  const bool ring2 = static_cast<int64_t>(a.n_work) * a.nkv <= kDecodeRing2MaxBlocks;
+  const bool ring2 = static_cast<int64_t>(a.n_work) * a.nkv * NW <= kDecodeRing2MaxWaves;
   switch (a.nq / a.nkv) {
     case 1: return launch_decode_g<HD, 1, NW>(ring2, grid, block, a, s);
     case 2: return launch_decode_g<HD, 2, NW>(ring2, grid, block, a, s);

@@ -168,7 +168,6 @@ __global__ __launch_bounds__(NW * 64) void gemm_skinny_kernel(const uint16_t* __
     }
   }
 
-  mfma_drain();
   __shared__ f32x4 red[NW][NT * MT][kWave];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt)
@@ -495,7 +494,6 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
   read_frags(nk - 1, 1, a1, b1);
   mfmas(a0, b0);
   mfmas(a1, b1);
-  mfma_drain();
 
   // Fully unrolled (acc must stay in registers).  Slice sums are stored raw:
   // to part[slice][m][n] with KS > 1, to part[unit][m - m0][n - n0] for a

@@ -301,3 +301,53 @@ def test_70b_widths_batch_128(metro):
         dec = decode_fed(m, seqs, feeds, [i])
     got, toks = stitched(pre, dec, i)
     compare(f"70B widths agent {i} ({lens[i]} tokens)", got, toks, want, f32, bounds)
+
+
+def test_8b_widths_logit_drift_across_batch_sizes(metro):
+    """The GEMM kernel and its k split are chosen from a call's row count, so
+    one agent's decode logits are bitwise the same in batches of equal size but
+    may differ by fp32 rounding across sizes.  This measures that drift: eight
+    agents decoded alone and inside batches of 16 .. 800 (forks of the same
+    sequences, the same fed tokens), 8B widths at depth 2.  Every batch's
+    logits must stay within the float32 noise floor of the B = 1 ones (the
+    parity bound at these widths is 1.25x the oracle's spread of ~3e-2 max-abs;
+    two evaluations each inside it differ by at most twice that), and greedy
+    choices may differ only where B = 1's top-2 margin is below 2e-2."""
+    shape = synth.with_layers(synth.LLAMA3_8B, 2)
+    V = shape["vocab"]
+    Bmax = 800
+    rng = np.random.default_rng(12)
+    prompts = [rng.integers(0, V, int(n)) for n in rng.integers(40, 300, Bmax)]
+    feed = rng.integers(0, V, Bmax)
+    say("batch drift: drawing weights")
+    w = synth.llama_weights(shape, 4, workers=16)
+    m = metro.Model(shape, max_batch=Bmax, max_tokens=64 * 300, max_context=512, max_seqs=2 * Bmax + 8,
+                    kv_pool_bytes=16 << 30)
+    sizes = [1, 16, 25, 64, 65, 128, 200, 256, 400, 800]
+    with m:
+        m.load_weights(w)
+        seqs = [m.seq_open() for _ in prompts]
+        prefill_batched(m, seqs, prompts, 512, 64, [])
+        lg = torch.empty(Bmax, V, device="cuda")
+
+        def decode(rows_of_batch):
+            forks = [m.seq_fork(seqs[i], len(prompts[i])) for i in rows_of_batch]
+            B = len(forks)
+            m.decode_step(forks, torch.tensor(feed[rows_of_batch], dtype=torch.int32, device="cuda"), lg[:B])
+            out = lg[:min(B, 8)].cpu().numpy().astype(np.float64)
+            for f in forks:
+                m.seq_close(f)
+            return out
+
+        alone = np.stack([decode([i])[0] for i in range(8)])
+        rows = {B: decode(list(range(B))) for B in sizes[1:]}
+    margin = np.sort(alone, axis=1)[:, -1] - np.sort(alone, axis=1)[:, -2]
+    for B in sizes[1:]:
+        got = rows[B]
+        d = np.abs(got - alone)
+        rel = np.linalg.norm(got - alone, axis=1) / np.linalg.norm(alone, axis=1)
+        flips = np.argmax(got, axis=1) != np.argmax(alone, axis=1)
+        say(f"batch {B} vs alone: agents 0..7 max-abs drift {d.max():.3e}, max rel-L2 {rel.max():.3e}, "
+            f"bitwise equal rows {int(np.sum(np.all(got == alone, axis=1)))} of 8, greedy changes {int(flips.sum())}")
+        assert d.max() <= 8e-2 and rel.max() <= 1e-2
+        assert not np.any(flips & (margin >= 2e-2))

@@ -210,3 +210,49 @@ def test_argmax_short_and_ragged_rows(metro, V):
     torch.cuda.synchronize()
     want = greedy_argmax(np.where(np.isnan(L), -np.inf, L))
     np.testing.assert_array_equal(out.cpu().numpy(), want)
+
+
+# One shape per kernel kind and epilogue: decode kernel with 1, 2 and 4
+# activation tiles and 2, 4 and 7 row tiles per wave, 128 x 128, 256 x 128 and
+# 256 x 256 tiles, k slices, a split last round, SwiGLU.
+REPEAT_CASES = [(7, 4096, 6144, 0, True), (25, 4096, 4096, 1, True), (25, 4096, 28672, 2, False),
+                (60, 14336, 4096, 1, True), (128, 4096, 4096, 1, True), (128, 4096, 28672, 2, False),
+                (200, 4096, 10240, 0, True), (1300, 2048, 4096, 1, True), (2600, 4096, 6144, 0, False)]
+
+
+def test_gemm_repeated_launches_are_bitwise_stable(metro):
+    """Every kernel kind gives the same bits launch after launch, also when
+    other GEMMs run in between (a result that depended on when the matrix
+    pipeline drained, or on a race between waves, would differ from launch to
+    launch), and its first result is within the fp32 bound of the exact one."""
+    rng = np.random.default_rng(77)
+    cases = []
+    for M, K, N, epi, split in REPEAT_CASES:
+        X = rand_bf16(rng, (M, K))
+        W = rand_bf16(rng, (N, K), 0.05)
+        swig = epi == 2
+        ldo = N // 2 if swig else N
+        out = (torch.zeros((M, ldo), dtype=torch.int16, device="cuda") if swig
+               else torch.zeros((M, ldo), device="cuda"))
+        ws = torch.full((8, M, N), float("nan"), device="cuda") if split else None
+        cases.append((M, K, N, epi, dev_u16(X), pack_dev(metro, W, K, K), out, ws, X, W))
+    first = [None] * len(cases)
+    for rep in range(24):
+        order = range(len(cases)) if rep % 2 == 0 else reversed(range(len(cases)))
+        for i in order:
+            M, K, N, epi, Xd, Wd, out, ws, X, W = cases[i]
+            if epi == 1:
+                out.zero_()
+            metro.op_gemm(Xd, Wd, M, N, K, epi, out, out.shape[1], workspace=ws)
+        torch.cuda.synchronize()
+        for i, c in enumerate(cases):
+            got = c[6].cpu().numpy().copy()
+            if first[i] is None:
+                first[i] = got
+                M, K, N, epi, X, W = c[0], c[1], c[2], c[3], c[8], c[9]
+                if epi != 2:
+                    ref = bf16_bits_to_f64(X) @ bf16_bits_to_f64(W).T
+                    bound = 1e-5 * (np.abs(bf16_bits_to_f64(X)) @ np.abs(bf16_bits_to_f64(W)).T) + 1e-6
+                    assert np.all(np.abs(got.astype(np.float64) - ref) <= bound), f"case {i}"
+            else:
+                np.testing.assert_array_equal(got, first[i], err_msg=f"case {c[:5]} launch {rep}")
