@@ -5,9 +5,10 @@ Workload (one step = the whole hot path over one batch): 25 agents call a
 Llama-3-8B-shaped decoder (32 layers, d 4096, 32/8 heads of 128, FFN 14336,
 vocab 128256, random N(0, 0.02) bf16 weights initialised on the device) with
 prompts of lognormal length (median 1200, sigma 0.5, clipped to [256, 4096]);
-the prompts are prefilled in 512-token chunks (all agents batched per call),
-then 64 tokens are generated greedily per agent: the first from the prefill,
-63 from batched decode steps (ready batch B = 25).  KV pages of 16 tokens.
+all prompts are prefilled in one forward (all agents batched; --chunk sets a
+smaller per-agent chunk, e.g. 512), then 64 tokens are generated greedily per
+agent: the first from the prefill, 63 from batched decode steps (ready batch
+B = 25).  KV pages of 16 tokens.
 
 Reported ``value``: decode tokens/s = 25 * 63 * steps / (GPU time of the
 decode steps), timed with HIP events on the launch stream.  ``ms_per_step``
@@ -755,6 +756,8 @@ def main():
                     help="agents (default): 25 agents, the benchmarked workload; trace: decode driven by the "
                          "seeded agent trace; prefix: prefix-heavy requests; 70b: Llama-3-70B shape at B=128; "
                          "sched: the out-of-order scheduler in closed loop with the engine vs parallel-sync")
+    ap.add_argument("--chunk", type=int, default=4096,
+                    help="agents workload: prompt tokens of one agent per prefill call (4096: whole prompts)")
     ap.add_argument("--max-calls", type=int, default=4,
                     help="sched workload: longest chain of LLM calls in one busy agent step")
     ap.add_argument("--trace-rule", choices=["radius5", "sched"], default="radius5",
@@ -787,13 +790,13 @@ def main():
     shape = synth.LLAMA3_8B
     prompts, n_new = synth.llama8b_agent_batch(args.seed, n_agents=args.agents)
     n = len(prompts)
-    chunk = 512
+    chunk = args.chunk
     lens = np.array([len(p) for p in prompts])
     log(f"workload: {n} agents, prompt tokens {lens.sum()} (min {lens.min()}, max {lens.max()}), "
         f"{n_new} generated each")
 
     t0 = time.time()
-    model = metro.Model(shape, max_batch=max(64, n), max_tokens=n * chunk, max_context=4096 + 128,
+    model = metro.Model(shape, max_batch=max(64, n), max_tokens=int(min(n * chunk, lens.sum())), max_context=4096 + 128,
                         max_seqs=2 * n, kv_pool_bytes=24 << 30, seed=args.seed)
     info = model.info()
     log(f"model ready in {time.time() - t0:.1f}s: weights {info.weight_bytes / 1e9:.2f} GB, "
@@ -851,7 +854,9 @@ def main():
            "vs_baseline": None, "dtype": "bf16",
            "data": "synthetic: seeded uniform token ids, random N(0,0.02) bf16 weights",
            "config": {"workload": "Llama-3-8B-shaped decoder, 25 agent requests, prompts lognormal(median 1200, "
-                                  "sigma 0.5) clipped to [256,4096], chunked prefill 512, 64 greedy tokens each",
+                                  "sigma 0.5) clipped to [256,4096], "
+                                  + ("all prompts prefilled in one forward" if chunk >= 4096 else
+                                     f"chunked prefill {chunk}") + ", 64 greedy tokens each",
                       "agents": n, "prompt_tokens": int(lens.sum()), "decode_steps": n_new - 1,
                       "ready_batch": n, "page_size": 16},
            "roofline": roofline,

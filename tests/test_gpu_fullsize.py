@@ -1,8 +1,8 @@
 """The HIP path against the oracle at the workloads' real sizes.
 
 Each case runs the full batch in the launch configuration of the workload
-(512-token chunked prefill with many agents per call, then decode steps over
-the whole ready batch) and compares sampled agents with the oracle, which
+(batched prefill with many agents per call, then decode steps over the whole
+ready batch) and compares sampled agents with the oracle, which
 evaluates them one by one (float64 with the bf16 storage points; the same
 function in float32 gives the noise floor of the bounds, see tests/parity.py).
 Decode steps are teacher-forced with seeded token ids on both sides, so one
@@ -11,8 +11,8 @@ free-running row instead feeds the GPU's own greedy tokens, and the oracle is
 fed the GPU's stream.
 
 - Llama-3-8B shape at full depth (32 layers): the benchmarked workload, 25
-  agents with lognormal prompts (median 1200), prefilled together in 512-token
-  chunks, decode at B = 25 for 16 steps.  Compared: five agents
+  agents with lognormal prompts (median 1200), all prefilled in one forward
+  (31527 tokens), decode at B = 25 for 16 steps.  Compared: five agents
   teacher-forced (the longest prompt, 2376 tokens, and four of 637..844
   tokens) and one free-running greedy stream (the 375-token agent).
 - 8B widths, 2 layers, a ready batch of 800 agents (the largest batch of the
@@ -175,12 +175,12 @@ def test_llama3_8b_full_depth_benchmark_batch(metro):
     say(f"8B full depth: agents {keep} ({lens[keep].tolist()} prompt tokens), drawing 16 GB of weights")
     w = synth.llama_weights(shape, 0, workers=16)
     say("8B full depth: gpu (upload, prefill of 25 agents, decode at B = 25)")
-    m = metro.Model(shape, max_batch=64, max_tokens=len(prompts) * 512, max_context=4096 + 128,
+    m = metro.Model(shape, max_batch=64, max_tokens=int(lens.sum()), max_context=4096 + 128,
                     max_seqs=2 * len(prompts), kv_pool_bytes=24 << 30)
     with m:
         m.load_weights(w)
         seqs = [m.seq_open() for _ in prompts]
-        pre = prefill_batched(m, seqs, prompts, 512, len(prompts), keep)
+        pre = prefill_batched(m, seqs, prompts, 4096, len(prompts), keep)   # all prompts in one forward
         dec = decode_free_and_fed(m, seqs, feeds, {i: pre[i][1] for i in free}, free, keep)
     # what the oracle is fed after each prompt: the fed tokens, or the GPU's own stream
     fed_in = {i: dec[i][2] for i in keep}
