@@ -279,25 +279,32 @@ __global__ __launch_bounds__(256) void reduce_parts_kernel(const float* __restri
 // kt + 1, after the barrier that every wave passes only once done reading it.
 // ---------------------------------------------------------------------------
 // Tile shapes: WN x WM waves, each TN x TM tiles of 32 x 32, NS stages of
-// 32-wide k in the LDS ring.  Big: 256 x 256 blocks for long prefill chunks.
-// Mid: 128 x 128 blocks for batches of 65 to a few hundred rows: 4 waves of
-// 64 x 64 and a ring of 5 stages (80 KiB), so that two workgroups share a CU
-// and one's barrier and LDS waits are the other's MFMA time.  Against 8 waves
-// of 32 x 64 with an 8-stage ring (128 KiB, one workgroup per CU) this took
-// 10-20% less time at M = 80..800 over the 8B and 70B projections (probes
-// with cache-cold weights; 3 stages starved the ring, 4 were 2-10% slower).
-template <int WN_, int WM_, int TN_, int TM_, int NS_>
+// KT 32-wide k tiles in the LDS ring.  Big: 256 x 256 blocks for long prefill
+// chunks.  Mid: 128 x 128 blocks for batches of 65 to a few hundred rows: 8
+// waves of 64 x 32 (two per SIMD) and a ring of 4 stages of 64-wide k (128
+// KiB).  At these sizes the k loop itself was the cost: with every global
+// load skipped the former Mid tile (4 waves of 64 x 64, 5 stages of 32-wide
+// k) still took 28 of its 62 us for the 8B gate/up at M=128, and the loads
+// added to that rather than hiding under it (ring depths 5, 8 and 9 all gave
+// the same time); stages twice as wide halve the barriers per unit of work
+// and the second wave per SIMD covers one wave's waits.  In the model: agent
+// trace 12.16k -> 12.56k tokens/s, fixed batch of 100 +5%, 70B at B=128
+// 2.55k -> 2.62k.
+// KT: 32-wide k tiles per stage (1, or 2 for 64-wide stages: half the
+// barriers per unit of work).
+template <int WN_, int WM_, int TN_, int TM_, int NS_, int KT_ = 1>
 struct TileShape {
-  static constexpr int WN = WN_, WM = WM_, TN = TN_, TM = TM_, NS = NS_;
+  static constexpr int WN = WN_, WM = WM_, TN = TN_, TM = TM_, NS = NS_, KT = KT_;
   static constexpr int WAVES = WN * WM, NTH = WAVES * 64;
   static constexpr int BN = WN * TN * 32, BM = WM * TM * 32;  // block tile
-  static constexpr int WT = BN / 16, XT = BM / 16;            // 16 x 32 tiles per stage
-  static constexpr int LPW = (WT + XT) / WAVES;               // direct loads per wave per stage
-  static_assert((WT + XT) % WAVES == 0, "the waves share the tiles of a stage evenly");
+  static constexpr int WT = BN / 16, XT = BM / 16;            // 16 x 32 tiles per k tile
+  static constexpr int LPW = KT * (WT + XT) / WAVES;          // direct loads per wave per stage
+  static_assert((KT * (WT + XT)) % WAVES == 0, "the waves share the tiles of a stage evenly");
   static_assert(NS >= 3, "the pipeline keeps a stage in use, one landed and loads in flight");
+  static_assert(KT == 1 || KT == 2 || KT == 4, "stages of 32, 64 or 128 k");
 };
 using BigTile = TileShape<4, 2, 2, 4, 5>;
-using MidTile = TileShape<2, 2, 2, 2, 5>;
+using MidTile = TileShape<2, 4, 2, 1, 4, 2>;
 // Wide: 256 rows of W x 128 activation rows, 8 waves of 64 x 64, 5 stages
 // (120 KiB), for wide products at up to 256 rows when 128 x 128 tiles would be
 // too many for one round: against 256 x 256 tiles it does no matrix work on
@@ -366,9 +373,9 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
                                                             float* __restrict__ outf, uint16_t* __restrict__ outb,
                                                             int ldo, float* __restrict__ part, int tail_first,
                                                             int tail_split, RopeKV rk) {
-  constexpr int WM = S::WM, TN = S::TN, TM = S::TM, NS = S::NS, LPW = S::LPW;
-  __shared__ uint4 wring[NS][S::WT * 64];  // per stage: WT tiles of 16 x 32 (1 KiB each)
-  __shared__ uint4 xring[NS][S::XT * 64];
+  constexpr int WM = S::WM, TN = S::TN, TM = S::TM, NS = S::NS, LPW = S::LPW, KT = S::KT;
+  __shared__ uint4 wring[NS][KT * S::WT * 64];  // per stage and k tile: WT tiles of 16 x 32 (1 KiB each)
+  __shared__ uint4 xring[NS][KT * S::XT * 64];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wn = wave / WM, wm = wave % WM;  // the wave's (TN*32) x (TM*32) tile
@@ -387,7 +394,7 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
     tile = i % gridDim.x;
   }
   const int kspan = Kp / KS, k0 = slice * kspan;
-  const int nk = kspan / 32;
+  const int nk = kspan / (32 * KT);
   int m0, n0;
   tile_origin<S>(tile, M, N, m0, n0);
 
@@ -400,20 +407,21 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
   uint32_t dst_step[LPW];  // bytes per stage of the operand's ring
 #pragma unroll
   for (int j = 0; j < LPW; ++j) {
-    const int t = wave * LPW + j;
-    if (t < S::WT) {
-      const int rt = min(n0 / 16 + t, N / 16 - 1);
-      src[j] = W + (static_cast<size_t>(rt) * (Kp / 32) + k0 / 32) * 512 + lane * 8;
+    const int t = wave * LPW + j;  // [k tile 0: W tiles .. k tile KT-1: W tiles][the same for X]
+    if (t < KT * S::WT) {
+      const int kk = t / S::WT, wt = t % S::WT;
+      const int rt = min(n0 / 16 + wt, N / 16 - 1);
+      src[j] = W + (static_cast<size_t>(rt) * (Kp / 32) + k0 / 32 + kk) * 512 + lane * 8;
       dst[j] = lds_address(&wring[0][0]) + t * 1024;
-      src_step[j] = 512;
-      dst_step[j] = S::WT * 1024;
+      src_step[j] = 512 * KT;
+      dst_step[j] = KT * S::WT * 1024;
     } else {
-      const int tx = t - S::WT;
+      const int u = t - KT * S::WT, kk = u / S::XT, tx = u % S::XT;
       const int row = min(m0 + 16 * tx + (lane & 15), M - 1);
-      src[j] = X + static_cast<size_t>(row) * ldx + k0 + 8 * (lane >> 4);
-      dst[j] = lds_address(&xring[0][0]) + tx * 1024;
-      src_step[j] = 32;
-      dst_step[j] = S::XT * 1024;
+      src[j] = X + static_cast<size_t>(row) * ldx + k0 + 32 * kk + 8 * (lane >> 4);
+      dst[j] = lds_address(&xring[0][0]) + u * 1024;
+      src_step[j] = 32 * KT;
+      dst_step[j] = KT * S::XT * 1024;
     }
   }
   auto issue = [&](int kt) __attribute__((always_inline)) {
@@ -430,11 +438,11 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // operand fragments of one 16-wide k half (ks) of stage kt
+  // operand fragments of the 16-wide k half ks (0 .. 2 KT - 1) of stage kt
   auto read_frags = [&](int kt, int ks, uint4 (&af)[TN], uint4 (&bf)[TM]) __attribute__((always_inline)) {
-    const uint4* ws = wring[kt % NS];
-    const uint4* xs = xring[kt % NS];
-    const int q = 16 * (2 * ks + lh);  // chunk of the lane's 8 k values within a tile
+    const uint4* ws = wring[kt % NS] + (ks >> 1) * S::WT * 64;
+    const uint4* xs = xring[kt % NS] + (ks >> 1) * S::XT * 64;
+    const int q = 16 * (2 * (ks & 1) + lh);  // chunk of the lane's 8 k values within a tile
 #pragma unroll
     for (int i = 0; i < TN; ++i) {
       const int row = wn * TN * 32 + i * 32 + lr;
@@ -470,12 +478,24 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
   lds_barrier();
   uint4 a0[TN], b0[TM], a1[TN], b1[TM];
   read_frags(0, 0, a0, b0);
+  // halves 0 .. 2 KT - 2 of stage kt, each multiplied while the next is read;
+  // the last one is left in a1, b1
+  auto inner_halves = [&](int kt) __attribute__((always_inline)) {
+#pragma unroll
+    for (int h = 0; h + 1 < 2 * KT; h += 2) {
+      read_frags(kt, h + 1, a1, b1);
+      mfmas(a0, b0);
+      if (h + 2 < 2 * KT) {
+        read_frags(kt, h + 2, a0, b0);
+        mfmas(a1, b1);
+      }
+    }
+  };
   // (the last step is peeled: a loop exit between the halves would merge
   // control flow there and make the compiler's LDS waits cover the reads
   // issued for the next step)
   for (int kt = 0; kt + 1 < nk; ++kt) {
-    read_frags(kt, 1, a1, b1);
-    mfmas(a0, b0);
+    inner_halves(kt);
     // stage kt + 1 has landed once only the loads of stages kt + 2 .. are
     // outstanding
     wait_later_stages<LPW, NS - 3>(nk - 2 - kt);
@@ -491,8 +511,7 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
 #pragma unroll
     for (int i = 1; i < TN; ++i) mfmas_row(i, a1, b1);
   }
-  read_frags(nk - 1, 1, a1, b1);
-  mfmas(a0, b0);
+  inner_halves(nk - 1);
   mfmas(a1, b1);
 
   // Fully unrolled (acc must stay in registers).  Slice sums are stored raw:
