@@ -133,7 +133,8 @@ const char* metro_last_error(void);
 /* Static name of a status code. */
 const char* metro_status_name(int32_t status);
 
-/* Create a model on the current HIP device.  Allocates the packed weights, the
+/* Create a model of the Llama family the paper serves (§4.1: Llama-3 8B and
+ * 70B) on the current HIP device.  Allocates the packed weights, the
  * KV page pool and scratch sized for cfg's maxima.  Every weight is filled on
  * the device from a counter-based generator keyed by init_seed: matrices with
  * N(0, 0.02) values rounded to bf16, norm gains with 1.0 (the random
@@ -160,7 +161,8 @@ metro_status metro_load_weight(metro_model* model, int32_t weight_id, int32_t la
 
 metro_status metro_model_get_info(const metro_model* model, metro_model_info* info);
 
-/* Open an empty sequence (one agent request / conversation).  With the
+/* Open an empty sequence: the context of one agent's LLM request (§3.1: a
+ * worker issues the requests of the agents of a ready cluster).  With the
  * prefix cache on, the pages its prefills fill are entered in the cache.
  * Errors: E_CAPACITY (max_seqs open). */
 metro_status metro_seq_open(metro_model* model, int64_t* seq);
@@ -213,7 +215,8 @@ metro_status metro_seq_open_cached(metro_model* model, const int32_t* tokens, in
 /* Open a new sequence whose first n_tokens positions are those of src
  * (0 < n_tokens <= length of src).  Whole pages are shared by reference (never
  * written again by either sequence); a partly filled last page is copied on
- * `stream`.  This is the by-reference sharing of a common prompt prefix.
+ * `stream`.  This is the by-reference sharing of a common prompt prefix
+ * (§4.1, prefix caching).
  * The new sequence enters no pages in the prefix cache.
  * Errors: E_SEQ, E_INVAL, E_CAPACITY, E_NOPAGES, E_HIP. */
 metro_status metro_seq_fork(metro_model* model, int64_t src, int32_t n_tokens, void* stream,
@@ -231,7 +234,9 @@ metro_status metro_seq_pages(const metro_model* model, int64_t seq, int32_t* pag
                              int32_t* n_pages);
 
 /* Chunked prefill: append a chunk of prompt tokens to each of n_items
- * sequences and run the forward pass over all of them in one batch.
+ * sequences and run the forward pass over all of them in one batch (the
+ * prompts of a ready cluster's requests served together, §3.1 and
+ * Algorithm 3; more ready agents make larger batches, §3.2).
  *   seqs      host [n_items] distinct open sequences
  *   cu_tokens host [n_items+1] prefix sums: item i owns tokens[cu[i] .. cu[i+1])
  *             (cu[0] == 0, each item >= 1 token, cu[n_items] <= max_tokens)
@@ -248,7 +253,9 @@ metro_status metro_prefill_chunk(metro_model* model, int32_t n_items, const int6
                                  int32_t* next_tok, void* stream);
 
 /* One decode step: append one token to each of `batch` sequences and return
- * the next-token distribution of each.
+ * the next-token distribution of each (one token for every ready agent's
+ * running request, §3.2; generation runs a fixed number of steps with no
+ * end-of-sequence stop, as in the replay of §4.1).
  *   seqs       host [batch] distinct open sequences, each of length >= 1
  *   tokens_dev device int32 [batch] token ids (e.g. the previous step's
  *              next_tok); an id outside [0, vocab) turns that row's outputs

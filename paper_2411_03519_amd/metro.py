@@ -249,8 +249,18 @@ class Model:
                                       _ptr(logits), _ptr(next_tok), _stream(stream)))
 
     def decode_step(self, seqs, tokens_dev, logits=None, next_tok=None, stream=None) -> None:
-        """One token per sequence: ``tokens_dev`` is a device int32 [batch]."""
+        """One token per sequence: ``tokens_dev`` is a device int32 [batch]
+        (e.g. the previous step's ``next_tok``).  Host tokens (a list, numpy
+        array or CPU tensor) are copied to the device first, on the call's
+        stream; the library itself reads device memory only."""
         s = _host_i64(seqs)
+        import torch
+        if not (isinstance(tokens_dev, torch.Tensor) and tokens_dev.is_cuda):
+            host = torch.as_tensor(np.ascontiguousarray(np.asarray(tokens_dev, dtype=np.int32)))
+            st = (torch.cuda.current_stream() if stream is None
+                  else torch.cuda.ExternalStream(stream) if isinstance(stream, int) else stream)
+            with torch.cuda.stream(st):
+                tokens_dev = host.to("cuda")
         check(lib.metro_decode_step(self._h, len(s), s.ctypes.data, _ptr(tokens_dev), _ptr(logits), _ptr(next_tok),
                                     _stream(stream)))
 

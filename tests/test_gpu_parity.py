@@ -124,6 +124,32 @@ def test_tiny_free_running_greedy_streams(metro, tiny_case):
         check_tokens(streams[i], tf)
 
 
+def test_decode_step_with_host_tokens_matches_device_tokens(metro, tiny_case):
+    """The binding copies host tokens (list, numpy, CPU tensor) to the device;
+    the library then runs exactly the device-token step."""
+    prompts, n_new, cases = tiny_case
+    w, gens = cases["ones"]
+    feeds = [g[0][:3] for g in gens]
+    outs = []
+    for kind in ("device", "list", "numpy", "cpu_tensor"):
+        with make_model(metro, synth.TINY, w) as m:
+            seqs = [m.seq_open() for _ in prompts]
+            lg = torch.empty(len(prompts), m.vocab, device="cuda")
+            nt = torch.empty(len(prompts), dtype=torch.int32, device="cuda")
+            m.prefill_chunk(seqs, prompts, lg, nt)
+            rows = []
+            for k in range(3):
+                host = [int(f[k]) for f in feeds]
+                feed = {"device": torch.tensor(host, dtype=torch.int32, device="cuda"), "list": host,
+                        "numpy": np.array(host, np.int64), "cpu_tensor": torch.tensor(host)}[kind]
+                m.decode_step(seqs, feed, lg, nt)
+                rows.append((lg.cpu().numpy().copy(), nt.cpu().numpy().copy()))
+        outs.append(rows)
+    for kind, rows in zip(("list", "numpy", "cpu_tensor"), outs[1:]):
+        for (a, ta), (b, tb) in zip(outs[0], rows):
+            assert np.array_equal(a.view(np.uint32), b.view(np.uint32)) and np.array_equal(ta, tb), kind
+
+
 @pytest.mark.parametrize("chunk", [16, 23, 64])
 def test_tiny_chunked_prefill(metro, tiny_case, chunk):
     prompts, n_new, cases = tiny_case
