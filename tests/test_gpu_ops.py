@@ -95,7 +95,11 @@ GEMM_CASES = [(1, 256, 64), (7, 640, 96), (16, 256, 32), (25, 4096, 512), (33, 7
               (129, 256, 20480),     # wide: 160 tiles of 256 x 128 over two row blocks
               (100, 256, 69632),     # wide: 272 tiles of 256 x 128, the 16 past the first round in 2 k slices
               (200, 256, 16384),     # wide: 128 tiles of 256 x 128, with a workspace 2 k slices each
-              (90, 128, 57344)]      # wide: 224 tiles of 256 x 128 (70B gate/up-sized, one round)
+              (90, 128, 57344),      # wide: 224 tiles of 256 x 128 (70B gate/up-sized, one round)
+              (128, 4096, 6144),     # 48 tiles of 128 x 128 x 4 k slices (8B QKV-sized)
+              (256, 4096, 4096),     # 64 tiles of 128 x 128 x 4 k slices
+              (129, 2048, 1056),     # ragged N: 18 tiles of 128 x 128, the last 32 rows of W past a 128 block
+              (250, 512, 288)]       # ragged in M and N, 128 x 128 tiles
 
 
 @pytest.mark.parametrize("M,K,N", GEMM_CASES + [(25, 14336, 512), (3, 1024, 4096)])
