@@ -21,7 +21,10 @@ GEMM with the SwiGLU epilogue), whose launches are timed with HIP events
 inside the library during the timed region, with its HBM traffic from the
 committed counter summary; ``roofline_prefill_kernel`` the same GEMM during
 the first warm-up step's prefill.  ``cpu_baseline`` times the CPU oracle on a
-bounded sample.
+bounded sample.  ``other_workloads`` (skipped with --no-others) holds short
+runs of two more configurations in the same process, after the timed region:
+the agent-trace decode (1000 agents, 200 ticks, plus the fixed-batch sweep)
+and one 70B step at B = 128, each with its own whole-step HBM roofline.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1]
 """
@@ -763,6 +766,8 @@ def main():
     ap.add_argument("--trace-rule", choices=["radius5", "sched"], default="radius5",
                     help="trace workload: ready batches from the constant Chebyshev-5 readiness rule (default) or "
                          "from the library's out-of-order scheduler with the rules of §3.3")
+    ap.add_argument("--no-others", action="store_true",
+                    help="agents workload: skip the short agent-trace and 70B runs reported under other_workloads")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device copy three times (counter calibration) and exit")
     args = ap.parse_args()
@@ -885,9 +890,34 @@ def main():
                                           "kernel": "gemm gate/up + SwiGLU (prefill chunks; a split last round "
                                                     "includes its fixup kernel)", "launches": pf_launches}
     model.close()
+    if not args.no_others:
+        out["other_workloads"] = other_workloads(args, torch, metro, synth)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.seed)
     print(json.dumps(out), flush=True)
+
+
+def other_workloads(args, torch, metro, synth):
+    """The agent-trace decode and one 70B step, after the c1 timed region, so
+    that one default run records them too.  A failure in either is reported
+    in its entry and does not touch the c1 figures."""
+    keep = ("value", "unit", "ms_per_step", "roofline", "fixed_batch", "prefill_tokens_per_s", "prefill_mfma_frac")
+    res = {}
+    for name, fn, over in (("trace", bench_trace, {"trace_rule": "radius5"}),
+                           ("70b", bench_70b, {"steps": 1, "warmup": 1})):
+        sub = argparse.Namespace(**{**vars(args), **over})
+        t0 = time.time()
+        try:
+            r = fn(sub, torch, metro, synth)
+            res[name] = {k: r[k] for k in keep if k in r}
+            res[name]["workload"] = r["config"]["workload"]
+        except Exception as e:  # reported, not raised: the c1 line stands on its own
+            res[name] = {"error": f"{type(e).__name__}: {e}"}
+        res[name]["wall_s"] = round(time.time() - t0, 1)
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        log(f"other workload {name}: {res[name].get('value', res[name].get('error'))}")
+    return res
 
 
 if __name__ == "__main__":
