@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define METRO_ABI_VERSION 1
+#define METRO_ABI_VERSION 2
 
 typedef enum metro_status {
   METRO_OK = 0,

@@ -105,10 +105,14 @@ metro_status metro_sched_state(const metro_sched* s, int32_t* steps, int32_t* xy
  * With model == NULL the engine only plans: metro_engine_step forms the items
  * as above and appends stand-in tokens without device work (for checking the
  * admission rules on a host without a GPU).
+ * When the KV pool cannot hold the pages of a forward (the model's call
+ * returns METRO_E_NOPAGES and changes nothing), the step is planned again with
+ * half the prompt tokens, down to a decode-only forward; only when no forward
+ * fits does metro_engine_step return METRO_E_NOPAGES (no request's state
+ * changes; retry once requests have retired or others are closed).
  * Errors: METRO_E_INVAL (NULL, bad sizes, a live request id), METRO_E_SEQ
- * (unknown request), METRO_E_NOMEM, and whatever the model calls return
- * (e.g. METRO_E_NOPAGES: no request's state changes, the step may be retried
- * after others retire). */
+ * (unknown request), METRO_E_NOMEM, METRO_E_NOPAGES as above, and whatever
+ * else the model calls return. */
 typedef struct metro_engine metro_engine;
 
 typedef struct {
@@ -125,6 +129,7 @@ typedef struct {
   int64_t decode_tokens; /* one-token decode items */
   int32_t live;          /* requests not yet finished */
   int32_t waiting;       /* of which not yet through their prompt */
+  int64_t page_retries;  /* forwards planned again with fewer prompt tokens for lack of KV pages */
 } metro_engine_stats;
 
 /* Create an engine on a model (or NULL: planning only); the model must

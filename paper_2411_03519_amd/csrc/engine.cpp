@@ -75,8 +75,9 @@ struct metro_engine {
     return a->arrival < b->arrival;
   }
 
-  // The items of the next forward: (request, tokens, is a decode token).
-  void plan() {
+  // The items of the next forward: (request, tokens, is a decode token), with
+  // at most prompt_cap prompt tokens.
+  void plan(int32_t prompt_cap) {
     plan_id.clear();
     plan_tokens.clear();
     plan_decode.clear();
@@ -95,7 +96,7 @@ struct metro_engine {
       plan_tokens.push_back(1);
       plan_decode.push_back(1);
     }
-    int32_t budget = cfg.max_tokens - static_cast<int32_t>(plan_id.size());
+    int32_t budget = std::min(cfg.max_tokens - static_cast<int32_t>(plan_id.size()), prompt_cap);
     for (Request* r : wait) {
       if (static_cast<int32_t>(plan_id.size()) >= cfg.max_items || budget <= 0) break;
       const int32_t take = std::min({cfg.chunk, static_cast<int32_t>(r->prompt.size()) - r->off, budget});
@@ -104,6 +105,45 @@ struct metro_engine {
       plan_decode.push_back(0);
       budget -= take;
     }
+  }
+
+  // Run the planned forward and leave each item's greedy token in next
+  // (planning only: a stand-in token per item).  Returns the model's status;
+  // on failure no request's state has changed.
+  metro_status forward(void* stream, std::vector<int32_t>& next) {
+    const int32_t n = static_cast<int32_t>(plan_id.size());
+    if (!model) {
+      for (int32_t i = 0; i < n; ++i) next[i] = static_cast<int32_t>((plan_id[i] * 31 + stats.forwards) % 1000);
+      return METRO_OK;
+    }
+    bool any_prompt = false;
+    for (int32_t d : plan_decode) any_prompt |= d == 0;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    std::vector<int64_t> seqs(n);
+    for (int32_t i = 0; i < n; ++i) seqs[i] = reqs[plan_id[i]].seq;
+    metro_status st;
+    if (any_prompt) {
+      std::vector<int32_t> cu(n + 1, 0), toks;
+      for (int32_t i = 0; i < n; ++i) {
+        const Request& r = reqs[plan_id[i]];
+        if (plan_decode[i]) toks.push_back(r.out.back());
+        else toks.insert(toks.end(), r.prompt.begin() + r.off, r.prompt.begin() + r.off + plan_tokens[i]);
+        cu[i + 1] = static_cast<int32_t>(toks.size());
+      }
+      st = metro_prefill_chunk(model, n, seqs.data(), cu.data(), toks.data(), nullptr, next_dev, stream);
+    } else {
+      for (int32_t i = 0; i < n; ++i) pinned[i] = reqs[plan_id[i]].out.back();
+      if (hipMemcpyAsync(tok_dev, pinned, n * 4, hipMemcpyHostToDevice, s) != hipSuccess)
+        return metro::report(METRO_E_HIP, "engine: token upload failed");
+      st = metro_decode_step(model, n, seqs.data(), tok_dev, nullptr, next_dev, stream);
+    }
+    if (st != METRO_OK) return st;
+    int32_t* back = pinned + cfg.max_items;
+    if (hipMemcpyAsync(back, next_dev, n * 4, hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+      return metro::report(METRO_E_HIP, "engine: token download failed");
+    std::memcpy(next.data(), back, n * 4);
+    return METRO_OK;
   }
 };
 
@@ -174,6 +214,7 @@ metro_status metro_engine_submit(metro_engine* e, int64_t request, int32_t step,
   try {
     e->reqs.emplace(request, std::move(r));
   } catch (const std::bad_alloc&) {
+    if (e->model && r.seq >= 0) (void)metro_seq_close(e->model, r.seq);  // (the id survives the failed move)
     return report(METRO_E_NOMEM, "engine submit: out of host memory");
   }
   return METRO_OK;
@@ -183,41 +224,34 @@ metro_status metro_engine_step(metro_engine* e, void* stream, int32_t* n_items) 
   metro::clear_error();
   metro_status st = check_engine(e);
   if (st != METRO_OK) return st;
-  e->plan();
-  const int32_t n = static_cast<int32_t>(e->plan_id.size());
-  if (n_items) *n_items = n;
-  if (n == 0) return METRO_OK;
-  bool any_prompt = false;
-  for (int32_t d : e->plan_decode) any_prompt |= d == 0;
-  std::vector<int32_t> next(n, 0);
-  if (e->model) {
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    std::vector<int64_t> seqs(n);
-    for (int32_t i = 0; i < n; ++i) seqs[i] = e->reqs[e->plan_id[i]].seq;
-    if (any_prompt) {
-      std::vector<int32_t> cu(n + 1, 0), toks;
-      for (int32_t i = 0; i < n; ++i) {
-        const Request& r = e->reqs[e->plan_id[i]];
-        if (e->plan_decode[i]) toks.push_back(r.out.back());
-        else toks.insert(toks.end(), r.prompt.begin() + r.off, r.prompt.begin() + r.off + e->plan_tokens[i]);
-        cu[i + 1] = static_cast<int32_t>(toks.size());
-      }
-      st = metro_prefill_chunk(e->model, n, seqs.data(), cu.data(), toks.data(), nullptr, e->next_dev, stream);
-    } else {
-      for (int32_t i = 0; i < n; ++i) e->pinned[i] = e->reqs[e->plan_id[i]].out.back();
-      if (hipMemcpyAsync(e->tok_dev, e->pinned, n * 4, hipMemcpyHostToDevice, s) != hipSuccess)
-        return report(METRO_E_HIP, "engine: token upload failed");
-      st = metro_decode_step(e->model, n, seqs.data(), e->tok_dev, nullptr, e->next_dev, stream);
+  // When the model runs short of KV pages for the forward, the same step is
+  // planned again with half the prompt tokens (the model's calls change no
+  // state when they fail that way), down to a decode-only forward.
+  int32_t prompt_cap = e->cfg.max_tokens;
+  int32_t n = 0;
+  std::vector<int32_t> next;
+  for (;;) {
+    e->plan(prompt_cap);
+    n = static_cast<int32_t>(e->plan_id.size());
+    if (n_items) *n_items = n;
+    int32_t prompt_tokens = 0;
+    for (int32_t i = 0; i < n; ++i)
+      if (!e->plan_decode[i]) prompt_tokens += e->plan_tokens[i];
+    if (n == 0) {
+      if (prompt_cap < e->cfg.max_tokens)
+        return report(METRO_E_NOPAGES, "engine: too few free KV pages for any forward (%d requests live)",
+                      static_cast<int>(e->reqs.size()));
+      return METRO_OK;
+    }
+    next.assign(n, 0);
+    st = e->forward(stream, next);
+    if (st == METRO_E_NOPAGES && prompt_tokens > 0) {
+      prompt_cap = prompt_tokens / 2;
+      e->stats.page_retries += 1;
+      continue;
     }
     if (st != METRO_OK) return st;
-    int32_t* back = e->pinned + e->cfg.max_items;
-    if (hipMemcpyAsync(back, e->next_dev, n * 4, hipMemcpyDeviceToHost, s) != hipSuccess ||
-        hipStreamSynchronize(s) != hipSuccess)
-      return report(METRO_E_HIP, "engine: token download failed");
-    std::memcpy(next.data(), back, n * 4);
-  } else {
-    // planning only: a stand-in token per item
-    for (int32_t i = 0; i < n; ++i) next[i] = static_cast<int32_t>((e->plan_id[i] * 31 + e->stats.forwards) % 1000);
+    break;
   }
   e->stats.forwards += 1;
   e->stats.items += n;

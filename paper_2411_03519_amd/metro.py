@@ -18,7 +18,7 @@ if not os.path.exists(_LIB_PATH):
     raise ImportError(f"{_LIB_PATH} is not built; run `python -m paper_2411_03519_amd.build`")
 lib = ctypes.CDLL(_LIB_PATH)
 
-ABI_VERSION = 1
+ABI_VERSION = 2
 
 STATUS = {0: "METRO_OK", -1: "METRO_E_INVAL", -2: "METRO_E_NOMEM", -3: "METRO_E_NOPAGES", -4: "METRO_E_SEQ",
           -5: "METRO_E_CAPACITY", -6: "METRO_E_HIP"}
@@ -410,7 +410,8 @@ class EngineConfig(ctypes.Structure):
 
 class EngineStats(ctypes.Structure):
     _fields_ = [("forwards", ctypes.c_int64), ("items", ctypes.c_int64), ("prompt_tokens", ctypes.c_int64),
-                ("decode_tokens", ctypes.c_int64), ("live", ctypes.c_int32), ("waiting", ctypes.c_int32)]
+                ("decode_tokens", ctypes.c_int64), ("live", ctypes.c_int32), ("waiting", ctypes.c_int32),
+                ("page_retries", ctypes.c_int64)]
 
 
 class Engine:

@@ -36,7 +36,7 @@ def test_binding_reports_abi_and_errors_without_gpu(repo_root):
     if not os.path.exists(path):
         pytest.skip("libmetro.so not built")
     from paper_2411_03519_amd import metro
-    assert metro.lib.metro_abi_version() == 1
+    assert metro.lib.metro_abi_version() == metro.ABI_VERSION == 2
     assert metro.lib.metro_status_name(-3) == b"METRO_E_NOPAGES"
     # configuration errors are found before any HIP call
     bad = metro.Config(n_layers=2, d_model=200, n_heads=4, n_kv_heads=2, head_dim=64, ffn_dim=688, vocab=4096,

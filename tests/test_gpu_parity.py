@@ -531,6 +531,56 @@ def test_sync_check_mode_gives_the_same_results(metro, monkeypatch):
     np.testing.assert_array_equal(outs[0][1], outs[1][1])
 
 
+def test_engine_under_page_pressure_plans_again_and_matches_oracle(metro):
+    """A forward whose pages the pool cannot hold fails in the model without
+    changing anything; the engine then plans the step again with half the
+    prompt tokens.  A stand-in sequence holds most of the pool until the
+    engine has had to do so at least once (or until no forward fits at all,
+    which the engine reports as E_NOPAGES), then releases it; every request
+    must still finish with the oracle's greedy stream."""
+    w = synth.llama_weights(synth.TINY, 12, norm="random")
+    ref = OracleModel(LlamaShape(**synth.TINY), w)
+    rng = np.random.default_rng(32)
+    reqs = [(i, int(rng.integers(0, 4)), rng.integers(0, synth.TINY["vocab"], int(n)), int(k))
+            for i, (n, k) in enumerate([(70, 6), (5, 9), (130, 3), (33, 7), (64, 5), (1, 4)])]
+    page_bytes = 16 * 2 * synth.TINY["n_layers"] * synth.TINY["n_kv_heads"] * synth.TINY["head_dim"] * 2
+    with make_model(metro, synth.TINY, w, max_batch=8, max_tokens=128, max_context=512,
+                    kv_pool_bytes=32 * page_bytes) as m:
+        hold = m.seq_open()
+        filler = rng.integers(0, synth.TINY["vocab"], 24 * 16)
+        for c in range(0, len(filler), 128):
+            m.prefill_chunk([hold], [filler[c:c + 128]])
+        torch.cuda.synchronize()
+        eng = metro.Engine(m, max_tokens=96, chunk=32, max_items=8, priority=True)
+        for rid, step, prompt, n_out in reqs:
+            eng.submit(rid, step, prompt, n_out)
+        released = nopages = 0
+        for _ in range(500):
+            try:
+                n = eng.step()
+            except metro.MetroError as e:
+                assert e.name == "METRO_E_NOPAGES" and hold is not None, e
+                nopages += 1
+                n = -1
+            if hold is not None and (eng.stats()["page_retries"] > 0 or n == -1):
+                m.seq_close(hold)
+                hold, released = None, 1
+            if n == 0:
+                break
+        st = eng.stats()
+        assert sorted(eng.finished()) == [r[0] for r in reqs]
+        streams = {rid: eng.result(rid) for rid, *_ in reqs}
+        eng.close()
+    print(f"engine under page pressure: {st['page_retries']} forwards planned again, {nopages} steps with no "
+          f"forward that fit, {st['forwards']} forwards", flush=True)
+    assert released and st["page_retries"] > 0
+    assert st["prompt_tokens"] == sum(len(r[2]) for r in reqs)
+    for rid, step, prompt, n_out in reqs:
+        s = streams[rid]
+        assert len(s) == n_out
+        check_tokens(s, ref.teacher_forced(prompt, s[:-1]), f"engine request {rid} (page pressure)")
+
+
 @pytest.mark.parametrize("priority", [True, False])
 def test_engine_mixed_batches_match_oracle(metro, priority):
     """The library's mixed continuous batching (metro_engine_*): requests with
