@@ -142,27 +142,42 @@ KERNEL_SOURCES = ["paper_2411_03519_amd/csrc/kernels/gemm.hip", "paper_2411_0351
 
 
 def kernel_source_hash() -> str:
+    return source_hash(KERNEL_SOURCES)
+
+
+# The whole decode step's HBM traffic (the same counters summed over every
+# kernel of the 63 decode steps of one c1 step) depends on every kernel and on
+# the launch sequence.
+STEP_TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_step_8b_b25_traffic.txt")
+STEP_SOURCES = KERNEL_SOURCES + ["paper_2411_03519_amd/csrc/kernels/attention.hip",
+                                 "paper_2411_03519_amd/csrc/kernels/elementwise.hip",
+                                 "paper_2411_03519_amd/csrc/kernels/kernels.h",
+                                 "paper_2411_03519_amd/csrc/runtime.hip"]
+
+
+def source_hash(sources=None) -> str:
     import hashlib
     h = hashlib.sha256()
-    for rel in KERNEL_SOURCES:
+    for rel in sources or KERNEL_SOURCES:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
 
 
-def measured_traffic():
-    """HBM bytes per launch of the decode gate/up GEMM from the profile summary,
-    or None if there is none or the kernel sources changed since."""
+def measured_traffic(summary=None, sources=None, key="traffic_bytes_per_launch"):
+    """HBM bytes from a committed profile summary (default: per launch of the
+    decode gate/up GEMM), or None if there is none or its sources changed
+    since the counters were taken."""
     try:
-        with open(TRAFFIC_SUMMARY) as f:
+        with open(summary or TRAFFIC_SUMMARY) as f:
             kv = dict(line.split(":", 1) for line in f if ":" in line and not line.startswith(" "))
     except OSError:
         return None
     kv = {k.strip(): v.strip() for k, v in kv.items()}
-    if kv.get("source_sha256") != kernel_source_hash():
+    if kv.get("source_sha256") != source_hash(sources):
         return None
     try:
-        return int(float(kv["traffic_bytes_per_launch"]))
+        return int(float(kv[key]))
     except (KeyError, ValueError):
         return None
 
@@ -841,6 +856,7 @@ def main():
     roofline = hbm_roofline(step_bytes * args.steps, decode_ms / 1e3,
                             "whole decode step (weights + KV read and write + fp32 logits)")
     roofline["bytes_per_step"] = int(step_bytes // (n_new - 1))
+    roofline["traffic"] = measured_traffic(STEP_TRAFFIC_SUMMARY, STEP_SOURCES, "traffic_bytes_per_step")
     items = sum(-(-int(L) // chunk) for L in lens)      # LM-head rows: one per item of every prefill call
     pf_all_flops = prefill_flops(shape, [np.arange(L) for L in lens], items)
     pf_all_tflops = pf_all_flops * args.steps / (prefill_ms / 1e3) / 1e12
