@@ -486,10 +486,13 @@ def bench_sched(args, torch, metro, synth):
     library's mixed continuous batching, against the parallel-sync baseline
     (Algorithm 1) on the same seeded world and calls (100 x 140 grid, radius_p
     4, max_vel 1, chains of up to 4 calls per busy agent step), with step
-    priority on and off: 25 agents for 12 steps (the paper's village size),
-    200 agents for 3 steps and 500 agents for 2."""
+    priority on and off: by default 25 agents for 12 steps (the paper's
+    village size), 200 agents for 3 steps and 500 agents for 2 (--sched-cases;
+    --sched-priority on skips the runs without priority).  ``value`` is the
+    second case (or the only one), out of order, with priority."""
     shape = synth.LLAMA3_8B
-    cases = [(25, 12), (200, 3), (500, 2)]
+    cases = [tuple(int(v) for v in c.split("x")) for c in args.sched_cases.split(",")]
+    priorities = (True, False) if args.sched_priority == "both" else (True,)
     max_items = 256
     pages = 640 * ((2048 + 64 + 15) // 16 + 1) + 64
     model = metro.Model(shape, max_batch=max_items, max_tokens=8192 + max_items, max_context=2048 + 64 + 16,
@@ -501,7 +504,7 @@ def bench_sched(args, torch, metro, synth):
     for n_agents, steps in cases:
         world = synth.SimWorld(args.seed, n_agents, grid=(100, 140))
         res = {}
-        for priority in (True, False):
+        for priority in priorities:
             pol = "priority" if priority else "no_priority"
             for mode in ("parallel_sync", "out_of_order"):
                 sched = metro.Scheduler(world.start, 4.0, 1.0, metro.DIST_CHEBYSHEV, steps,
@@ -518,7 +521,8 @@ def bench_sched(args, torch, metro, synth):
                 res[f"parallel_sync/{pol}"]["seconds"] / res[f"out_of_order/{pol}"]["seconds"], 3)
         out[f"{n_agents}x{steps}"] = res
     model.close()
-    head = out["200x3"]["out_of_order/priority"]
+    head_case = "%dx%d" % cases[1 if len(cases) > 1 else 0]
+    head = out[head_case]["out_of_order/priority"]
     flops = 2.0 * shape["n_layers"] * layer_params(shape) * (head["prompt_tokens"] + head["decode_tokens"])
     roof = {"bound": "mfma", "achieved": round(flops / head["seconds"] / 1e12, 1), "peak": BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s", "frac": round(flops / head["seconds"] / 1e12 / BF16_PEAK_TFLOPS, 4), "traffic": None,
@@ -532,9 +536,9 @@ def bench_sched(args, torch, metro, synth):
                                    f"{args.max_calls} LLM calls per busy agent step (prompts lognormal median 640, outputs median "
                                    "18), radius_p 4, max_vel 1, Chebyshev distance; library mixed continuous "
                                    "batching (8192-token forwards, 512-token chunks) with step priority on/off; "
-                                   "value: 200 agents x 3 steps, out of order, priority",
+                                   f"value: {head_case.replace('x', ' agents x ')} steps, out of order, priority",
                        "cases": [f"{n}x{s}" for n, s in cases]},
-            "speedup_vs_parallel_sync": out["200x3"]["speedup_vs_parallel_sync/priority"],
+            "speedup_vs_parallel_sync": out[head_case]["speedup_vs_parallel_sync/priority"],
             "cases": out, "roofline": roof}
 
 
@@ -778,6 +782,10 @@ def main():
                     help="agents workload: prompt tokens of one agent per prefill call (4096: whole prompts)")
     ap.add_argument("--max-calls", type=int, default=4,
                     help="sched workload: longest chain of LLM calls in one busy agent step")
+    ap.add_argument("--sched-cases", default="25x12,200x3,500x2",
+                    help="sched workload: agents x steps of each closed-loop run, comma separated")
+    ap.add_argument("--sched-priority", choices=["both", "on"], default="both",
+                    help="sched workload: run with step priority on and off, or on only")
     ap.add_argument("--trace-rule", choices=["radius5", "sched"], default="radius5",
                     help="trace workload: ready batches from the constant Chebyshev-5 readiness rule (default) or "
                          "from the library's out-of-order scheduler with the rules of §3.3")
