@@ -51,9 +51,10 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def run_step(model, prompts, n_new, chunk, torch):
+def run_step(model, prompts, n_new, chunk, torch, step_events=None):
     """Prefill all prompts (chunked, batched), then n_new - 1 decode steps.
-    Returns the three HIP events (start, prefill done, decode done)."""
+    Returns the three HIP events (start, prefill done, decode done); with a
+    list ``step_events``, also appends an event after every decode step."""
     n = len(prompts)
     V = model.vocab
     seqs = [model.seq_open() for _ in range(n)]
@@ -79,6 +80,9 @@ def run_step(model, prompts, n_new, chunk, torch):
     for _ in range(n_new - 1):
         model.decode_step(seqs, tok, logits, tok2)
         tok, tok2 = tok2, tok
+        if step_events is not None:
+            step_events.append(torch.cuda.Event(enable_timing=True))
+            step_events[-1].record()
     ev[2].record()
     for s in seqs:
         model.seq_close(s)
@@ -383,7 +387,11 @@ def bench_trace(args, torch, metro, synth):
                        "ticks": len(batches), "decode_tokens": tokens, "batch_min": int(sizes.min()),
                        "batch_median": float(np.median(sizes)), "batch_max": int(sizes.max()),
                        "context_tokens": int(lens.sum())},
-            "roofline": roof, "fixed_batch": fixed}
+            "roofline": roof, "fixed_batch": fixed,
+            "batch_histogram": {f"{lo}-{hi - 1}": int(np.sum((sizes >= lo) & (sizes < hi)))
+                                for lo, hi in ((1, 64), (64, 128), (128, 256), (256, 512), (512, 1024))},
+            "tick_ms": {"p50": round(float(np.percentile(ms, 50)), 3), "p90": round(float(np.percentile(ms, 90)), 3),
+                        "max": round(float(np.max(ms)), 3)}}
 
 
 def sched_chain(world, seed, step, agent, vocab, max_calls):
@@ -831,13 +839,17 @@ def main():
         f"KV pool {info.kv_pool_bytes / 1e9:.1f} GB ({info.n_pages} pages)")
 
     # warmup (untimed); the first one also measures the prefill gate/up GEMM
+    dstep_ms = None  # decode step times of the first warm-up step (events between steps)
     for w in range(args.warmup):
         if w == 0:
             model.profile_start("gemm_gate_up", "prefill")
-        ev = run_step(model, prompts, n_new, chunk, torch)
+        marks = [] if w == 0 else None
+        ev = run_step(model, prompts, n_new, chunk, torch, marks)
         torch.cuda.synchronize()
         if w == 0:
             pf_ms, pf_launches = model.profile_stop()
+            dstep_ms = np.array([ev[1].elapsed_time(marks[0])] +
+                               [a.elapsed_time(b) for a, b in zip(marks[:-1], marks[1:])])
         log(f"warmup {w}: prefill {ev[0].elapsed_time(ev[1]):.1f} ms, decode {ev[1].elapsed_time(ev[2]):.1f} ms")
 
     # timed region
@@ -903,6 +915,10 @@ def main():
                                  "on the same inputs and greedy choices may differ at fp32-undecidable steps "
                                  "(tests/parity.py)"},
            "decode_ms_per_step": round(decode_ms / args.steps, 2),
+           "decode_step_ms": None if dstep_ms is None else {
+               "p50": round(float(np.percentile(dstep_ms, 50)), 3), "p90": round(float(np.percentile(dstep_ms, 90)), 3),
+               "max": round(float(dstep_ms.max()), 3), "n": int(dstep_ms.size),
+               "note": "the 63 decode steps of the first warm-up step, timed between events"},
            "prefill_ms_per_step": round(prefill_ms / args.steps, 2),
            "prefill_tokens_per_s": round(prefill_tps, 1)}
     if args.warmup > 0 and pf_launches:
@@ -925,7 +941,8 @@ def other_workloads(args, torch, metro, synth):
     """The agent-trace decode and one 70B step, after the c1 timed region, so
     that one default run records them too.  A failure in either is reported
     in its entry and does not touch the c1 figures."""
-    keep = ("value", "unit", "ms_per_step", "roofline", "fixed_batch", "prefill_tokens_per_s", "prefill_mfma_frac")
+    keep = ("value", "unit", "ms_per_step", "roofline", "fixed_batch", "batch_histogram", "tick_ms",
+            "prefill_tokens_per_s", "prefill_mfma_frac")
     res = {}
     for name, fn, over in (("trace", bench_trace, {"trace_rule": "radius5"}),
                            ("70b", bench_70b, {"steps": 1, "warmup": 1})):
