@@ -57,7 +57,8 @@ def metro():
 
 
 def say(*a):
-    print(*a, flush=True)
+    from tests.conftest import progress  # shown under -q too: the oracle runs for minutes
+    progress(*a)
 
 
 def oracle_rows(shape, weights, prompt, feed, dtype):
