@@ -81,12 +81,13 @@ __device__ __forceinline__ void store_rope_kv(f32x4 a, f32x4 b, int m, int head,
       *reinterpret_cast<uint2*>(dst + d0) = make_uint2(pack_bf16x2(ra[0], ra[1]), pack_bf16x2(ra[2], ra[3]));
       *reinterpret_cast<uint2*>(dst + d0 + half) = make_uint2(pack_bf16x2(rb[0], rb[1]), pack_bf16x2(rb[2], rb[3]));
     } else {
+      // dims d0 .. d0+3 (d0 % 4 == 0) are 4 consecutive elements of the K
+      // tile: one 8-byte store each for the two halves
       uint16_t* kt = rk.kv + kv_offset(page, 0, rk.nkv, head - rk.nq, 0, hd, 0);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        kt[k_tile_offset(off, d0 + i)] = f32_to_bf16(ra[i]);
-        kt[k_tile_offset(off, d0 + i + half)] = f32_to_bf16(rb[i]);
-      }
+      *reinterpret_cast<uint2*>(kt + k_tile_offset(off, d0)) =
+          make_uint2(pack_bf16x2(ra[0], ra[1]), pack_bf16x2(ra[2], ra[3]));
+      *reinterpret_cast<uint2*>(kt + k_tile_offset(off, d0 + half)) =
+          make_uint2(pack_bf16x2(rb[0], rb[1]), pack_bf16x2(rb[2], rb[3]));
     }
   } else {
     uint16_t* vt = rk.kv + kv_offset(page, 1, rk.nkv, head - rk.nq - rk.nkv, 0, hd, 0);
