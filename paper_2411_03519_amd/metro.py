@@ -264,7 +264,6 @@ class Model:
         check(lib.metro_decode_step(self._h, len(s), s.ctypes.data, _ptr(tokens_dev), _ptr(logits), _ptr(next_tok),
                                     _stream(stream)))
 
-
     # -- launch timing ------------------------------------------------------------
     def profile_start(self, kernel_class: str, phase: str = "any") -> None:
         check(lib.metro_profile_start(self._h, KERNEL_CLASS[kernel_class], PHASE[phase]))

@@ -409,6 +409,67 @@ def test_error_conventions(metro):
         assert nt.cpu().numpy()[1] == -1
 
 
+def test_empty_calls_boundaries_and_maximum_sizes(metro, tiny_case):
+    """Degenerate and limit cases against the oracle: a one-token prompt,
+    prompts ending one short of, on, and one past a page boundary (15, 16, 17,
+    32 tokens), all five prefilled in one call of exactly max_tokens tokens at
+    exactly max_batch items, then decoded until the longest sequence holds
+    exactly max_context tokens (every row crosses a page boundary on the way).
+    One more step with that sequence is refused with nothing changed, the
+    other four take it; empty calls and empty items are refused."""
+    _, _, cases = tiny_case
+    w = cases["random"][0]
+    V = synth.TINY["vocab"]
+    rng = np.random.default_rng(41)
+    lens = [1, 15, 16, 17, 32]
+    prompts = [rng.integers(0, V, n) for n in lens]
+    n_new = 9  # the longest row reaches 32 + 7 = max_context after 7 decode steps
+    ref = OracleModel(LlamaShape(**synth.TINY), w)
+    gens = [ref.generate(p, n_new) for p in prompts]
+    page_bytes = 2 * 2 * 64 * 16 * 2 * 2  # K+V, 2 kv heads, 16 slots, hd 64, bf16, 2 layers
+    with make_model(metro, synth.TINY, w, max_batch=5, max_tokens=sum(lens), max_context=39,
+                    kv_pool_bytes=16 * page_bytes) as m:
+        with pytest.raises(metro.MetroError) as e:
+            m.prefill_chunk([], [])
+        assert e.value.name == "METRO_E_INVAL"
+        with pytest.raises(metro.MetroError) as e:
+            m.decode_step([], torch.empty(0, dtype=torch.int32, device="cuda"))
+        assert e.value.name == "METRO_E_INVAL"
+        seqs = [m.seq_open() for _ in prompts]
+        with pytest.raises(metro.MetroError) as e:
+            m.prefill_chunk([seqs[0]], [[]])
+        assert e.value.name == "METRO_E_INVAL"
+        with pytest.raises(metro.MetroError) as e:
+            m.decode_step(seqs + [seqs[0]], torch.zeros(6, dtype=torch.int32, device="cuda"))
+        assert e.value.name == "METRO_E_CAPACITY"
+        assert all(m.seq_length(s) == 0 for s in seqs)
+
+        lg = torch.empty(5, V, device="cuda")
+        nt = torch.empty(5, dtype=torch.int32, device="cuda")
+        m.prefill_chunk(seqs, prompts, lg, nt)
+        rows, toks = [lg.cpu().numpy()], [nt.cpu().numpy()]
+        for k in range(1, 8):
+            m.decode_step(seqs, [int(g[0][k - 1]) for g in gens], lg, nt)
+            rows.append(lg.cpu().numpy())
+            toks.append(nt.cpu().numpy())
+        assert [m.seq_length(s) for s in seqs] == [n + 7 for n in lens]
+        assert m.seq_length(seqs[4]) == 39
+        free = m.info().free_pages
+        with pytest.raises(metro.MetroError) as e:
+            m.decode_step(seqs, [int(g[0][7]) for g in gens], lg, nt)
+        assert e.value.name == "METRO_E_CAPACITY"
+        assert [m.seq_length(s) for s in seqs] == [n + 7 for n in lens] and m.info().free_pages == free
+        m.decode_step(seqs[:4], [int(g[0][7]) for g in gens[:4]], lg[:4], nt[:4])
+        last, last_tok = lg[:4].cpu().numpy(), nt[:4].cpu().numpy()
+    got = np.stack(rows, axis=1)
+    want = np.stack([g[1][:8] for g in gens])
+    assert_logits_close(got, want, "edge lengths")
+    check_tokens(np.stack(toks, axis=1), want, "edge lengths")
+    want_last = np.stack([g[1][8] for g in gens[:4]])
+    assert_logits_close(last, want_last, "edge lengths, step past the full row")
+    check_tokens(last_tok, want_last, "edge lengths, step past the full row")
+
+
 def test_llama3_8b_widths_two_layers(metro):
     """Llama-3-8B layer widths (d 4096, 32/8 heads of 128, FFN 14336, vocab
     128256) at depth 2: two agents with 256- and 203-token prompts, prefilled in
