@@ -272,10 +272,15 @@ __global__ __launch_bounds__(256) void reduce_parts_kernel(const float* __restri
 // Operands reach LDS by direct loads (global_load_lds_dwordx4: each lane's 16
 // bytes land at LDS base + 16 * lane), through a ring of 4 stages of 32-wide
 // k; the loads of three stages are in flight while one is consumed, with no
-// staging registers.  In LDS both operands are kept as 16 x 32 tiles in lane
-// order (the packed weight layout; activations are gathered into the same
-// form, 64 contiguous bytes of each of 16 rows per wave load), so every MFMA
-// operand read by 16 lanes is 256 contiguous bytes, free of bank conflicts.
+// staging registers.  In LDS the weights keep their packed 16 x 32 tiles in
+// lane order, so every MFMA operand read by 16 lanes is 256 contiguous bytes,
+// free of bank conflicts.  Activations in 32-wide k stages are gathered into
+// the same form (64 contiguous bytes of each of 16 rows per wave load); in
+// 64-wide k stages one wave load takes 8 whole rows of the stage (8 x 128
+// bytes, whole cache lines) into a 1 KiB block whose 16-byte chunks are
+// XOR-swizzled by row (act_chunk_slot), which keeps the operand reads free of
+// bank conflicts: 8 consecutive rows of one k chunk fall in 8 distinct
+// 16-byte slots of a 128-byte bank period.
 // The stage consumed in step kt is refilled (with stage kt + 4) in step
 // kt + 1, after the barrier that every wave passes only once done reading it.
 // ---------------------------------------------------------------------------
@@ -317,6 +322,13 @@ using WideTile = TileShape<4, 2, 2, 2, 5>;
 __device__ __forceinline__ f32x16 mfma32(uint4 a, uint4 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
 }
+
+// Slot of 16-byte chunk c of tile row `row` within that row's 128 bytes of a
+// swizzled activation block (64-wide k stages); the map is its own inverse,
+// so it also gives the chunk held in slot c.  The 8 rows of a block put one
+// chunk into 8 distinct slots of a 128-byte bank period, and rows of the next
+// block into the other half of a 256-byte one.
+__device__ __forceinline__ int act_chunk_slot(int c, int row) { return c ^ (row & 7) ^ ((row >> 3) & 1); }
 
 // wait until at most PER * min(later, MAXC) direct loads of this wave are outstanding
 template <int PER, int MAXC>
@@ -418,8 +430,17 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
       dst_step[j] = KT * S::WT * 1024;
     } else {
       const int u = t - KT * S::WT, kk = u / S::XT, tx = u % S::XT;
-      const int row = min(m0 + 16 * tx + (lane & 15), M - 1);
-      src[j] = X + static_cast<size_t>(row) * ldx + k0 + 32 * kk + 8 * (lane >> 4);
+      if constexpr (KT == 2) {
+        // block u: rows 8u .. 8u+7 of the tile, all 64 k of the stage; lane l
+        // fills slot l % 8 of row 8u + l / 8
+        const int row = min(m0 + 8 * u + (lane >> 3), M - 1);
+        src[j] = X + static_cast<size_t>(row) * ldx + k0 + 8 * act_chunk_slot(lane & 7, 8 * u + (lane >> 3));
+        (void)kk;
+        (void)tx;
+      } else {
+        const int row = min(m0 + 16 * tx + (lane & 15), M - 1);
+        src[j] = X + static_cast<size_t>(row) * ldx + k0 + 32 * kk + 8 * (lane >> 4);
+      }
       dst[j] = lds_address(&xring[0][0]) + u * 1024;
       src_step[j] = 32 * KT;
       dst_step[j] = KT * S::XT * 1024;
@@ -442,17 +463,26 @@ __global__ __launch_bounds__(S::NTH) void gemm_tiled_kernel(const uint16_t* __re
   // operand fragments of the 16-wide k half ks (0 .. 2 KT - 1) of stage kt
   auto read_frags = [&](int kt, int ks, uint4 (&af)[TN], uint4 (&bf)[TM]) __attribute__((always_inline)) {
     const uint4* ws = wring[kt % NS] + (ks >> 1) * S::WT * 64;
-    const uint4* xs = xring[kt % NS] + (ks >> 1) * S::XT * 64;
     const int q = 16 * (2 * (ks & 1) + lh);  // chunk of the lane's 8 k values within a tile
 #pragma unroll
     for (int i = 0; i < TN; ++i) {
       const int row = wn * TN * 32 + i * 32 + lr;
       af[i] = ws[(row >> 4) * 64 + (row & 15) + q];
     }
+    if constexpr (KT == 2) {
+      const uint4* xs = xring[kt % NS];
 #pragma unroll
-    for (int j = 0; j < TM; ++j) {
-      const int row = wm * TM * 32 + j * 32 + lr;
-      bf[j] = xs[(row >> 4) * 64 + (row & 15) + q];
+      for (int j = 0; j < TM; ++j) {
+        const int row = wm * TM * 32 + j * 32 + lr;
+        bf[j] = xs[(row >> 3) * 64 + (row & 7) * 8 + act_chunk_slot(2 * ks + lh, row)];
+      }
+    } else {
+      const uint4* xs = xring[kt % NS] + (ks >> 1) * S::XT * 64;
+#pragma unroll
+      for (int j = 0; j < TM; ++j) {
+        const int row = wm * TM * 32 + j * 32 + lr;
+        bf[j] = xs[(row >> 4) * 64 + (row & 15) + q];
+      }
     }
   };
   auto mfmas = [&](const uint4 (&af)[TN], const uint4 (&bf)[TM]) __attribute__((always_inline)) {
