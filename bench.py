@@ -160,12 +160,41 @@ STEP_SOURCES = KERNEL_SOURCES + ["paper_2411_03519_amd/csrc/kernels/attention.hi
                                  "paper_2411_03519_amd/csrc/runtime.hip"]
 
 
+def code_only(text: str) -> str:
+    """C/C++/HIP source without its comments and with every run of white
+    space made one blank: what the compiler sees of it, so that an edit of a
+    comment does not mark a measurement of the code stale.  String and
+    character literals are kept as they are."""
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if c in "\"'":
+            j = i + 1
+            while j < n and text[j] != c:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        elif text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def source_hash(sources=None) -> str:
+    """sha256 over the code (code_only) of the listed sources, in order."""
     import hashlib
     h = hashlib.sha256()
     for rel in sources or KERNEL_SOURCES:
-        with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, rel), encoding="utf-8") as f:
+            h.update(code_only(f.read()).encode())
+        h.update(b"\0")
     return h.hexdigest()
 
 

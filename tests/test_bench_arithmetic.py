@@ -71,3 +71,22 @@ def test_decode_step_bytes_of_the_70b_batch():
     per_step = sum(bench.decode_step_bytes(S70, lens + k) for k in range(n_new - 1)) / (n_new - 1)
     # 139.0 GB of weights plus about 84 GB of KV for contexts averaging ~2000 tokens
     assert abs(per_step - 222.8e9) < 0.01 * 222.8e9
+
+
+def test_code_only_drops_comments_and_keeps_literals():
+    src = ('int a = 1;   // a note\n/* a block\n   comment */ const char* s = "x // y /* z */";\n'
+           "char c = '\"'; char d = '\\''; asm(\"s_nop 0\");\n")
+    assert bench.code_only(src) == ('int a = 1; const char* s = "x // y /* z */"; char c = \'"\'; '
+                                    "char d = '\\''; asm(\"s_nop 0\");")
+
+
+def test_source_hash_ignores_comment_edits(tmp_path, monkeypatch):
+    """The hash that marks a traffic measurement stale follows code changes
+    only: an edited comment keeps it, a changed expression does not."""
+    a, b, c = tmp_path / "a.hip", tmp_path / "b.hip", tmp_path / "c.hip"
+    a.write_text("// v1\nx = y + 1; /* note */\n")
+    b.write_text("// v2, reworded\nx = y + 1;   /* other note */\n")
+    c.write_text("// v1\nx = y + 2; /* note */\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.source_hash(["a.hip"]) == bench.source_hash(["b.hip"])
+    assert bench.source_hash(["a.hip"]) != bench.source_hash(["c.hip"])
