@@ -35,7 +35,9 @@ metro_status metro_op_pack_weight(const uint16_t* W_rowmajor, int32_t ld, int32_
 /* Projection GEMM of the Llama block (QKV, O, gate/up, down, LM head):
  *   acc[m, n] = sum_k X[m, k] * W[n, k]   (bf16 operands, fp32 accumulation)
  * X: bf16 [M, ldx] row-major, the first Kp columns used; W: bf16 [N, Kp] in
- * the layout metro_op_pack_weight writes; Kp % 128 == 0, N % 32 == 0.
+ * the layout metro_op_pack_weight writes; Kp % 128 == 0, N % 32 == 0,
+ * ldx % 8 == 0; X, W, workspace and out_f32 16-byte aligned, out_bf16 8-byte
+ * aligned (E_INVAL otherwise: the kernels move 16-byte pieces).
  * epilogue:
  *   0  out_f32[m*ldo + n]  = acc[m, n]
  *   1  out_f32[m*ldo + n] += acc[m, n]                       (residual add)

@@ -1016,6 +1016,12 @@ metro_status metro_op_gemm(const uint16_t* X, int32_t ldx, const uint16_t* W, in
   if (epilogue == metro::kEpiSwiGLU ? !out_bf16 : !out_f32) return fail(METRO_E_INVAL, "gemm: output is NULL");
   if ((epilogue == metro::kEpiSwiGLU ? ldo < N / 2 : ldo < N) || ldo % 4)
     return fail(METRO_E_INVAL, "gemm: bad ldo");
+  // the kernels move X and W in 16-byte pieces and store 4 outputs at a time
+  auto misaligned = [](const void* p, uintptr_t a) { return p && reinterpret_cast<uintptr_t>(p) % a != 0; };
+  if (ldx % 8 || misaligned(X, 16) || misaligned(W, 16) || misaligned(out_f32, 16) || misaligned(out_bf16, 8) ||
+      misaligned(workspace, 16))
+    return fail(METRO_E_INVAL, "gemm: X, W and workspace must be 16-byte aligned, ldx a multiple of 8, out_f32 "
+                               "16-byte and out_bf16 8-byte aligned");
   int parts = 0;
   hipError_t e = metro::launch_gemm(X, ldx, W, Kp, M, N, epilogue, out_f32, out_bf16, ldo, workspace,
                                     8LL * M * N, &parts,

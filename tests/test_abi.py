@@ -100,3 +100,20 @@ def test_gemm_plan_rejects_bad_shapes(repo_root):
     for args in ((0, 4096, 4096, 0), (64, 4016, 4096, 0), (64, 4096, 4000, 0), (64, 4096, 4096, 7)):
         with pytest.raises(metro.MetroError):
             metro.op_gemm_plan(*args)
+
+
+def test_gemm_rejects_misaligned_operands_before_any_launch(repo_root):
+    """Alignment and stride are checked on the host (E_INVAL) before any device
+    work, so this runs without a GPU: the pointers are never dereferenced."""
+    if not os.path.exists(os.path.join(repo_root, "paper_2411_03519_amd", "libmetro.so")):
+        pytest.skip("libmetro.so not built")
+    from paper_2411_03519_amd import metro
+    lib = metro.lib
+    P = ctypes.c_void_p
+    base = 1 << 20  # stand-in device addresses, 16-byte aligned
+    cases = [(base + 2, 4096, base, base), (base, 4100, base, base), (base, 4096, base + 8, base),
+             (base, 4096, base, base + 4)]
+    for X, ldx, W, out in cases:
+        st = lib.metro_op_gemm(P(X), ldx, P(W), 4096, 64, 4096, 0, P(out), None, 4096, None, None)
+        assert st == -1, (X, ldx, W, out)
+        assert b"aligned" in lib.metro_last_error()
