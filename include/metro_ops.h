@@ -69,7 +69,8 @@ metro_status metro_op_gemm_plan(int32_t M, int32_t N, int32_t Kp, int32_t epilog
                                 int32_t* kind, int32_t* k_slices, int32_t* tail_split);
 
 /* RMSNorm (Zhang & Sennrich 2019): h[r, :] = bf16(x[r, :] / sqrt(mean(x[r, :]^2)
- * + eps) * g), x fp32 [rows, d], g bf16 [d], h bf16 [rows, d], d % 4 == 0, d <= 8192. */
+ * + eps) * g), x fp32 [rows, d], g bf16 [d], h bf16 [rows, d], d % 4 == 0, d <= 8192;
+ * x 16-byte aligned, g and h 8-byte aligned (E_INVAL otherwise). */
 metro_status metro_op_rmsnorm(float* x, const uint16_t* g, float eps, uint16_t* h, int32_t rows, int32_t d,
                               void* stream);
 
@@ -95,11 +96,11 @@ metro_status metro_op_argmax(const float* logits, int32_t rows, int32_t vocab, i
  * with fp32 scores, softmax and accumulation (the weights enter the bf16
  * matrix cores as a bf16 pair hi + lo).  Rows of more than 128 pages are cut
  * into 128-page work items whose states are merged in order, as in the model.
- *   q            device bf16 [rows, nq, hd]
- *   kv           device bf16, n_pages pages in the layout above
+ *   q            device bf16 [rows, nq, hd], 16-byte aligned
+ *   kv           device bf16, n_pages pages in the layout above, 16-byte aligned
  *   ctx          host int32 [rows], >= 1
  *   block_tables host int32, row after row: ceil(ctx[i] / 16) page ids each
- *   out          device bf16 [rows, nq * hd]
+ *   out          device bf16 [rows, nq * hd], 8-byte aligned
  * hd is 64 or 128; nq / nkv is 1, 2, 4 or 8.  Allocates and frees device
  * memory for its descriptors and split states and returns after the kernels
  * have finished on `stream` (a test entry point, not for serving loops).

@@ -1007,6 +1007,9 @@ metro_status metro_op_pack_weight(const uint16_t* W_rowmajor, int32_t ld, int32_
   return METRO_OK;
 }
 
+// whether p (if given) is not a multiple of a bytes
+static bool misaligned(const void* p, uintptr_t a) { return p && reinterpret_cast<uintptr_t>(p) % a != 0; }
+
 metro_status metro_op_gemm(const uint16_t* X, int32_t ldx, const uint16_t* W, int32_t Kp, int32_t M, int32_t N,
                            int32_t epilogue, float* out_f32, uint16_t* out_bf16, int32_t ldo, float* workspace,
                            void* stream) {
@@ -1017,7 +1020,6 @@ metro_status metro_op_gemm(const uint16_t* X, int32_t ldx, const uint16_t* W, in
   if ((epilogue == metro::kEpiSwiGLU ? ldo < N / 2 : ldo < N) || ldo % 4)
     return fail(METRO_E_INVAL, "gemm: bad ldo");
   // the kernels move X and W in 16-byte pieces and store 4 outputs at a time
-  auto misaligned = [](const void* p, uintptr_t a) { return p && reinterpret_cast<uintptr_t>(p) % a != 0; };
   if (ldx % 8 || misaligned(X, 16) || misaligned(W, 16) || misaligned(out_f32, 16) || misaligned(out_bf16, 8) ||
       misaligned(workspace, 16))
     return fail(METRO_E_INVAL, "gemm: X, W and workspace must be 16-byte aligned, ldx a multiple of 8, out_f32 "
@@ -1050,6 +1052,8 @@ metro_status metro_op_rmsnorm(float* x, const uint16_t* g, float eps, uint16_t* 
   g_err.clear();
   if (!x || !g || !h || rows < 0 || d <= 0 || d % 4 || d > metro::kRmsNormMaxDim)
     return fail(METRO_E_INVAL, "rmsnorm: bad arguments");
+  if (misaligned(x, 16) || misaligned(g, 8) || misaligned(h, 8))
+    return fail(METRO_E_INVAL, "rmsnorm: x must be 16-byte aligned, g and h 8-byte aligned");
   hipError_t e = metro::launch_rmsnorm(x, d, g, eps, h, d, rows, d, nullptr, 0, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(nullptr, e, "launch_rmsnorm");
   return METRO_OK;
@@ -1064,8 +1068,11 @@ struct OpBuffer {
   }
 };
 
-metro_status check_attn_shape(int32_t nq, int32_t nkv, int32_t hd, int32_t n_pages) {
+metro_status check_attn_shape(int32_t nq, int32_t nkv, int32_t hd, int32_t n_pages, const void* q, const void* kv,
+                              const void* out) {
   if (hd != 64 && hd != 128) return fail(METRO_E_INVAL, "attention: head_dim must be 64 or 128");
+  if (misaligned(q, 16) || misaligned(kv, 16) || misaligned(out, 8))
+    return fail(METRO_E_INVAL, "attention: q and kv must be 16-byte aligned, out 8-byte aligned");
   if (nkv <= 0 || nq <= 0 || nq % nkv) return fail(METRO_E_INVAL, "attention: n_heads %% n_kv_heads != 0");
   const int g = nq / nkv;
   if (g != 1 && g != 2 && g != 4 && g != 8) return fail(METRO_E_INVAL, "attention: group size must be 1, 2, 4 or 8");
@@ -1077,7 +1084,7 @@ metro_status metro_op_attn_decode(const uint16_t* q, const uint16_t* kv, int32_t
                                   int32_t hd, int32_t rows, const int32_t* ctx, const int32_t* block_tables,
                                   uint16_t* out, void* stream) {
   g_err.clear();
-  metro_status st = check_attn_shape(nq, nkv, hd, n_pages);
+  metro_status st = check_attn_shape(nq, nkv, hd, n_pages, q, kv, out);
   if (st != METRO_OK) return st;
   if (rows < 0 || (rows > 0 && (!q || !kv || !ctx || !block_tables || !out)))
     return fail(METRO_E_INVAL, "attn_decode: NULL argument or rows < 0");
@@ -1150,7 +1157,7 @@ metro_status metro_op_attn_decode_noalloc(const uint16_t* q, const uint16_t* kv,
                                           int32_t nkv, int32_t hd, int32_t rows, const int32_t* ctx,
                                           const int32_t* block_tables, uint16_t* out, void* stream) {
   g_err.clear();
-  metro_status st = check_attn_shape(nq, nkv, hd, n_pages);
+  metro_status st = check_attn_shape(nq, nkv, hd, n_pages, q, kv, out);
   if (st != METRO_OK) return st;
   if (rows < 0 || (rows > 0 && (!q || !kv || !ctx || !block_tables || !out)))
     return fail(METRO_E_INVAL, "attn_decode_noalloc: NULL argument or rows < 0");
@@ -1224,7 +1231,7 @@ metro_status metro_op_attn_prefill(const uint16_t* q, const uint16_t* kv, int32_
                                    int32_t hd, int32_t n_items, const int32_t* cu_q, const int32_t* ctx_before,
                                    const int32_t* block_tables, uint16_t* out, void* stream) {
   g_err.clear();
-  metro_status st = check_attn_shape(nq, nkv, hd, n_pages);
+  metro_status st = check_attn_shape(nq, nkv, hd, n_pages, q, kv, out);
   if (st != METRO_OK) return st;
   if (n_items < 0 || (n_items > 0 && (!q || !kv || !cu_q || !ctx_before || !block_tables || !out)))
     return fail(METRO_E_INVAL, "attn_prefill: NULL argument or n_items < 0");

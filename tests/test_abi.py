@@ -117,3 +117,19 @@ def test_gemm_rejects_misaligned_operands_before_any_launch(repo_root):
         st = lib.metro_op_gemm(P(X), ldx, P(W), 4096, 64, 4096, 0, P(out), None, 4096, None, None)
         assert st == -1, (X, ldx, W, out)
         assert b"aligned" in lib.metro_last_error()
+
+
+def test_rmsnorm_and_attention_reject_misaligned_buffers(repo_root):
+    if not os.path.exists(os.path.join(repo_root, "paper_2411_03519_amd", "libmetro.so")):
+        pytest.skip("libmetro.so not built")
+    from paper_2411_03519_amd import metro
+    lib = metro.lib
+    P = ctypes.c_void_p
+    base = 1 << 20
+    assert lib.metro_op_rmsnorm(P(base + 8), P(base), ctypes.c_float(1e-5), P(base), 4, 256, None) == -1
+    assert b"aligned" in lib.metro_last_error()
+    ctx = (ctypes.c_int32 * 1)(16)
+    bt = (ctypes.c_int32 * 1)(0)
+    for q, kv, out in ((base + 8, base, base), (base, base + 4, base), (base, base, base + 2)):
+        assert lib.metro_op_attn_decode(P(q), P(kv), 1, 4, 2, 64, 1, ctx, bt, P(out), None) == -1
+        assert b"aligned" in lib.metro_last_error()
